@@ -1,0 +1,108 @@
+"""EVA oracle: fp64 CPU reference (test infrastructure only).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  It wraps oracle/eva_oracle.c through ctypes and shares no code
+with the HIP library.  Every array handed in is converted to contiguous
+float64 numpy first, so callers may pass torch tensors (any dtype, any device
+already copied to the host) or numpy arrays.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_lp = ctypes.POINTER(ctypes.c_long)
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_build.LIB):
+        _build.build()
+    lib = ctypes.CDLL(_build.LIB)
+    lib.eva_ref_visible_summaries.restype = ctypes.c_long
+    lib.eva_ref_visible_summaries.argtypes = [ctypes.c_long, ctypes.c_long, ctypes.c_long]
+    lib.eva_ref_summaries.restype = None
+    lib.eva_ref_summaries.argtypes = [_dp, _dp, ctypes.c_long, ctypes.c_int, ctypes.c_long, _dp, _dp]
+    lib.eva_ref_attend_row.restype = None
+    lib.eva_ref_attend_row.argtypes = [_dp, _dp, _dp, _dp, _dp, ctypes.c_long, ctypes.c_int,
+                                       ctypes.c_long, ctypes.c_long, _dp]
+    lib.eva_ref_attend_rows.restype = None
+    lib.eva_ref_attend_rows.argtypes = [_dp, _lp, ctypes.c_long, _dp, _dp, _dp, _dp, ctypes.c_int,
+                                        ctypes.c_long, ctypes.c_long, _dp]
+    lib.eva_ref_prefill.restype = None
+    lib.eva_ref_prefill.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_long, ctypes.c_int, ctypes.c_long, ctypes.c_long, _dp, _dp]
+    lib.eva_ref_num_threads.restype = ctypes.c_int
+    lib.eva_ref_num_threads.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _f64(x):
+    if hasattr(x, "detach"):  # torch tensor
+        x = x.detach().to("cpu").double().numpy()
+    return np.ascontiguousarray(x, dtype=np.float64)
+
+
+def _ptr(a):
+    return a.ctypes.data_as(_dp)
+
+
+def num_threads() -> int:
+    return int(_load().eva_ref_num_threads())
+
+
+def visible_summaries(n: int, W: int, C: int) -> int:
+    """s(n): number of chunk summaries the query at position n attends."""
+    return int(_load().eva_ref_visible_summaries(n, W, C))
+
+
+def summaries(K, V, C: int):
+    """Chunk summaries of one sequence. K, V: [L, d] -> (Ksum, Vsum): [L // C, d]."""
+    K, V = _f64(K), _f64(V)
+    L, d = K.shape
+    n_chunks = L // C
+    Ks = np.zeros((n_chunks, d))
+    Vs = np.zeros((n_chunks, d))
+    _load().eva_ref_summaries(_ptr(K), _ptr(V), L, d, C, _ptr(Ks), _ptr(Vs))
+    return Ks, Vs
+
+
+def attend_rows(Qrows, rows, K, V, Ksum, Vsum, W: int, C: int):
+    """Rows `rows` (positions) of one sequence; Qrows[r] is the query at rows[r]."""
+    Qrows, K, V = _f64(Qrows), _f64(K), _f64(V)
+    Ksum, Vsum = _f64(Ksum), _f64(Vsum)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    d = K.shape[1]
+    assert Qrows.shape == (rows.shape[0], d)
+    if Ksum.shape[0] == 0:  # keep a valid pointer for empty summary sets
+        Ksum = np.zeros((1, d))
+        Vsum = np.zeros((1, d))
+    out = np.zeros((rows.shape[0], d))
+    _load().eva_ref_attend_rows(_ptr(Qrows), rows.ctypes.data_as(_lp), rows.shape[0], _ptr(K), _ptr(V),
+                                _ptr(Ksum), _ptr(Vsum), d, W, C, _ptr(out))
+    return out
+
+
+def prefill(Q, K, V, W: int, C: int, return_summaries: bool = False):
+    """Whole EVA prefill. Q: [B, H, L, d]; K, V: [B, Hkv, L, d] -> O: [B, H, L, d] (fp64)."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    assert K.shape == (B, Hkv, L, d) and V.shape == K.shape and H % Hkv == 0
+    n_chunks = L // C
+    O = np.zeros_like(Q)
+    Ks = np.zeros((B, Hkv, max(n_chunks, 1), d))
+    Vs = np.zeros((B, Hkv, max(n_chunks, 1), d))
+    _load().eva_ref_prefill(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C,
+                            _ptr(Ks), _ptr(Vs))
+    if return_summaries:
+        return O, Ks[:, :, :n_chunks], Vs[:, :, :n_chunks]
+    return O

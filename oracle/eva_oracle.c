@@ -1,0 +1,184 @@
+/*
+ * EVA attention oracle: plain, slow, obviously correct CPU reference in fp64.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
+ * load this file.  Only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header, table or helper with the
+ * HIP library.
+ *
+ * What it computes (FlashEVA, section "FlashEVA", the reformulation of EVA as
+ * softmax attention over an augmented key/value set; with the local set E and
+ * the disjoint chunk partition P_c of section "EVA Attention", eq. (eva) and
+ * eq. (eva_normalization)):
+ *
+ *   Summaries, one per complete chunk c of C tokens, positions [cC, cC+C):
+ *     khat_c = (1/C) * sum_j k_j                     (mean key)
+ *     a_j    = khat_c . k_j / sqrt(d)
+ *     vhat_c = sum_j softmax_j(a) * v_j             (query-independent value,
+ *                                                    the S=1 property)
+ *   Attention row n (causal):
+ *     window   E(n) = [max(0, n-W+1), n]              (W tokens, self included)
+ *     summaries c < s(n), s(n) = floor(max(0, n-W+1) / C)
+ *                                   (only chunks lying fully before the window)
+ *     logits   q_n.k_m / sqrt(d)          for m in E(n)
+ *              q_n.khat_c / sqrt(d) + ln C for c < s(n)
+ *     o_n = sum_i exp(l_i - max l) val_i / sum_i exp(l_i - max l)
+ *
+ * Everything is the plain definition: no tiling, no online softmax, no
+ * reordering.  Inputs are fp64 copies of whatever the caller rounded them to.
+ * The paper is silent on several details (window extent, chunk alignment,
+ * tokens between the last summarized chunk and the window, the summary key
+ * form, the logit offset, 1/sqrt(d) scaling, GQA head mapping); the readings
+ * taken here are the ones listed in the design notes and are pinned by the
+ * CPU tests (closed forms, reductions to exact softmax attention,
+ * invariants).
+ *
+ * Layouts: row-major, contiguous.
+ *   single sequence: K, V [L][d]; Ksum, Vsum [floor(L/C)][d]
+ *   batched:         Q, O [B][H][L][d]; K, V [B][Hkv][L][d]
+ *   GQA: query head h reads key/value head h / (H/Hkv).
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Number of chunk summaries visible to the query at position n. */
+long eva_ref_visible_summaries(long n, long W, long C)
+{
+    long window_start = n - W + 1;
+    if (window_start <= 0) return 0;
+    return window_start / C;
+}
+
+/* Summaries of one sequence: for each complete chunk, the mean key and the
+ * softmax(mean-key . key / sqrt(d))-weighted value. */
+void eva_ref_summaries(const double* K, const double* V, long L, int d, long C,
+                       double* Ksum, double* Vsum)
+{
+    long n_chunks = L / C;
+    double inv_sqrt_d = 1.0 / sqrt((double)d);
+    double* a = (double*)malloc((size_t)C * sizeof(double));
+    for (long c = 0; c < n_chunks; ++c) {
+        const double* Kc = K + (size_t)c * C * d;
+        const double* Vc = V + (size_t)c * C * d;
+        double* kh = Ksum + (size_t)c * d;
+        double* vh = Vsum + (size_t)c * d;
+
+        /* mean key */
+        for (int e = 0; e < d; ++e) {
+            double s = 0.0;
+            for (long j = 0; j < C; ++j) s += Kc[(size_t)j * d + e];
+            kh[e] = s / (double)C;
+        }
+        /* scores of each chunk key against the mean key */
+        double amax = -INFINITY;
+        for (long j = 0; j < C; ++j) {
+            double s = 0.0;
+            for (int e = 0; e < d; ++e) s += kh[e] * Kc[(size_t)j * d + e];
+            a[j] = s * inv_sqrt_d;
+            if (a[j] > amax) amax = a[j];
+        }
+        /* softmax-weighted value */
+        double den = 0.0;
+        for (long j = 0; j < C; ++j) den += exp(a[j] - amax);
+        for (int e = 0; e < d; ++e) {
+            double num = 0.0;
+            for (long j = 0; j < C; ++j) num += exp(a[j] - amax) * Vc[(size_t)j * d + e];
+            vh[e] = num / den;
+        }
+    }
+    free(a);
+}
+
+/* One attention row: query q at position n against the exact keys of its
+ * window and the visible chunk summaries. */
+void eva_ref_attend_row(const double* q, const double* K, const double* V,
+                        const double* Ksum, const double* Vsum,
+                        long n, int d, long W, long C, double* o)
+{
+    double inv_sqrt_d = 1.0 / sqrt((double)d);
+    long lo = n - W + 1;
+    if (lo < 0) lo = 0;
+    long n_win = n - lo + 1;
+    long n_sum = eva_ref_visible_summaries(n, W, C);
+    long count = n_win + n_sum;
+
+    double* logit = (double*)malloc((size_t)count * sizeof(double));
+    const double** val = (const double**)malloc((size_t)count * sizeof(double*));
+    long i = 0;
+    for (long m = lo; m <= n; ++m, ++i) {
+        double s = 0.0;
+        for (int e = 0; e < d; ++e) s += q[e] * K[(size_t)m * d + e];
+        logit[i] = s * inv_sqrt_d;
+        val[i] = V + (size_t)m * d;
+    }
+    for (long c = 0; c < n_sum; ++c, ++i) {
+        double s = 0.0;
+        for (int e = 0; e < d; ++e) s += q[e] * Ksum[(size_t)c * d + e];
+        logit[i] = s * inv_sqrt_d + log((double)C);
+        val[i] = Vsum + (size_t)c * d;
+    }
+
+    double lmax = -INFINITY;
+    for (i = 0; i < count; ++i)
+        if (logit[i] > lmax) lmax = logit[i];
+    double den = 0.0;
+    for (i = 0; i < count; ++i) den += exp(logit[i] - lmax);
+    for (int e = 0; e < d; ++e) {
+        double num = 0.0;
+        for (i = 0; i < count; ++i) num += exp(logit[i] - lmax) * val[i][e];
+        o[e] = num / den;
+    }
+    free(logit);
+    free(val);
+}
+
+/* Selected rows of one sequence: rows[r] is a position, Qrows[r] its query. */
+void eva_ref_attend_rows(const double* Qrows, const long* rows, long n_rows,
+                         const double* K, const double* V,
+                         const double* Ksum, const double* Vsum,
+                         int d, long W, long C, double* Orows)
+{
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (long r = 0; r < n_rows; ++r)
+        eva_ref_attend_row(Qrows + (size_t)r * d, K, V, Ksum, Vsum, rows[r], d, W, C,
+                           Orows + (size_t)r * d);
+}
+
+/* Whole prefill: summaries of every (b, kv head), then every row of every
+ * query head.  Ksum/Vsum receive [B][Hkv][floor(L/C)][d]. */
+void eva_ref_prefill(const double* Q, const double* K, const double* V, double* O,
+                     int B, int H, int Hkv, long L, int d, long W, long C,
+                     double* Ksum, double* Vsum)
+{
+    int G = H / Hkv;
+    long n_chunks = L / C;
+    size_t seq = (size_t)L * d;
+    size_t sseq = (size_t)n_chunks * d;
+
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (long bg = 0; bg < (long)B * Hkv; ++bg)
+        eva_ref_summaries(K + bg * seq, V + bg * seq, L, d, C, Ksum + bg * sseq, Vsum + bg * sseq);
+
+    #pragma omp parallel for collapse(2) schedule(dynamic, 16)
+    for (long bh = 0; bh < (long)B * H; ++bh) {
+        for (long n = 0; n < L; ++n) {
+            long b = bh / H, h = bh % H;
+            long bg = b * Hkv + h / G;
+            eva_ref_attend_row(Q + bh * seq + (size_t)n * d, K + bg * seq, V + bg * seq,
+                               Ksum + bg * sseq, Vsum + bg * sseq, n, d, W, C,
+                               O + bh * seq + (size_t)n * d);
+        }
+    }
+}
+
+/* Threads the OpenMP runtime will use (1 when built without OpenMP). */
+int eva_ref_num_threads(void)
+{
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,110 @@
+"""Seeded synthetic inputs shared by the tests, the smoke check and the benchmark.
+
+This module draws random numbers and names workload shapes; it holds none of
+the attention arithmetic.  Every draw uses a torch CPU generator seeded by the
+caller: Q first, then K, then V, as float32 N(0, 1), then cast to the requested
+dtype with round-to-nearest-even (torch's cast).  Both the HIP path and the
+oracle read the same rounded host tensors.
+"""
+from dataclasses import dataclass
+
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    L: int
+    d: int
+    W: int
+    C: int
+    dtype: torch.dtype
+    seed: int
+
+
+# Workloads shaped like the LLM attention layers the method targets (head dim
+# 128, 32 query heads, grouped-query attention, contexts of 4k to 32k tokens).
+TINY_F32 = Workload("tiny-f32 B1 H2 L256 d64 W32 C16", 1, 2, 2, 256, 64, 32, 16, torch.float32, 1)
+LLM_BF16 = Workload("llm-bf16 B8 H32 L4096 d128 W256 C64", 8, 32, 32, 4096, 128, 256, 64, torch.bfloat16, 2)
+GQA_BF16 = Workload("gqa-bf16 B4 H32/8 L8192 d128 W512 C128", 4, 32, 8, 8192, 128, 512, 128, torch.bfloat16, 3)
+LONG_BF16 = Workload("long-bf16 B1 H32/8 L32768 d128 W1024 C256", 1, 32, 8, 32768, 128, 1024, 256,
+                     torch.bfloat16, 5)
+
+
+@dataclass(frozen=True)
+class DecodeWorkload:
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    d: int
+    W: int
+    C: int
+    context: int  # tokens already held by the cache before the decoded token
+    dtype: torch.dtype
+    seed: int
+
+
+# 64 sequences, 8192 tokens of context held as a 512-token exact window plus
+# 60 chunk summaries of 128 tokens each.
+DECODE_BF16 = DecodeWorkload("decode-bf16 B64 H32/8 d128 ctx8192 W512 C128", 64, 32, 8, 128, 512, 128, 8192,
+                             torch.bfloat16, 4)
+
+
+def normal(shape, seed: int, dtype=torch.float32, generator=None) -> torch.Tensor:
+    g = generator if generator is not None else torch.Generator().manual_seed(seed)
+    return torch.randn(*shape, generator=g, dtype=torch.float32).to(dtype)
+
+
+def qkv(B, H, Hkv, L, d, dtype=torch.bfloat16, seed=0):
+    """Q [B,H,L,d], K, V [B,Hkv,L,d], i.i.d. N(0,1), drawn in that order."""
+    g = torch.Generator().manual_seed(seed)
+    q = normal((B, H, L, d), seed, dtype, g)
+    k = normal((B, Hkv, L, d), seed, dtype, g)
+    v = normal((B, Hkv, L, d), seed, dtype, g)
+    return q, k, v
+
+
+def workload_qkv(w: Workload):
+    return qkv(w.B, w.H, w.Hkv, w.L, w.d, w.dtype, w.seed)
+
+
+def needle_qkv(B, H, Hkv, L, d, dtype=torch.bfloat16, seed=0, magnitude=100.0):
+    """Mask probe: Q = K = 0 and V zero except one token per feature.
+
+    Feature e of V is `magnitude` at one position m_e (spread over the whole
+    sequence, seeded) and 0 elsewhere, so output feature e of row n is
+    magnitude times the weight row n gives token m_e: a token wrongly included
+    in or excluded from a row moves that feature by magnitude / (tokens
+    attended), far above bf16 rounding.
+    """
+    g = torch.Generator().manual_seed(seed)
+    q = torch.zeros(B, H, L, d, dtype=dtype)
+    k = torch.zeros(B, Hkv, L, d, dtype=dtype)
+    v = torch.zeros(B, Hkv, L, d, dtype=torch.float32)
+    pos = torch.randint(0, L, (B, Hkv, d), generator=g)
+    v.scatter_(2, pos.unsqueeze(2), magnitude)
+    return q, k, v.to(dtype)
+
+
+def spike_qkv(B, H, Hkv, L, d, dtype=torch.bfloat16, seed=0, alpha=3.0):
+    """Mask probe through the logit path: N(0,1) Q, K, V plus, per (b, kv head),
+    a set of positions whose key is alpha * u and every query gets + alpha * u
+    (u a fixed random unit direction scaled to norm sqrt(d)), so those keys
+    dominate any row that attends them exactly."""
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(B, H, L, d, generator=g)
+    k = torch.randn(B, Hkv, L, d, generator=g)
+    v = torch.randn(B, Hkv, L, d, generator=g)
+    u = torch.randn(d, generator=g)
+    u = u / u.norm() * (d ** 0.5)
+    n_spikes = max(1, L // 97)
+    pos = torch.randint(0, L, (B, Hkv, n_spikes), generator=g)
+    for b in range(B):
+        for hk in range(Hkv):
+            k[b, hk, pos[b, hk]] = alpha * u
+    q = q * 0.25 + alpha * u
+    return q.to(dtype), k.to(dtype), v.to(dtype)

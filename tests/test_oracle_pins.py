@@ -1,0 +1,293 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests re-types the oracle's formula: each checks it against a
+library routine it must reduce to, a closed form worked out for a structured
+input, a hand-expanded fixture, or an invariant of softmax attention.  A
+plausible slip in the oracle (window off by one, summary logit without ln C or
+with log2, sum instead of mean for the summary key, missing 1/sqrt(d), the gap
+tokens counted, a transposed head mapping) fails at least one of them.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rand(shape, seed):
+    return np.random.default_rng(seed).standard_normal(shape)
+
+
+def sdpa(q, k, v, mask=None, causal=False):
+    """torch's scaled_dot_product_attention in fp64 on the CPU."""
+    q, k, v = (torch.from_numpy(np.asarray(x, dtype=np.float64)) for x in (q, k, v))
+    out = torch.nn.functional.scaled_dot_product_attention(
+        q, k, v, attn_mask=None if mask is None else torch.from_numpy(mask), is_causal=causal)
+    return out.numpy()
+
+
+def expand_kv(k, G):
+    return np.repeat(k, G, axis=1)
+
+
+# ---------------------------------------------------------------------------
+# Reductions to exact softmax attention (eq. softmax_attn, causal case)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("W", [1, 2, 5, 17])
+def test_chunk_of_one_is_exact_causal_attention(W):
+    # C = 1: every summary is the token itself (mean of one key, softmax over
+    # one value, ln 1 = 0), so EVA is exact causal softmax attention.
+    B, H, Hkv, L, d = 2, 4, 2, 37, 8
+    q, k, v = rand((B, H, L, d), 1), rand((B, Hkv, L, d), 2), rand((B, Hkv, L, d), 3)
+    o = oracle.prefill(q, k, v, W=W, C=1)
+    ref = sdpa(q, expand_kv(k, H // Hkv), expand_kv(v, H // Hkv), causal=True)
+    np.testing.assert_allclose(o, ref, rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("C", [1, 3, 8, 64])
+def test_window_covering_sequence_is_exact_causal_attention(C):
+    B, H, Hkv, L, d = 1, 3, 1, 29, 16
+    q, k, v = rand((B, H, L, d), 4), rand((B, Hkv, L, d), 5), rand((B, Hkv, L, d), 6)
+    o = oracle.prefill(q, k, v, W=L, C=C)
+    ref = sdpa(q, expand_kv(k, H), expand_kv(v, H), causal=True)
+    np.testing.assert_allclose(o, ref, rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("W", [1, 4, 9])
+def test_no_complete_chunk_is_sliding_window_attention(W):
+    # C > L: no summaries at all, only the W-token sliding window (self included).
+    B, H, L, d = 1, 2, 23, 4
+    q, k, v = rand((B, H, L, d), 7), rand((B, H, L, d), 8), rand((B, H, L, d), 9)
+    o = oracle.prefill(q, k, v, W=W, C=L + 1)
+    n = np.arange(L)[:, None]
+    m = np.arange(L)[None, :]
+    mask = (m <= n) & (m > n - W)
+    ref = sdpa(q, k, v, mask=mask)
+    np.testing.assert_allclose(o, ref, rtol=1e-11, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Closed forms
+# ---------------------------------------------------------------------------
+
+def attended_token_sets(L, W, C):
+    """For each row, (window positions, positions inside summarized chunks)."""
+    out = []
+    for n in range(L):
+        start = n - W + 1
+        win = list(range(max(0, start), n + 1))
+        s = max(0, start) // C if start > 0 else 0
+        summarized = list(range(0, s * C))
+        out.append((win, summarized))
+    return out
+
+
+@pytest.mark.parametrize("L,W,C", [(40, 7, 4), (33, 5, 3), (64, 16, 8), (19, 1, 2)])
+def test_equal_keys_gives_uniform_mean_over_attended_tokens(L, W, C):
+    # All keys equal to u: each summary softmax is uniform so vhat is the chunk
+    # mean; the summary key is u (mean, not sum), its logit is q.u/sqrt(d) + ln C,
+    # exactly the window logit plus ln C.  Every attended token thus carries
+    # the same weight: o_n is the plain mean of v over window + summarized chunks.
+    d = 6
+    u = rand((d,), 11)
+    q = rand((1, 1, L, d), 12) * 2.0
+    k = np.broadcast_to(u, (1, 1, L, d)).copy()
+    v = rand((1, 1, L, d), 13)
+    o = oracle.prefill(q, k, v, W=W, C=C)[0, 0]
+    for n, (win, summ) in enumerate(attended_token_sets(L, W, C)):
+        toks = win + summ
+        np.testing.assert_allclose(o[n], v[0, 0, toks].mean(axis=0), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("L,W,C", [(50, 6, 5), (41, 10, 4)])
+def test_zero_query_chunk_constant_values(L, W, C):
+    # Q = 0, random K, V constant inside each chunk (value c_j for chunk j):
+    # every window logit is 0, every summary logit is ln C, and vhat_j = c_j
+    # whatever K is.  So o_n = (sum_window v + C * sum_{j<s(n)} c_j) / (w + C s).
+    d = 3
+    n_chunks = -(-L // C)
+    cvals = rand((n_chunks, d), 21)
+    v = np.repeat(cvals, C, axis=0)[:L][None, None]
+    k = rand((1, 1, L, d), 22) * 3.0
+    q = np.zeros((1, 1, L, d))
+    o = oracle.prefill(q, k, v, W=W, C=C)[0, 0]
+    for n, (win, summ) in enumerate(attended_token_sets(L, W, C)):
+        s = len(summ) // C
+        num = v[0, 0, win].sum(axis=0) + C * cvals[:s].sum(axis=0)
+        np.testing.assert_allclose(o[n], num / (len(win) + C * s), rtol=1e-12, atol=1e-12)
+
+
+def test_summary_with_one_spiked_key_closed_form():
+    # Chunk of C = 4 keys in d = 4: k_0 = (a,0,0,0), others 0.  The mean key is
+    # (a/4,0,0,0); scores are a^2/(4*sqrt(4)) = a^2/8 for j = 0 and 0 otherwise.
+    a = 3.0
+    C, d = 4, 4
+    K = np.zeros((C, d))
+    K[0, 0] = a
+    V = rand((C, d), 31)
+    Ks, Vs = oracle.summaries(K, V, C)
+    np.testing.assert_allclose(Ks[0], [a / 4, 0, 0, 0], rtol=0, atol=0)
+    w0 = math.exp(a * a / 8.0)
+    expect = (w0 * V[0] + V[1] + V[2] + V[3]) / (w0 + 3.0)
+    np.testing.assert_allclose(Vs[0], expect, rtol=1e-13)
+
+
+def test_summary_two_level_keys_closed_form():
+    # Chunk of C = 3 in d = 2 with keys (1,0), (1,0), (-1,2): mean (1/3, 2/3).
+    # Scores /sqrt(2): (1/3)/sqrt2, (1/3)/sqrt2, (-1/3 + 4/3)/sqrt2 = 1/sqrt2.
+    K = np.array([[1.0, 0.0], [1.0, 0.0], [-1.0, 2.0]])
+    V = np.array([[1.0, 0.0], [0.0, 1.0], [2.0, 2.0]])
+    Ks, Vs = oracle.summaries(K, V, 3)
+    np.testing.assert_allclose(Ks[0], [1 / 3, 2 / 3], rtol=1e-15)
+    e1 = math.exp((1 / 3) / math.sqrt(2))
+    e3 = math.exp(1 / math.sqrt(2))
+    expect = (e1 * V[0] + e1 * V[1] + e3 * V[2]) / (2 * e1 + e3)
+    np.testing.assert_allclose(Vs[0], expect, rtol=1e-14)
+
+
+def test_summaries_cover_complete_chunks_only():
+    L, C, d = 23, 5, 3
+    K, V = rand((L, d), 41), rand((L, d), 42)
+    Ks, Vs = oracle.summaries(K, V, C)
+    assert Ks.shape == (4, d)
+    # Chunk 2 depends only on tokens 10..14.
+    K2, V2 = K.copy(), V.copy()
+    K2[:10] += 5.0
+    K2[15:] -= 3.0
+    V2[20:] = 0.0
+    Ks2, Vs2 = oracle.summaries(K2, V2, C)
+    np.testing.assert_array_equal(Ks[2], Ks2[2])
+    np.testing.assert_array_equal(Vs[2], Vs2[2])
+
+
+def test_summary_logit_offset_is_natural_log():
+    # A single row attending one window token and one summarized chunk with
+    # Q = 0: weights 1 (window) and C (summary, exp(ln C)).
+    L, W, C, d = 5, 1, 4, 1
+    v = np.array([[1.0], [1.0], [1.0], [1.0], [0.0]])[None, None]
+    q = np.zeros((1, 1, L, d))
+    k = np.zeros((1, 1, L, d))
+    o = oracle.prefill(q, k, v, W=W, C=C)[0, 0]
+    # Row 4: window {4} (v = 0) and chunk {0..3} (vhat = 1, weight 4).
+    assert o[4, 0] == pytest.approx(4.0 / 5.0, rel=1e-15)
+
+
+def test_hand_expanded_golden_cases():
+    with open(os.path.join(GOLDEN, "zero_query_cases.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        L, W, C = case["L"], case["W"], case["C"]
+        v = np.array(case["v"], dtype=np.float64).reshape(1, 1, L, 1)
+        z = np.zeros_like(v)
+        o = oracle.prefill(z, z, v, W=W, C=C)[0, 0, :, 0]
+        expect = [float(Fraction(a, b)) for a, b in case["expected"]]
+        np.testing.assert_allclose(o, expect, rtol=1e-14, err_msg=case["name"])
+
+
+def test_visible_summary_count():
+    # s(n) = floor(max(0, n-W+1)/C); spot values worked out by hand.
+    assert oracle.visible_summaries(0, 4, 3) == 0
+    assert oracle.visible_summaries(5, 4, 3) == 0
+    assert oracle.visible_summaries(6, 4, 3) == 1
+    assert oracle.visible_summaries(8, 4, 3) == 1
+    assert oracle.visible_summaries(9, 4, 3) == 2
+    # 8192-token context decoded at position 8192 with W = 512, C = 128:
+    # the window is 7681..8192 and 60 chunks lie fully before it.
+    assert oracle.visible_summaries(8192, 512, 128) == 60
+
+
+# ---------------------------------------------------------------------------
+# Invariants of softmax attention over an augmented key/value set
+# ---------------------------------------------------------------------------
+
+def _case(seed, L=45, d=8, H=2, Hkv=1):
+    q = rand((1, H, L, d), seed)
+    k = rand((1, Hkv, L, d), seed + 1)
+    v = rand((1, Hkv, L, d), seed + 2)
+    return q, k, v
+
+
+def test_rows_are_convex_combinations_of_past_values():
+    q, k, v = _case(51)
+    W, C = 6, 4
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    for h in range(2):
+        for n in range(45):
+            past = v[0, 0, : n + 1]
+            assert np.all(o[0, h, n] <= past.max(axis=0) + 1e-12)
+            assert np.all(o[0, h, n] >= past.min(axis=0) - 1e-12)
+
+
+def test_constant_values_shift_and_linearity():
+    q, k, v = _case(61)
+    W, C = 5, 3
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    const = np.broadcast_to(rand((8,), 64), v.shape).copy()
+    np.testing.assert_allclose(oracle.prefill(q, k, const, W=W, C=C), np.broadcast_to(const, o.shape),
+                               rtol=1e-12, atol=1e-12)
+    shift = rand((8,), 65)
+    np.testing.assert_allclose(oracle.prefill(q, k, v + shift, W=W, C=C), o + shift, rtol=1e-11, atol=1e-11)
+    v2 = rand(v.shape, 66)
+    np.testing.assert_allclose(oracle.prefill(q, k, 2.0 * v - 3.0 * v2, W=W, C=C),
+                               2.0 * o - 3.0 * oracle.prefill(q, k, v2, W=W, C=C), rtol=1e-10, atol=1e-11)
+
+
+def test_causality():
+    q, k, v = _case(71)
+    W, C = 7, 5
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    cut = 20
+    q2, k2, v2 = q.copy(), k.copy(), v.copy()
+    q2[:, :, cut:] = rand(q2[:, :, cut:].shape, 72)
+    k2[:, :, cut:] = rand(k2[:, :, cut:].shape, 73)
+    v2[:, :, cut:] = rand(v2[:, :, cut:].shape, 74)
+    o2 = oracle.prefill(q2, k2, v2, W=W, C=C)
+    np.testing.assert_array_equal(o[:, :, :cut], o2[:, :, :cut])
+
+
+def test_permutation_inside_summarized_chunk():
+    q, k, v = _case(81, L=40)
+    W, C = 6, 5
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    perm = np.array([3, 0, 4, 1, 2]) + 5  # chunk 1 = tokens 5..9
+    k2, v2 = k.copy(), v.copy()
+    k2[:, :, 5:10] = k[:, :, perm]
+    v2[:, :, 5:10] = v[:, :, perm]
+    o2 = oracle.prefill(q, k2, v2, W=W, C=C)
+    # rows whose window starts at or after token 10 see chunk 1 only as a summary
+    rows = [n for n in range(40) if n - W + 1 >= 10]
+    np.testing.assert_allclose(o2[:, :, rows], o[:, :, rows], rtol=1e-12, atol=1e-13)
+    # a row whose window starts inside the permuted chunk sees a different
+    # subset of its tokens (row 12: window 7..12, tokens 5 and 6 in no term)
+    assert not np.allclose(o2[:, :, 12], o[:, :, 12])
+
+
+def test_gqa_head_mapping_consecutive_heads_share_kv():
+    # H = 4 query heads over 2 kv heads: heads 0,1 read kv head 0; 2,3 read 1.
+    L, d, W, C = 21, 4, 4, 3
+    q = rand((1, 4, L, d), 91)
+    k = rand((1, 2, L, d), 92)
+    v = rand((1, 2, L, d), 93)
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    for h in range(4):
+        g = h // 2
+        oh = oracle.prefill(q[:, h:h + 1], k[:, g:g + 1], v[:, g:g + 1], W=W, C=C)
+        np.testing.assert_array_equal(o[:, h], oh[:, 0])
+
+
+def test_rows_entry_matches_whole_prefill():
+    q, k, v = _case(101, L=50)
+    W, C = 8, 4
+    o = oracle.prefill(q, k, v, W=W, C=C)
+    Ks, Vs = oracle.summaries(k[0, 0], v[0, 0], C)
+    rows = np.array([0, 7, 8, 11, 12, 31, 49])
+    got = oracle.attend_rows(q[0, 1, rows], rows, k[0, 0], v[0, 0], Ks, Vs, W, C)
+    np.testing.assert_array_equal(got, o[0, 1, rows])
