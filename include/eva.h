@@ -1,0 +1,157 @@
+/*
+ * eva.h — C ABI of the MI355X (gfx950) EVA attention library (libeva.so).
+ *
+ * EVA attention as FlashEVA computes it (section "FlashEVA": EVA rewritten as
+ * one softmax attention over an augmented key/value set; the local set E and
+ * the chunk partition P_c come from section "EVA Attention", eq. (eva) and
+ * eq. (eva_normalization)):
+ *
+ *   - the causal sequence is cut into chunks of C tokens, chunk c covering
+ *     positions [cC, cC + C);
+ *   - each complete chunk becomes one summary pair
+ *         khat_c = mean of the chunk's keys
+ *         vhat_c = sum_j softmax_j(khat_c . k_j / sqrt(d)) v_j
+ *     (query independent: the single-sample property of eq. (eva) lets the
+ *     random-feature value be computed once per chunk);
+ *   - the query at position n takes ONE softmax over
+ *         q_n . k_m / sqrt(d)           for m in [max(0, n-W+1), n]   (window)
+ *         q_n . khat_c / sqrt(d) + ln C for c < s(n),
+ *                                       s(n) = floor(max(0, n-W+1) / C)
+ *     with values v_m and vhat_c.  The + ln C gives each summary the weight
+ *     of the C tokens it stands for (eq. (eva_normalization) approximates a
+ *     chunk's sum of C exponentials by one).  Tokens between the last
+ *     summarized chunk and the window start belong to neither term.
+ *
+ * Shapes and layouts (all row-major, contiguous, device memory):
+ *   Q, O          [B][H][L][d]
+ *   K, V          [B][H_kv][L][d]
+ *   Ksum, Vsum    [B][H_kv][L / C][d]       (complete chunks only)
+ * Grouped-query attention: H must be a multiple of H_kv; query head h reads
+ * key/value head h / (H / H_kv).
+ *
+ * Element types: EVA_BF16 (bfloat16 storage, fp32 accumulation; the softmax
+ * weights are rounded to bf16 before the weighted sum of values) or EVA_F32
+ * (fp32 throughout).  One call uses one type for every tensor it touches.
+ * Head dimension d must be 64 or 128.
+ *
+ * Streams and ownership: `stream` is a hipStream_t passed as void* (NULL =
+ * the default stream).  Every call validates its arguments, enqueues kernels
+ * on `stream` and returns; it never allocates, frees or synchronizes.  The
+ * caller owns every buffer and must keep it alive until the work completes.
+ * Kernel faults surface at the caller's next synchronization.
+ *
+ * Errors: functions return EVA_OK (0) or a negative eva_status; invalid
+ * arguments are rejected before anything is enqueued.  No C++ exception
+ * crosses this boundary.
+ */
+#ifndef EVA_H
+#define EVA_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    EVA_OK = 0,
+    EVA_ERR_INVALID = -1,     /* bad shape, window, chunk size or null pointer */
+    EVA_ERR_UNSUPPORTED = -2, /* head dim or element type this build does not handle */
+    EVA_ERR_CAPACITY = -3,    /* cache ring or summary array too small */
+    EVA_ERR_HIP = -4          /* the HIP runtime refused a launch */
+} eva_status;
+
+typedef enum { EVA_BF16 = 0, EVA_F32 = 1 } eva_dtype;
+
+/*
+ * Decode cache: the state one decoded token needs — the exact keys/values of
+ * the window and the chunk summaries (FlashEVA keeps a compressed cache whose
+ * size grows with the number of chunks, not tokens).
+ *
+ * The struct is caller-owned host memory; the four arrays are caller-owned
+ * device memory of the cache's dtype.  Position p of (b, g) lives in ring slot
+ * p mod R.  Values are stored transposed (feature-major) so the decode kernel
+ * can feed them to the matrix cores straight from HBM:
+ *   k_ring   [B][H_kv][R][d]         keys, row per slot
+ *   vt_ring  [B][H_kv][d][R]         values, transposed
+ *   k_sum    [B][H_kv][S_max][d]     summary keys
+ *   vt_sum   [B][H_kv][d][S_max]     summary values, transposed
+ * Requirements: R >= W + C - 1 and R a multiple of 32; S_max a multiple of 32.
+ * n_tok counts the tokens the cache has absorbed (the same for every
+ * sequence of the batch); the library updates it.
+ */
+typedef struct eva_cache {
+    int B, H, H_kv, d, W, C;
+    int dtype;        /* eva_dtype */
+    int R;            /* ring slots per (b, kv head) */
+    int S_max;        /* summary capacity per (b, kv head) */
+    long long n_tok;  /* tokens held; host-side state */
+    void* k_ring;
+    void* vt_ring;
+    void* k_sum;
+    void* vt_sum;
+} eva_cache;
+
+/*
+ * Chunk summaries (section "EVA Attention", the single-sample property after
+ * eq. (eva_normalization)): for every (b, g) and complete chunk c < L / C,
+ *   Ksum[b][g][c] = mean of K[b][g][cC .. cC+C-1]
+ *   Vsum[b][g][c] = sum_j softmax_j(Ksum . K_j / sqrt(d)) V_j
+ * computed in fp32 and stored in `dtype`.  L < C is valid and writes nothing.
+ * Errors: INVALID for null pointers with L >= C, B/H_kv/L/C < 1;
+ * UNSUPPORTED for d not in {64, 128} or an unknown dtype.
+ */
+int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum,
+                        int B, int H_kv, int L, int d, int C, int dtype, void* stream);
+
+/*
+ * EVA prefill (section "FlashEVA"): O = one softmax per row over the window
+ * keys and the visible chunk summaries, as described at the top of this file.
+ * Builds the summaries first (into Ksum/Vsum, caller-provided, shape
+ * [B][H_kv][L / C][d]; may be NULL only when L < C), then runs the fused
+ * window + summary attention kernel.  If `cache` is not NULL it must describe
+ * the same B, H, H_kv, d, W, C and dtype with S_max >= L / C; the call then
+ * also writes the last min(L, R) keys/values into the ring, all L / C
+ * summaries into the cache, and sets cache->n_tok = L.
+ * Errors: INVALID (shapes, W < 1, C < 1, H % H_kv != 0, null pointers,
+ * cache mismatch), CAPACITY (cache too small), UNSUPPORTED (d, dtype).
+ */
+int eva_prefill(const void* Q, const void* K, const void* V, void* O,
+                int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                void* Ksum, void* Vsum, eva_cache* cache, void* stream);
+
+/*
+ * Append one token per sequence: k_new, v_new [B][H_kv][d].  The token takes
+ * position p = cache->n_tok.  If that position makes chunk S = s(p) - 1 newly
+ * visible (s(p) > s(p - 1)), its summary is built from the ring first, then
+ * the token is written to slot p mod R, then n_tok becomes p + 1.
+ * Errors: INVALID (null pointers, malformed cache), CAPACITY (a summary
+ * index >= S_max would be needed).
+ */
+int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, void* stream);
+
+/*
+ * One decode step: q [B][H][d] is the query of position p = n_tok - 1 (the
+ * token appended last); o [B][H][d] receives its EVA attention output over
+ * the ring window [p-W+1, p] and the summaries c < s(p).  Row p of the
+ * prefill of the same tokens gives the same result up to rounding order.
+ * `ws` is optional device scratch of `ws_bytes` bytes: with at least
+ * eva_decode_workspace_bytes(cache) bytes the rows of each sequence are split
+ * over more workgroups (for small B * H_kv); with less (or NULL) the call
+ * still works, one workgroup per (b, kv head, 16 query heads).
+ * Errors: INVALID (n_tok == 0, null pointers, malformed cache).
+ */
+int eva_decode_step(const eva_cache* cache, const void* q, void* o,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace that lets eva_decode_step split rows across workgroups. */
+size_t eva_decode_workspace_bytes(const eva_cache* cache);
+
+/* Static description of an eva_status value. */
+const char* eva_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EVA_H */

@@ -1,0 +1,80 @@
+"""ctypes declarations of libeva.so (the C ABI in include/eva.h).
+
+The library is loaded from this package's directory.  There is no fallback:
+if libeva.so is missing or lacks a symbol, loading raises.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libeva.so")
+
+EVA_OK = 0
+EVA_ERR_INVALID = -1
+EVA_ERR_UNSUPPORTED = -2
+EVA_ERR_CAPACITY = -3
+EVA_ERR_HIP = -4
+EVA_BF16 = 0
+EVA_F32 = 1
+
+# Every entry point include/eva.h declares.
+SYMBOLS = (
+    "eva_build_summaries",
+    "eva_prefill",
+    "eva_cache_append",
+    "eva_decode_step",
+    "eva_decode_workspace_bytes",
+    "eva_status_string",
+)
+
+
+class EvaCacheStruct(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int), ("H", ctypes.c_int), ("H_kv", ctypes.c_int), ("d", ctypes.c_int),
+        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("R", ctypes.c_int),
+        ("S_max", ctypes.c_int), ("n_tok", ctypes.c_longlong),
+        ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
+        ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load():
+    """Load libeva.so and declare its signatures (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() or "
+                           "python paper_2511_00576_amd/build.py")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    cp = ctypes.POINTER(EvaCacheStruct)
+    lib.eva_build_summaries.restype = i
+    lib.eva_build_summaries.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
+    lib.eva_prefill.restype = i
+    lib.eva_prefill.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
+    lib.eva_cache_append.restype = i
+    lib.eva_cache_append.argtypes = [cp, vp, vp, vp]
+    lib.eva_decode_step.restype = i
+    lib.eva_decode_step.argtypes = [cp, vp, vp, vp, sz, vp]
+    lib.eva_decode_workspace_bytes.restype = sz
+    lib.eva_decode_workspace_bytes.argtypes = [cp]
+    lib.eva_status_string.restype = ctypes.c_char_p
+    lib.eva_status_string.argtypes = [i]
+    _lib = lib
+    return lib
+
+
+class EvaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        msg = load().eva_status_string(status).decode()
+        super().__init__(f"{fn} failed: {msg} ({status})")
+        self.status = status
+
+
+def check(fn: str, status: int) -> None:
+    if status != EVA_OK:
+        raise EvaError(fn, status)

@@ -1,0 +1,362 @@
+// Decode-side kernels: cache fill after a prefill, per-token append (with the
+// chunk summary that becomes due), and the bandwidth-bound decode step.
+//
+// Cache layout (per (b, kv head)): keys row-major by ring slot [R][D], values
+// transposed [D][R]; summary keys [S_max][D], summary values [D][S_max].
+// Position p lives in slot p mod R; R is a multiple of 32 so a 32-aligned run
+// of positions is a 32-aligned run of slots.
+//
+// Decode works on 32-row chunks: summary chunks (rows of the summary arrays)
+// and window chunks (32-aligned position runs of the ring).  Per chunk a wave
+// computes S^T = K Q^T with the matrix cores, reading the key rows straight
+// from HBM as A operands (rows permuted so that each lane's 8 softmax weights
+// land on 8 consecutive keys), then O^T += V^T P^T with the transposed values
+// read straight from HBM as A operands: every byte of K and V is read once,
+// 16 B per lane, and never staged through LDS.  Query heads sharing a kv head
+// (up to 16) are the MFMA columns, so the keys and values are read once for
+// all of them.
+#include "eva_kernels.hpp"
+#include "summary.hpp"
+
+namespace eva {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// cache fill
+// ---------------------------------------------------------------------------
+template <int D, typename T>
+__global__ void cache_fill_kernel(CacheView c, const T* __restrict__ K, const T* __restrict__ V,
+                                  const T* __restrict__ Ks, const T* __restrict__ Vs, int L, int n_chunks) {
+    const size_t bg = blockIdx.y;
+    const int first = max(0, L - c.R);
+    const int rows = L - first;
+    T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
+    T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
+    T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
+    T* vs = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+    const T* K0 = K + bg * (size_t)L * D;
+    const T* V0 = V + bg * (size_t)L * D;
+    const T* Ks0 = Ks + bg * (size_t)n_chunks * D;
+    const T* Vs0 = Vs + bg * (size_t)n_chunks * D;
+    const long long total = (long long)(rows + n_chunks) * D;
+    for (long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x; e < total;
+         e += (long long)gridDim.x * blockDim.x) {
+        const int r = (int)(e / D), d = (int)(e % D);
+        if (r < rows) {
+            const int pos = first + r;
+            const int slot = pos % c.R;
+            kr[(size_t)slot * D + d] = K0[(size_t)pos * D + d];
+            vr[(size_t)d * c.R + slot] = V0[(size_t)pos * D + d];
+        } else {
+            const int s = r - rows;
+            ks[(size_t)s * D + d] = Ks0[(size_t)s * D + d];
+            vs[(size_t)d * c.S_max + s] = Vs0[(size_t)s * D + d];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// append (one workgroup per (b, kv head))
+// ---------------------------------------------------------------------------
+template <int D, typename T>
+__global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView c, const T* __restrict__ k_new,
+                                                                       const T* __restrict__ v_new, int s_new) {
+    extern __shared__ float smem[];
+    const size_t bg = blockIdx.x;
+    T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
+    T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
+    if (s_new >= 0) {
+        // the chunk's rows are still in the ring: positions [s_new*C, s_new*C + C)
+        RingChunk<D, T> src{kr, vr, (long long)s_new * c.C, c.R};
+        float kh[8], vh[8];
+        chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
+        const int t = threadIdx.x;
+        if (t < D / 8) {
+            T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
+            T* vs = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                ks[(size_t)s_new * D + t * 8 + i] = from_f32<T>(kh[i]);
+                vs[(size_t)(t * 8 + i) * c.S_max + s_new] = from_f32<T>(vh[i]);
+            }
+        }
+        __syncthreads();  // every read of the chunk precedes the slot overwrite below
+    }
+    const int slot = (int)(c.n_tok % c.R);
+    for (int d = threadIdx.x; d < D; d += blockDim.x) {
+        kr[(size_t)slot * D + d] = k_new[bg * D + d];
+        vr[(size_t)d * c.R + slot] = v_new[bg * D + d];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// decode step
+// ---------------------------------------------------------------------------
+constexpr int kDecWaves = 4;
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
+    typedef bf16 T;
+    constexpr int NDC = D / 32;  // 32-feature contraction steps
+    constexpr int NDB = D / 16;  // 16-feature output blocks
+    __shared__ float red_m[kDecWaves][16];
+    __shared__ float red_l[kDecWaves][16];
+    __shared__ float red_o[kDecWaves][D][17];
+
+    const int split = blockIdx.x;
+    const int kvh = blockIdx.y / a.n_hg;
+    const int hg = blockIdx.y % a.n_hg;
+    const int b = blockIdx.z;
+    const CacheView& c = a.c;
+    const size_t bg = (size_t)b * c.Hkv + kvh;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int h0 = kvh * a.G + hg * 16;
+    const int ncols = min(16, a.G - hg * 16);
+
+    const T* kring = static_cast<const T*>(c.k_ring) + bg * (size_t)c.R * D;
+    const T* vring = static_cast<const T*>(c.vt_ring) + bg * (size_t)c.R * D;
+    const T* ksum = static_cast<const T*>(c.k_sum) + bg * (size_t)c.S_max * D;
+    const T* vsum = static_cast<const T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+
+    // query fragments: column c16 = head h0 + c16, features dc*32 + 8g .. +7
+    bf16x8 qf[NDC];
+    {
+        const T* qrow = static_cast<const T*>(a.q) + ((size_t)b * c.H + h0 + min(c16, ncols - 1)) * D;
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc) {
+            qf[dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
+            if (c16 >= ncols) qf[dc] = bf16x8{};
+        }
+    }
+
+    floatx4 acc[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const int n_chunks = a.n_sum_chunks + a.n_win_chunks;
+    const int worker = split * kDecWaves + wave;
+    const int n_workers = a.splits * kDecWaves;
+    // key row of the A operand for S^T block kb (row c16 of the 16-row block):
+    // keys of lane group g' = c16/4 land on 8 consecutive keys 8g'..8g'+7
+    const int krow0 = (c16 >> 2) * 8 + (c16 & 3);
+
+    for (int ch = worker; ch < n_chunks; ch += n_workers) {
+        const bool is_sum = ch < a.n_sum_chunks;
+        const T* kbase;
+        const T* vbase;  // element (d, key) at vbase + d * vstride + key
+        int vstride, key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
+        if (is_sum) {
+            const int r0 = ch * 32;
+            kbase = ksum + (size_t)r0 * D;
+            vbase = vsum + r0;
+            vstride = c.S_max;
+            key_lo = 0;
+            key_hi = min(31, a.n_sum - 1 - r0);
+        } else {
+            const int pos0 = (a.first_win_chunk + ch - a.n_sum_chunks) * 32;
+            const int slot0 = pos0 % c.R;
+            kbase = kring + (size_t)slot0 * D;
+            vbase = vring + slot0;
+            vstride = c.R;
+            key_lo = max(0, a.win_lo - pos0);
+            key_hi = min(31, a.p - pos0);
+        }
+        const bool full = key_lo == 0 && key_hi == 31;
+
+        // all 16-B fragment loads of the chunk first: 2*NDC key + NDB value
+        bf16x8 ka[2][NDC], va[NDB];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const T* krow = kbase + (size_t)(krow0 + kb * 4) * D + g * 8;
+#pragma unroll
+            for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = *reinterpret_cast<const bf16x8*>(krow + dc * 32);
+        }
+        // A operand of O^T += V^T P^T, lane (g, c16): feature db*16+c16, keys 8g..8g+7
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+            va[db] = *reinterpret_cast<const bf16x8*>(vbase + (size_t)(db * 16 + c16) * vstride + g * 8);
+
+        // S^T = K Q^T over the chunk: s[kb] rows = keys 8g + 4kb + i
+        floatx4 s[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int dc = 0; dc < NDC; ++dc) s[kb] = mfma_bf16(ka[kb][dc], qf[dc], s[kb]);
+        }
+        if (!full) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = g * 8 + kb * 4 + i;
+                    if (key < key_lo || key > key_hi) s[kb][i] = -INFINITY;
+                }
+            // stale ring slots may hold any bit pattern: zero their values
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int key = g * 8 + j;
+                    if (key < key_lo || key > key_hi) va[db][j] = (bf16)0.f;
+                }
+        }
+        const float bias = is_sum ? a.log2C : 0.f;
+        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        mx = xgroup_max(mx) * a.scale_log2 + bias;
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = fast_exp2(m_run - m_use);  // m_run = -inf -> 0
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+        m_run = m_new;
+        const float off = bias - m_use;
+        bf16x8 pf;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float p = fast_exp2(fmaf(s[kb][i], a.scale_log2, off));
+                l_run += p;
+                pf[kb * 4 + i] = to_bf16(p);
+            }
+
+        // O^T += V^T P^T
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) acc[db] = mfma_bf16(va[db], pf, acc[db]);
+    }
+
+    // ---- combine the four waves ----
+    const float l_wave = xgroup_sum(l_run);
+    if (g == 0) {
+        red_m[wave][c16] = m_run;
+        red_l[wave][c16] = l_wave;
+    }
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red_o[wave][db * 16 + g * 4 + i][c16] = acc[db][i];
+    __syncthreads();
+
+    // thread -> (column, feature run): 16 columns x 16 runs of D/16 features
+    const int col = tid & 15;
+    const int run = tid >> 4;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, red_m[w][col]);
+    float wgt[kDecWaves];
+    float lsum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+        wgt[w] = M == -INFINITY ? 0.f : fast_exp2(red_m[w][col] - M);
+        lsum += wgt[w] * red_l[w][col];
+    }
+    constexpr int FPT = D / 16;  // features per thread
+    float out[FPT];
+#pragma unroll
+    for (int f = 0; f < FPT; ++f) {
+        const int d = run * FPT + f;
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < kDecWaves; ++w) v += wgt[w] * red_o[w][d][col];
+        out[f] = v;
+    }
+    if (col >= ncols) return;
+    if (a.splits == 1) {
+        const float inv = 1.f / lsum;
+        T* orow = static_cast<T*>(a.o) + ((size_t)b * c.H + h0 + col) * D + run * FPT;
+#pragma unroll
+        for (int f = 0; f < FPT; ++f) orow[f] = to_bf16(out[f] * inv);
+    } else {
+        // partial: [m, l, o[D]] per (b, kv head, head group, split, column)
+        float* w = a.ws + ((((size_t)b * c.Hkv + kvh) * a.n_hg + hg) * a.splits + split) * 16 * (D + 2) +
+                   (size_t)col * (D + 2);
+        if (run == 0) {
+            w[0] = M;
+            w[1] = lsum;
+        }
+#pragma unroll
+        for (int f = 0; f < FPT; ++f) w[2 + run * FPT + f] = out[f];
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
+    typedef bf16 T;
+    const int kvh = blockIdx.y / a.n_hg;
+    const int hg = blockIdx.y % a.n_hg;
+    const int b = blockIdx.z;
+    const CacheView& c = a.c;
+    const int ncols = min(16, a.G - hg * 16);
+    const float* base = a.ws + (((size_t)b * c.Hkv + kvh) * a.n_hg + hg) * a.splits * 16 * (D + 2);
+    for (int e = threadIdx.x; e < ncols * D; e += blockDim.x) {
+        const int col = e / D, d = e % D;
+        float M = -INFINITY;
+        for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, base[((size_t)sp * 16 + col) * (D + 2)]);
+        float num = 0.f, den = 0.f;
+        for (int sp = 0; sp < a.splits; ++sp) {
+            const float* w = base + ((size_t)sp * 16 + col) * (D + 2);
+            const float wt = w[0] == -INFINITY ? 0.f : fast_exp2(w[0] - M);
+            den += wt * w[1];
+            num += wt * w[2 + d];
+        }
+        T* orow = static_cast<T*>(a.o) + ((size_t)b * c.H + kvh * a.G + hg * 16 + col) * D;
+        orow[d] = to_bf16(num / den);
+    }
+}
+
+}  // namespace
+
+template <int D, typename T>
+hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,
+                             int L, hipStream_t stream) {
+    const int n_chunks = L / c.C;
+    const int rows = min(L, c.R) + n_chunks;
+    const int per_bg = (rows * D + 255) / 256;
+    dim3 grid(min(per_bg, 64), c.B * c.Hkv);
+    hipLaunchKernelGGL((cache_fill_kernel<D, T>), grid, dim3(256), 0, stream, c, static_cast<const T*>(K),
+                       static_cast<const T*>(V), static_cast<const T*>(Ks), static_cast<const T*>(Vs), L, n_chunks);
+    return hipGetLastError();
+}
+
+template <int D, typename T>
+hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int s_new,
+                               hipStream_t stream) {
+    const size_t lds = s_new >= 0 ? (size_t)(c.C + summary_red_floats<D>()) * sizeof(float) : 0;
+    hipLaunchKernelGGL((cache_append_kernel<D, T>), dim3(c.B * c.Hkv), dim3(kSummaryThreads), lds, stream, c,
+                       static_cast<const T*>(k_new), static_cast<const T*>(v_new), s_new);
+    return hipGetLastError();
+}
+
+template <int D, typename T>
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
+    static_assert(sizeof(T) == 2, "decode runs on bf16 caches");
+    dim3 grid(p.splits, p.c.Hkv * p.n_hg, p.c.B);
+    hipLaunchKernelGGL((decode_kernel<D>), grid, dim3(256), 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.splits == 1) return e;
+    hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(1, p.c.Hkv * p.n_hg, p.c.B), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+template hipError_t launch_cache_fill<64, bf16>(const CacheView&, const void*, const void*, const void*, const void*,
+                                                int, hipStream_t);
+template hipError_t launch_cache_fill<128, bf16>(const CacheView&, const void*, const void*, const void*,
+                                                 const void*, int, hipStream_t);
+template hipError_t launch_cache_fill<64, float>(const CacheView&, const void*, const void*, const void*,
+                                                 const void*, int, hipStream_t);
+template hipError_t launch_cache_fill<128, float>(const CacheView&, const void*, const void*, const void*,
+                                                  const void*, int, hipStream_t);
+template hipError_t launch_cache_append<64, bf16>(const CacheView&, const void*, const void*, int, hipStream_t);
+template hipError_t launch_cache_append<128, bf16>(const CacheView&, const void*, const void*, int, hipStream_t);
+template hipError_t launch_cache_append<64, float>(const CacheView&, const void*, const void*, int, hipStream_t);
+template hipError_t launch_cache_append<128, float>(const CacheView&, const void*, const void*, int, hipStream_t);
+template hipError_t launch_decode<64, bf16>(const DecodeParams&, hipStream_t);
+template hipError_t launch_decode<128, bf16>(const DecodeParams&, hipStream_t);
+
+}  // namespace eva

@@ -1,0 +1,269 @@
+// C ABI of libeva: argument validation, launch geometry, dtype/head-dim
+// dispatch and the decode cache's host-side bookkeeping.  Every function
+// validates before enqueuing anything and never allocates, frees or
+// synchronizes.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/eva.h"
+#include "eva_device.hpp"
+#include "eva_kernels.hpp"
+
+using eva::bf16;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int supported(int d, int dtype) {
+    if (dtype != EVA_BF16 && dtype != EVA_F32) return EVA_ERR_UNSUPPORTED;
+    if (d != 64 && d != 128) return EVA_ERR_UNSUPPORTED;
+    return EVA_OK;
+}
+
+int visible_summaries(long long n, long long W, long long C) {
+    long long start = n - W + 1;
+    return start > 0 ? (int)(start / C) : 0;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? EVA_OK : EVA_ERR_HIP; }
+
+template <typename F>
+hipError_t dispatch(int d, int dtype, F&& f) {
+    if (dtype == EVA_BF16) {
+        if (d == 64) return f(std::integral_constant<int, 64>(), bf16());
+        return f(std::integral_constant<int, 128>(), bf16());
+    }
+    if (d == 64) return f(std::integral_constant<int, 64>(), float());
+    return f(std::integral_constant<int, 128>(), float());
+}
+
+// Largest C whose logits fit the summary kernel's LDS scratch.
+constexpr int kMaxChunk = 8192;
+
+int check_cache(const eva_cache* c) {
+    if (!c) return EVA_ERR_INVALID;
+    if (c->B < 1 || c->H < 1 || c->H_kv < 1 || c->H % c->H_kv != 0 || c->W < 1 || c->C < 1 || c->C > kMaxChunk)
+        return EVA_ERR_INVALID;
+    int st = supported(c->d, c->dtype);
+    if (st != EVA_OK) return st;
+    if (!c->k_ring || !c->vt_ring || !c->k_sum || !c->vt_sum) return EVA_ERR_INVALID;
+    if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
+        return EVA_ERR_INVALID;
+    if (c->n_tok < 0) return EVA_ERR_INVALID;
+    if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
+    if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
+    if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    return EVA_OK;
+}
+
+eva::CacheView view_of(const eva_cache* c) {
+    eva::CacheView v;
+    v.B = c->B;
+    v.H = c->H;
+    v.Hkv = c->H_kv;
+    v.W = c->W;
+    v.C = c->C;
+    v.R = c->R;
+    v.S_max = c->S_max;
+    v.n_tok = c->n_tok;
+    v.k_ring = c->k_ring;
+    v.vt_ring = c->vt_ring;
+    v.k_sum = c->k_sum;
+    v.vt_sum = c->vt_sum;
+    return v;
+}
+
+int gcd(int a, int b) {
+    while (b) {
+        int t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+// Split count for decode: enough workgroups to cover the chip when B * H_kv
+// is small, never more than one wave per chunk.
+int decode_splits(int units, int n_chunks) {
+    if (units >= 256) return 1;
+    int s = (512 + units - 1) / units;
+    int max_s = (n_chunks + 3) / 4;
+    if (s > max_s) s = max_s;
+    return s < 1 ? 1 : s;
+}
+
+int decode_chunks(const eva_cache* c, long long p, int* n_sum_out, int* win_lo_out, int* n_sum_chunks,
+                  int* n_win_chunks) {
+    const int n_sum = visible_summaries(p, c->W, c->C);
+    const long long win_lo = p - c->W + 1 > 0 ? p - c->W + 1 : 0;
+    *n_sum_out = n_sum;
+    *win_lo_out = (int)win_lo;
+    *n_sum_chunks = (n_sum + 31) / 32;
+    *n_win_chunks = (int)(p / 32 - win_lo / 32 + 1);
+    return *n_sum_chunks + *n_win_chunks;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* eva_status_string(int status) {
+    switch (status) {
+        case EVA_OK: return "ok";
+        case EVA_ERR_INVALID: return "invalid argument";
+        case EVA_ERR_UNSUPPORTED: return "unsupported head dimension, element type or size";
+        case EVA_ERR_CAPACITY: return "cache capacity exceeded";
+        case EVA_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum, int B, int H_kv, int L, int d, int C,
+                        int dtype, void* stream) {
+    if (B < 1 || H_kv < 1 || L < 1 || C < 1) return EVA_ERR_INVALID;
+    int st = supported(d, dtype);
+    if (st != EVA_OK) return st;
+    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (L / C == 0) return EVA_OK;
+    if (!K || !V || !Ksum || !Vsum) return EVA_ERR_INVALID;
+    if (!aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
+        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, s);
+    }));
+}
+
+int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
+                int C, int dtype, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
+    if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    int st = supported(d, dtype);
+    if (st != EVA_OK) return st;
+    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (!Q || !K || !V || !O) return EVA_ERR_INVALID;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return EVA_ERR_INVALID;
+    const int n_chunks = L / C;
+    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
+    if (cache) {
+        st = check_cache(cache);
+        if (st != EVA_OK) return st;
+        if (cache->B != B || cache->H != H || cache->H_kv != H_kv || cache->d != d || cache->W != W ||
+            cache->C != C || cache->dtype != dtype)
+            return EVA_ERR_INVALID;
+        if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
+    }
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = dispatch(d, dtype, [&](auto dd, auto t) {
+        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, s);
+    });
+    if (e != hipSuccess) return EVA_ERR_HIP;
+
+    eva::PrefillParams p;
+    p.Q = Q;
+    p.K = K;
+    p.V = V;
+    p.Ks = Ksum;
+    p.Vs = Vsum;
+    p.O = O;
+    p.B = B;
+    p.H = H;
+    p.Hkv = H_kv;
+    p.L = L;
+    p.W = W;
+    p.C = C;
+    p.n_chunks = n_chunks;
+    p.G = H / H_kv;
+    p.Gt = gcd(p.G, 4);
+    p.n_hg = p.G / p.Gt;
+    p.pos_per_wg = 32 * 4 / p.Gt;
+    p.n_pos_tiles = (L + p.pos_per_wg - 1) / p.pos_per_wg;
+    const long long tiles = (long long)B * H_kv * p.n_hg * p.n_pos_tiles;
+    if (tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
+    p.n_tiles = (int)tiles;
+    p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
+    p.log2C = (float)log2((double)C);
+    e = dispatch(d, dtype, [&](auto dd, auto t) {
+        return eva::launch_prefill<decltype(dd)::value, decltype(t)>(p, s);
+    });
+    if (e != hipSuccess) return EVA_ERR_HIP;
+
+    if (cache) {
+        eva::CacheView v = view_of(cache);
+        e = dispatch(d, dtype, [&](auto dd, auto t) {
+            return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, s);
+        });
+        if (e != hipSuccess) return EVA_ERR_HIP;
+        cache->n_tok = L;
+    }
+    return EVA_OK;
+}
+
+int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, void* stream) {
+    int st = check_cache(cache);
+    if (st != EVA_OK) return st;
+    if (!k_new || !v_new) return EVA_ERR_INVALID;
+    const long long p = cache->n_tok;
+    if (p >= 0x7fffffffLL) return EVA_ERR_CAPACITY;
+    const int s_prev = p > 0 ? visible_summaries(p - 1, cache->W, cache->C) : 0;
+    const int s_now = visible_summaries(p, cache->W, cache->C);
+    int s_new = -1;
+    if (s_now > s_prev) {
+        s_new = s_now - 1;  // s grows by at most one per token
+        if (s_new >= cache->S_max) return EVA_ERR_CAPACITY;
+    }
+    eva::CacheView v = view_of(cache);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
+        return eva::launch_cache_append<decltype(dd)::value, decltype(t)>(v, k_new, v_new, s_new, s);
+    });
+    if (e != hipSuccess) return EVA_ERR_HIP;
+    cache->n_tok = p + 1;
+    return EVA_OK;
+}
+
+size_t eva_decode_workspace_bytes(const eva_cache* cache) {
+    if (check_cache(cache) != EVA_OK || cache->n_tok < 1) return 0;
+    const int G = cache->H / cache->H_kv;
+    const int n_hg = (G + 15) / 16;
+    int n_sum, win_lo, nsc, nwc;
+    const int n_chunks = decode_chunks(cache, cache->n_tok - 1, &n_sum, &win_lo, &nsc, &nwc);
+    const int units = cache->B * cache->H_kv * n_hg;
+    const int splits = decode_splits(units, n_chunks);
+    if (splits == 1) return 0;
+    return (size_t)units * splits * 16 * (cache->d + 2) * sizeof(float);
+}
+
+int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_cache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
+    if (cache->n_tok < 1) return EVA_ERR_INVALID;
+    if (cache->n_tok - 1 > 0x7fffffffLL - 64) return EVA_ERR_CAPACITY;
+
+    eva::DecodeParams p;
+    p.c = view_of(cache);
+    p.q = q;
+    p.o = o;
+    p.p = (int)(cache->n_tok - 1);
+    const int n_chunks = decode_chunks(cache, p.p, &p.n_sum, &p.win_lo, &p.n_sum_chunks, &p.n_win_chunks);
+    if (p.n_sum > cache->S_max) return EVA_ERR_CAPACITY;
+    p.first_win_chunk = p.win_lo / 32;
+    p.G = cache->H / cache->H_kv;
+    p.n_hg = (p.G + 15) / 16;
+    const int units = cache->B * cache->H_kv * p.n_hg;
+    p.splits = decode_splits(units, n_chunks);
+    const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
+    if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
+    p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
+    p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
+    p.log2C = (float)log2((double)cache->C);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    return hip_status(e);
+}
+
+}  // extern "C"

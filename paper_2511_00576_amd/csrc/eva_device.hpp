@@ -1,0 +1,98 @@
+// Device-side building blocks shared by the EVA kernels (gfx950 / CDNA4).
+//
+// Matrix-core operand layouts used throughout (wave of 64 lanes, lane l,
+// lane group g = l / 16, column c = l % 16):
+//   v_mfma_f32_16x16x32_bf16  A[16 x 32]: lane holds A[c][8g .. 8g+7]
+//                             B[32 x 16]: lane holds B[8g .. 8g+7][c]
+//                             D[16 x 16]: lane holds D[4g .. 4g+3][c]
+//   v_mfma_f32_16x16x4_f32    A[16 x 4]:  lane holds A[c][g]
+//                             B[4 x 16]:  lane holds B[g][c]
+//                             D as above.
+// The contraction index may be permuted freely as long as A and B agree.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace eva {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 with round-to-nearest-even (hardware conversion on gfx950).
+__device__ __forceinline__ bf16 to_bf16(float x) { return (bf16)x; }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    bf16 a = to_bf16(lo), b = to_bf16(hi);
+    return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f32(float x) { return x; }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return to_bf16(x); }
+
+__device__ __forceinline__ floatx4 mfma_bf16(const bf16x8& a, const bf16x8& b, const floatx4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma_f32(float a, float b, const floatx4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Reductions across the four 16-lane groups (lanes l, l^16, l^32, l^48):
+// v_permlane16_swap / v_permlane32_swap exchange halves of the wave in one
+// VALU op each, no LDS traffic.
+__device__ __forceinline__ float xgroup_max(float x) {
+    uint32_t u = __float_as_uint(x);
+    auto s16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    float y = fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+    uint32_t v = __float_as_uint(y);
+    auto s32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+}
+__device__ __forceinline__ float xgroup_sum(float x) {
+    uint32_t u = __float_as_uint(x);
+    auto s16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    float y = __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
+    uint32_t v = __float_as_uint(y);
+    auto s32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
+}
+
+// Butterfly reductions inside 16-lane rows (DPP-friendly xor distances).
+__device__ __forceinline__ float row16_sum(float x) {
+    x += __shfl_xor(x, 1, 64);
+    x += __shfl_xor(x, 2, 64);
+    x += __shfl_xor(x, 4, 64);
+    x += __shfl_xor(x, 8, 64);
+    return x;
+}
+
+// LDS transposing read: each lane of a 16-lane group passes the address of 4
+// consecutive 16-bit elements; lanes 4j..4j+3 together name row j (16
+// elements).  Lane i of the group receives element i of rows 0..3.
+typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
+__device__ __forceinline__ shortx4 lds_read_tr16(const bf16* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(p));
+}
+
+__device__ __forceinline__ int visible_summaries(int n, int W, int C) {
+    int start = n - W + 1;
+    return start > 0 ? start / C : 0;
+}
+
+}  // namespace eva

@@ -1,0 +1,77 @@
+// Internal launch interface between the C ABI layer (eva_api.cpp) and the
+// kernel translation units.  Host-visible; no torch types anywhere.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace eva {
+
+struct PrefillParams {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* Ks;  // [B][Hkv][n_chunks][d]
+    const void* Vs;
+    void* O;
+    int B, H, Hkv, L, W, C, n_chunks;
+    int G;            // H / Hkv
+    int Gt;           // heads packed per workgroup (1, 2 or 4)
+    int n_hg;         // G / Gt
+    int pos_per_wg;   // 32 * 4 / Gt
+    int n_pos_tiles;  // ceil(L / pos_per_wg)
+    int n_tiles;      // B * Hkv * n_hg * n_pos_tiles
+    float scale_log2; // log2(e) / sqrt(d)
+    float log2C;      // log2(C): the ln C summary offset in log2 units
+};
+
+template <int D, typename T>
+hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
+
+template <int D, typename T>
+hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
+                            hipStream_t stream);
+
+struct CacheView {
+    int B, H, Hkv, W, C, R, S_max;
+    long long n_tok;
+    void* k_ring;
+    void* vt_ring;
+    void* k_sum;
+    void* vt_sum;
+};
+
+// Copy the last min(L, R) positions of K/V into the ring and the L / C
+// summaries (row-major Ks/Vs) into the cache arrays.
+template <int D, typename T>
+hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,
+                             int L, hipStream_t stream);
+
+// Build summary `s_new` from ring rows (when s_new >= 0), then write the token
+// at position p = c.n_tok.
+template <int D, typename T>
+hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int s_new,
+                               hipStream_t stream);
+
+struct DecodeParams {
+    CacheView c;
+    const void* q;  // [B][H][d]
+    void* o;        // [B][H][d]
+    float* ws;      // split partials or nullptr
+    int p;          // position of the query (n_tok - 1)
+    int n_sum;      // visible summaries s(p)
+    int win_lo;     // first window position
+    int n_sum_chunks;  // 32-row chunks of summaries
+    int n_win_chunks;  // 32-slot chunks of the ring touched by the window
+    int first_win_chunk;
+    int splits;     // workgroups per (b, kv head, head group)
+    int n_hg;       // head groups of 16 per kv head
+    int G;
+    float scale_log2;
+    float log2C;
+};
+
+template <int D, typename T>
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
+
+}  // namespace eva

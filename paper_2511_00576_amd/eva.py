@@ -1,0 +1,141 @@
+"""Torch-facing binding of libeva: marshals device tensors and the current HIP
+stream into the C ABI.  Every computation runs in the library's HIP kernels;
+this module only checks shapes, allocates outputs with torch and forwards
+pointers.  Tensors must live on a ROCm device; there is no CPU path.
+"""
+import ctypes
+
+import torch
+
+from . import _lib
+
+_DTYPES = {torch.bfloat16: _lib.EVA_BF16, torch.float32: _lib.EVA_F32}
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    try:
+        return _DTYPES[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32") from None
+
+
+def _require_device(*ts):
+    for t in ts:
+        if not t.is_cuda:
+            raise RuntimeError("EVA kernels run on the GPU only: tensors must be on a ROCm device")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def build_summaries(K: torch.Tensor, V: torch.Tensor, C: int):
+    """Chunk summaries. K, V: [B, Hkv, L, d] -> (Ksum, Vsum): [B, Hkv, L // C, d]."""
+    _require_device(K, V)
+    B, Hkv, L, d = K.shape
+    Ks = torch.empty(B, Hkv, L // C, d, dtype=K.dtype, device=K.device)
+    Vs = torch.empty_like(Ks)
+    lib = _lib.load()
+    _lib.check("eva_build_summaries",
+               lib.eva_build_summaries(_ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), B, Hkv, L, d, C, _dtype_code(K),
+                                       _stream()))
+    return Ks, Vs
+
+
+class Cache:
+    """Window + summary decode cache in device memory (see eva_cache in eva.h).
+
+    k_ring [B, Hkv, R, d], vt_ring [B, Hkv, d, R] (values transposed),
+    k_sum [B, Hkv, S_max, d], vt_sum [B, Hkv, d, S_max].  The ring holds the
+    last R positions (R >= W + C - 1, a multiple of 32); S_max bounds the number
+    of chunk summaries, i.e. the tokens the cache can ever absorb.
+    """
+
+    def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None,
+                 fill=None):
+        if R is None:
+            R = -(-(W + C - 1) // 32) * 32
+        S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
+        mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
+            (lambda *s: torch.empty(*s, dtype=dtype, device=device))
+        self.k_ring = mk(B, Hkv, R, d)
+        self.vt_ring = mk(B, Hkv, d, R)
+        self.k_sum = mk(B, Hkv, S_max, d)
+        self.vt_sum = mk(B, Hkv, d, S_max)
+        self.dtype = dtype
+        self.struct = _lib.EvaCacheStruct(B, H, Hkv, d, W, C, _DTYPES[dtype], R, S_max, 0,
+                                          self.k_ring.data_ptr(), self.vt_ring.data_ptr(),
+                                          self.k_sum.data_ptr(), self.vt_sum.data_ptr())
+        self._ws = None
+
+    @property
+    def n_tok(self) -> int:
+        return int(self.struct.n_tok)
+
+    @property
+    def R(self) -> int:
+        return int(self.struct.R)
+
+    @property
+    def S_max(self) -> int:
+        return int(self.struct.S_max)
+
+    def workspace(self):
+        """Decode split workspace for the current length (cached, grown on demand)."""
+        n = _lib.load().eva_decode_workspace_bytes(ctypes.byref(self.struct))
+        if n == 0:
+            return None
+        if self._ws is None or self._ws.numel() * 4 < n:
+            self._ws = torch.empty((n + 3) // 4, dtype=torch.float32, device=self.k_ring.device)
+        return self._ws
+
+
+def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool = False):
+    """EVA prefill. Q [B, H, L, d]; K, V [B, Hkv, L, d] -> O [B, H, L, d]."""
+    _require_device(Q, K, V)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    if K.shape != (B, Hkv, L, d) or V.shape != K.shape or Q.dtype != K.dtype or V.dtype != K.dtype:
+        raise ValueError("Q [B,H,L,d], K and V [B,Hkv,L,d] of one dtype expected")
+    O = torch.empty_like(Q)
+    n_chunks = L // C
+    Ks = torch.empty(B, Hkv, n_chunks, d, dtype=Q.dtype, device=Q.device)
+    Vs = torch.empty_like(Ks)
+    lib = _lib.load()
+    cref = ctypes.byref(cache.struct) if cache is not None else None
+    _lib.check("eva_prefill",
+               lib.eva_prefill(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C, _dtype_code(Q),
+                               _ptr(Ks) if n_chunks else None, _ptr(Vs) if n_chunks else None, cref, _stream()))
+    if return_summaries:
+        return O, Ks, Vs
+    return O
+
+
+def cache_append(cache: Cache, k_new, v_new):
+    """Append one token per sequence: k_new, v_new [B, Hkv, d]."""
+    _require_device(k_new, v_new)
+    s = cache.struct
+    if tuple(k_new.shape) != (s.B, s.H_kv, s.d) or v_new.shape != k_new.shape or k_new.dtype != cache.dtype:
+        raise ValueError("k_new, v_new must be [B, Hkv, d] in the cache dtype")
+    _lib.check("eva_cache_append",
+               _lib.load().eva_cache_append(ctypes.byref(s), _ptr(k_new), _ptr(v_new), _stream()))
+
+
+def decode_step(cache: Cache, q, use_workspace: bool = True):
+    """Attention output of the last appended position: q [B, H, d] -> o [B, H, d]."""
+    _require_device(q)
+    s = cache.struct
+    if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
+        raise ValueError("q must be [B, H, d] in the cache dtype")
+    o = torch.empty_like(q)
+    ws = cache.workspace() if use_workspace else None
+    nbytes = ws.numel() * 4 if ws is not None else 0
+    _lib.check("eva_decode_step",
+               _lib.load().eva_decode_step(ctypes.byref(s), _ptr(q), _ptr(o), _ptr(ws), nbytes, _stream()))
+    return o

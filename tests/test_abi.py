@@ -1,0 +1,132 @@
+"""The C ABI library loads, exports every symbol include/eva.h declares, and
+rejects bad arguments with the documented status codes before touching the
+GPU (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2511_00576_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def header_functions():
+    with open(os.path.join(ROOT, "include", "eva.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eva_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = header_functions()
+    for fn in ("eva_build_summaries", "eva_prefill", "eva_decode_step", "eva_cache_append"):
+        assert fn in names
+    assert sorted(_lib.SYMBOLS) == names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert lib.eva_status_string(0) == b"ok"
+    for code in (-1, -2, -3, -4):
+        assert lib.eva_status_string(code) not in (b"ok", b"unknown status")
+    assert lib.eva_status_string(7) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
+
+
+def prefill_call(lib, **kw):
+    a = dict(Q=FAKE, K=FAKE, V=FAKE, O=FAKE, B=1, H=4, H_kv=2, L=64, d=64, W=8, C=4, dtype=_lib.EVA_BF16,
+             Ks=FAKE, Vs=FAKE, cache=None)
+    a.update(kw)
+    return lib.eva_prefill(a["Q"], a["K"], a["V"], a["O"], a["B"], a["H"], a["H_kv"], a["L"], a["d"], a["W"],
+                           a["C"], a["dtype"], a["Ks"], a["Vs"], a["cache"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=3, H_kv=2), _lib.EVA_ERR_INVALID),
+    (dict(W=0), _lib.EVA_ERR_INVALID),
+    (dict(C=0), _lib.EVA_ERR_INVALID),
+    (dict(L=0), _lib.EVA_ERR_INVALID),
+    (dict(B=0), _lib.EVA_ERR_INVALID),
+    (dict(Q=None), _lib.EVA_ERR_INVALID),
+    (dict(Ks=None), _lib.EVA_ERR_INVALID),
+    (dict(Q=ctypes.c_void_p(0x10008)), _lib.EVA_ERR_INVALID),
+    (dict(d=96), _lib.EVA_ERR_UNSUPPORTED),
+    (dict(d=256), _lib.EVA_ERR_UNSUPPORTED),
+    (dict(dtype=5), _lib.EVA_ERR_UNSUPPORTED),
+    (dict(C=100000), _lib.EVA_ERR_UNSUPPORTED),
+])
+def test_prefill_rejects(lib, kw, code):
+    assert prefill_call(lib, **kw) == code
+
+
+def make_cache(**kw):
+    a = dict(B=1, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, R=32, S_max=32, n_tok=0,
+             k_ring=0x10000, vt_ring=0x20000, k_sum=0x30000, vt_sum=0x40000)
+    a.update(kw)
+    return _lib.EvaCacheStruct(a["B"], a["H"], a["H_kv"], a["d"], a["W"], a["C"], a["dtype"], a["R"], a["S_max"],
+                               a["n_tok"], a["k_ring"], a["vt_ring"], a["k_sum"], a["vt_sum"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(R=16), _lib.EVA_ERR_INVALID),          # not a multiple of 32
+    (dict(R=40), _lib.EVA_ERR_INVALID),
+    (dict(W=30, C=4), _lib.EVA_ERR_CAPACITY),     # R = 32 < W + C - 1 = 33
+    (dict(S_max=0), _lib.EVA_ERR_INVALID),
+    (dict(k_ring=0), _lib.EVA_ERR_INVALID),
+    (dict(vt_sum=0x40004), _lib.EVA_ERR_INVALID),  # misaligned
+    (dict(H=3), _lib.EVA_ERR_INVALID),
+    (dict(d=80), _lib.EVA_ERR_UNSUPPORTED),
+])
+def test_cache_validation(lib, kw, code):
+    c = make_cache(**kw)
+    assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == code
+    assert c.n_tok == 0
+
+
+def test_decode_needs_a_token(lib):
+    c = make_cache()
+    assert lib.eva_decode_step(ctypes.byref(c), FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert lib.eva_decode_workspace_bytes(ctypes.byref(c)) == 0
+
+
+def test_decode_rejects_fp32_cache(lib):
+    c = make_cache(dtype=_lib.EVA_F32, n_tok=5)
+    assert lib.eva_decode_step(ctypes.byref(c), FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+
+
+def test_append_capacity(lib):
+    # W = 8, C = 4: position p makes chunk s(p)-1 visible when s(p) grows;
+    # with S_max = 32 the 33rd summary (index 32) does not fit.
+    p = 8 - 1 + 33 * 4  # s(p) = floor((p - 7) / 4) = 33 -> new summary index 32
+    c = make_cache(n_tok=p)
+    assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_CAPACITY
+    assert c.n_tok == p
+
+
+def test_prefill_cache_mismatch(lib):
+    c = make_cache(W=16)
+    assert prefill_call(lib, cache=ctypes.byref(c)) == _lib.EVA_ERR_INVALID
+    c = make_cache(S_max=32)
+    assert prefill_call(lib, L=4 * 33, cache=ctypes.byref(c)) == _lib.EVA_ERR_CAPACITY
+
+
+def test_summaries_rejects(lib):
+    f = lib.eva_build_summaries
+    assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 64, 64, 0, 0, None) == _lib.EVA_ERR_INVALID
+    assert f(None, FAKE, FAKE, FAKE, 1, 1, 64, 64, 4, 0, None) == _lib.EVA_ERR_INVALID
+    assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 64, 32, 4, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    # fewer tokens than one chunk: nothing to do, no pointer needed
+    assert f(None, None, None, None, 1, 1, 3, 64, 4, 0, None) == _lib.EVA_OK

@@ -1,0 +1,132 @@
+"""GPU parity of the decode cache path: eva_prefill with a cache, then
+eva_cache_append + eva_decode_step, against oracle rows of the same tokens.
+
+Decode of position p must equal row p of a prefill over the whole history
+(same window, same summaries); multi-step runs cross chunk boundaries and
+wrap the ring several times.  Caches pre-filled with NaN prove that no stale
+slot or unused summary row leaks into an output.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_00576_amd import eva, inputs
+from parity import assert_parity, to64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    eva._lib.load()
+
+
+def oracle_row(qrow, K, V, p, W, C):
+    """Oracle output of the query at position p; K, V hold positions 0..p."""
+    Ks, Vs = oracle.summaries(K[: p + 1], V[: p + 1], C)
+    return oracle.attend_rows(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C)[0]
+
+
+def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1):
+    """Prefill L0 tokens (if L0 > 0) into a cache, then append + decode `steps`
+    tokens; compare every `check_every`-th decode output with the oracle."""
+    print(f"decode B{B} H{H}/{Hkv} d{d} W{W} C{C} L0={L0} steps={steps} fill={fill} ws={use_ws}", flush=True)
+    dtype = torch.bfloat16
+    total = L0 + steps
+    q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
+    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=total, dtype=dtype, fill=fill)
+    if L0 > 0:
+        eva.prefill(q[:, :, :L0].contiguous().cuda(), k[:, :, :L0].contiguous().cuda(),
+                    v[:, :, :L0].contiguous().cuda(), W, C, cache=cache)
+        assert cache.n_tok == L0
+    k64, v64 = to64(k), to64(v)
+    worst = 0.0
+    for t in range(steps):
+        p = L0 + t
+        eva.cache_append(cache, k[:, :, p].contiguous().cuda(), v[:, :, p].contiguous().cuda())
+        o = eva.decode_step(cache, q[:, :, p].contiguous().cuda(), use_workspace=use_ws)
+        assert cache.n_tok == p + 1
+        if t % check_every and t != steps - 1:
+            continue
+        torch.cuda.synchronize()
+        got = to64(o)
+        for b in range(B):
+            for h in range(H):
+                g = h // (H // Hkv)
+                ref = oracle_row(to64(q[b, h, p]), k64[b, g], v64[b, g], p, W, C)
+                worst = max(worst, assert_parity(got[b, h][None], ref[None], dtype, f"p={p} b{b} h{h}"))
+    return cache
+
+
+def test_decode_after_prefill_matches_next_row():
+    run_sequence(2, 8, 2, 128, 64, 16, L0=300, steps=1, seed=21)
+
+
+def test_decode_many_steps_cross_chunks_and_ring_wraps():
+    # R = 96 slots for W = 64, C = 16: 260 steps wrap the ring ~3 times and
+    # make 16 summaries due during decode.
+    run_sequence(1, 4, 2, 128, 64, 16, L0=100, steps=260, seed=22, check_every=7)
+
+
+def test_decode_from_empty_cache():
+    run_sequence(1, 4, 1, 64, 24, 8, L0=0, steps=120, seed=23, check_every=5)
+
+
+def test_decode_nan_filled_cache():
+    run_sequence(2, 4, 2, 128, 40, 8, L0=77, steps=60, seed=24, fill=float("nan"), check_every=3)
+
+
+@pytest.mark.parametrize("H,Hkv", [(2, 2), (32, 2), (48, 1)])
+def test_decode_head_groupings(H, Hkv):
+    # G = 1, G = 16 (one full column block), G = 48 (three head groups)
+    run_sequence(1, H, Hkv, 128, 48, 16, L0=200, steps=20, seed=25, check_every=6)
+
+
+@pytest.mark.parametrize("use_ws", [True, False])
+def test_decode_split_and_unsplit(use_ws):
+    # B * Hkv = 2 units: with a workspace the rows are split over many workgroups
+    run_sequence(1, 8, 2, 128, 512, 64, L0=3000, steps=3, seed=26, use_ws=use_ws)
+
+
+def test_cache_summaries_match_oracle():
+    B, H, Hkv, d, W, C, L0, steps = 1, 2, 2, 64, 32, 8, 50, 90
+    cache = run_sequence(B, H, Hkv, d, W, C, L0=L0, steps=steps, seed=27, check_every=1000)
+    q, k, v = inputs.qkv(B, H, Hkv, L0 + steps, d, torch.bfloat16, seed=27)
+    n_sum = oracle.visible_summaries(L0 + steps - 1, W, C)
+    for g in range(Hkv):
+        rK, rV = oracle.summaries(k[0, g], v[0, g], C)
+        got_k = to64(cache.k_sum[0, g, :n_sum])
+        got_v = to64(cache.vt_sum[0, g, :, :n_sum]).T
+        assert_parity(got_k, rK[:n_sum], torch.bfloat16, "k_sum")
+        assert_parity(got_v, rV[:n_sum], torch.bfloat16, "vt_sum")
+
+
+def test_decode_workload_full_size_sampled():
+    w = inputs.DECODE_BF16
+    print(f"full-size {w.name}", flush=True)
+    L0 = w.context
+    _, k, v = inputs.qkv(w.B, 1, w.Hkv, L0 + 1, w.d, w.dtype, seed=w.seed)
+    # history queries only shape the history's prefill outputs, which decode
+    # never reads; draw them on the device
+    gen = torch.Generator(device="cuda").manual_seed(w.seed)
+    qh = torch.randn(w.B, w.H, L0, w.d, generator=gen, device="cuda").to(w.dtype)
+    q_new = inputs.normal((w.B, w.H, w.d), w.seed + 100, w.dtype)
+    cache = eva.Cache(w.B, w.H, w.Hkv, w.d, w.W, w.C, max_tokens=L0 + 1, dtype=w.dtype)
+    eva.prefill(qh, k[:, :, :L0].contiguous().cuda(), v[:, :, :L0].contiguous().cuda(), w.W, w.C, cache=cache)
+    del qh
+    eva.cache_append(cache, k[:, :, L0].contiguous().cuda(), v[:, :, L0].contiguous().cuda())
+    o = eva.decode_step(cache, q_new.cuda())
+    torch.cuda.synchronize()
+    p = L0
+    assert oracle.visible_summaries(p, w.W, w.C) == 60
+    got = to64(o)
+    for b in (0, 17, w.B - 1):
+        for g in (0, w.Hkv - 1):
+            K64, V64 = to64(k[b, g]), to64(v[b, g])
+            Ks, Vs = oracle.summaries(K64, V64, w.C)
+            heads = list(range(g * (w.H // w.Hkv), (g + 1) * (w.H // w.Hkv)))
+            ref = oracle.attend_rows(to64(q_new[b, heads]), np.full(len(heads), p), K64, V64, Ks, Vs, w.W, w.C)
+            assert_parity(got[b, heads], ref, w.dtype, f"b{b} g{g}")

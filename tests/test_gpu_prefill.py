@@ -1,0 +1,155 @@
+"""GPU parity of eva_build_summaries and eva_prefill against the fp64 oracle.
+
+Small shapes are compared element by element over every row (several query
+tiles, ragged tails, GQA packings, degenerate windows and chunks).  The
+LLM-shaped workloads are run at full size in the launch configuration the
+benchmark times and compared on sampled rows around every boundary.  Mask
+probes (zero Q/K with one-hot values, and dominant spiked keys) make a token
+wrongly included or excluded cost far more than the bf16 tolerance.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_00576_amd import eva, inputs
+from parity import assert_parity, edge_rows, oracle_sampled, to64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    eva._lib.load()
+
+
+def cuda(*ts):
+    return [t.cuda() for t in ts]
+
+
+def check_prefill(B, H, Hkv, L, d, W, C, dtype, seed, maker=inputs.qkv):
+    print(f"prefill B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C} {dtype} seed{seed} {maker.__name__}", flush=True)
+    q, k, v = maker(B, H, Hkv, L, d, dtype=dtype, seed=seed)
+    O, Ks, Vs = eva.prefill(*cuda(q, k, v), W, C, return_summaries=True)
+    torch.cuda.synchronize()
+    ref, rKs, rVs = oracle.prefill(q, k, v, W, C, return_summaries=True)
+    err = assert_parity(to64(O), ref, dtype, "O")
+    assert_parity(to64(Ks), rKs, dtype, "Ksum")
+    assert_parity(to64(Vs), rVs, dtype, "Vsum")
+    return err
+
+
+SMALL = [
+    # B, H, Hkv, L, d, W, C
+    (1, 2, 2, 256, 64, 32, 16),     # the tiny fp32 workload
+    (2, 4, 2, 300, 128, 50, 7),     # ragged tail, odd chunk, G = 2
+    (1, 8, 2, 517, 64, 64, 32),     # G = 4, ragged
+    (1, 16, 2, 400, 128, 96, 16),   # G = 8: two head groups per kv head
+    (1, 3, 1, 333, 64, 40, 8),      # G = 3: one head per workgroup
+    (1, 2, 1, 200, 128, 1, 3),      # W = 1: self plus summaries only
+    (1, 2, 2, 150, 64, 200, 16),    # W >= L: exact causal attention
+    (1, 2, 2, 130, 64, 20, 1),      # C = 1: exact causal attention
+    (1, 2, 2, 100, 128, 10, 128),   # C > L: no summaries, sliding window
+    (1, 2, 2, 1, 64, 4, 4),         # one token
+    (2, 2, 1, 17, 128, 5, 3),       # shorter than one query tile
+    (1, 4, 4, 1030, 128, 256, 64),  # many summary blocks + window blocks
+]
+
+
+@pytest.mark.parametrize("shape", SMALL)
+def test_prefill_f32(shape):
+    check_prefill(*shape, torch.float32, seed=11)
+
+
+@pytest.mark.parametrize("shape", SMALL)
+def test_prefill_bf16(shape):
+    check_prefill(*shape, torch.bfloat16, seed=12)
+
+
+def test_tiny_f32_workload():
+    w = inputs.TINY_F32
+    check_prefill(w.B, w.H, w.Hkv, w.L, w.d, w.W, w.C, w.dtype, seed=w.seed)
+
+
+@pytest.mark.parametrize("W,C", [(256, 64), (512, 128), (200, 48)])
+def test_prefill_f32_llm_head_shape(W, C):
+    # fp32 instantiation of the same tiling at LLM head shapes: pins every
+    # mask boundary to 1e-5 (bf16 tolerance is too loose for a one-token slip).
+    check_prefill(1, 4, 1, 4096, 128, W, C, torch.float32, seed=13)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("W,C", [(256, 64), (77, 13), (512, 128)])
+def test_mask_probe_one_hot_values(dtype, W, C):
+    check_prefill(1, 4, 2, 2048, 128, W, C, dtype, seed=14, maker=inputs.needle_qkv)
+
+
+@pytest.mark.parametrize("W,C", [(256, 64), (100, 20)])
+def test_mask_probe_spiked_keys(W, C):
+    check_prefill(2, 4, 2, 1500, 128, W, C, torch.bfloat16, seed=15, maker=inputs.spike_qkv)
+
+
+def test_prefill_deterministic():
+    q, k, v = cuda(*inputs.qkv(2, 8, 2, 777, 128, torch.bfloat16, seed=16))
+    a = eva.prefill(q, k, v, 100, 16)
+    b = eva.prefill(q, k, v, 100, 16)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("L,C", [(1000, 7), (64, 64), (63, 64), (4096, 256)])
+@pytest.mark.parametrize("d", [64, 128])
+def test_summaries(L, C, d):
+    for dtype in (torch.float32, torch.bfloat16):
+        _, k, v = inputs.qkv(2, 1, 3, L, d, dtype, seed=17)
+        Ks, Vs = eva.build_summaries(*cuda(k, v), C)
+        torch.cuda.synchronize()
+        assert Ks.shape == (2, 3, L // C, d)
+        for b in range(2):
+            for g in range(3):
+                rK, rV = oracle.summaries(k[b, g], v[b, g], C)
+                assert_parity(to64(Ks[b, g]), rK, dtype, "Ksum")
+                assert_parity(to64(Vs[b, g]), rV, dtype, "Vsum")
+
+
+FULL = [inputs.LLM_BF16, inputs.GQA_BF16, inputs.LONG_BF16]
+
+
+@pytest.mark.parametrize("w", FULL, ids=lambda w: w.name.split()[0])
+def test_full_size_sampled(w):
+    print(f"full-size {w.name}", flush=True)
+    q, k, v = inputs.workload_qkv(w)
+    O = eva.prefill(*cuda(q, k, v), w.W, w.C)
+    torch.cuda.synchronize()
+    rows = edge_rows(w.L, w.W, w.C, extra=48, seed=w.seed)
+    heads = [(0, 0), (w.B - 1, w.H - 1), (w.B // 2, w.H // 3)]
+    ref = oracle_sampled(q, k, v, w.W, w.C, heads, rows)
+    for (b, h), r in ref.items():
+        got = to64(O[b, h, torch.from_numpy(rows)])
+        assert_parity(got, r, w.dtype, f"{w.name} b{b} h{h}")
+
+
+@pytest.mark.parametrize("C", [64, 128])
+def test_long_context_chunk_sweep_sampled(C):
+    w = inputs.LONG_BF16
+    print(f"long-context sweep C={C}", flush=True)
+    q, k, v = inputs.workload_qkv(w)
+    O = eva.prefill(*cuda(q, k, v), w.W, C)
+    torch.cuda.synchronize()
+    rows = edge_rows(w.L, w.W, C, extra=32, seed=C)
+    ref = oracle_sampled(q, k, v, w.W, C, [(0, 5), (0, 30)], rows)
+    for (b, h), r in ref.items():
+        assert_parity(to64(O[b, h, torch.from_numpy(rows)]), r, w.dtype, f"C={C} h{h}")
+
+
+def test_full_size_mask_probe():
+    # dominant spiked keys at the LLM workload's window/chunk geometry: a spike
+    # entering or leaving a window moves that row by O(1)
+    w = inputs.LLM_BF16
+    q, k, v = inputs.spike_qkv(1, 2, 2, w.L, w.d, w.dtype, seed=18)
+    O = eva.prefill(*cuda(q, k, v), w.W, w.C)
+    torch.cuda.synchronize()
+    ref = oracle.prefill(q, k, v, w.W, w.C)
+    assert_parity(to64(O), ref, w.dtype, "needles")
