@@ -1,0 +1,312 @@
+#!/usr/bin/env python
+"""EVA attention benchmark on one MI355X (gfx950).
+
+Step = one pass of the whole hot path over one batch of the LLM-shaped
+prefill workload (B=8, H=H_kv=32, L=4096, d=128, W=256, C=64, bf16):
+  summaries -> fused window+summary prefill -> cache fill -> append -> decode.
+Each part is bracketed by HIP events on the stream the kernels run on.
+value = algorithmic prefill FLOPs per step / step time (TFLOP/s).
+
+The decode workload (64 sequences, H=32, H_kv=8, d=128, 8192-token context
+held as a 512-token window plus 60 chunk summaries of 128 tokens) is timed in
+the same run: append + decode per token, over 4 rotating caches so the
+151 MB working set is read from HBM rather than the 256 MB Infinity Cache;
+the iterations are captured in one HIP graph so host launch latency does not
+enter the kernel timing.
+
+Prints ONE JSON line.  Algorithmic counts:
+  prefill FLOPs  = B*H*4d*sum_n (w(n) + s(n))      (QK^T and PV of attended keys)
+  prefill bytes  = Q + K + V + Ksum + Vsum + O     (fused attention kernel)
+  summary bytes  = K + V + Ksum + Vsum
+  decode bytes   = B*H_kv*(w + s)*d*2*e + q + o
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
+N_CACHES = 4
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
+DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
+
+
+def attended(L, W, C):
+    """sum_n (w(n) + s(n)) over n < L."""
+    import numpy as np
+    n = np.arange(L, dtype=np.int64)
+    w = np.minimum(W, n + 1)
+    start = n - W + 1
+    s = np.where(start > 0, start // C, 0)
+    return int((w + s).sum())
+
+
+def prefill_counts(B, H, Hkv, L, d, W, C, e):
+    nc = L // C
+    flops = B * H * 4 * d * attended(L, W, C)
+    attn_bytes = (2 * B * H * L * d + 2 * B * Hkv * L * d + 2 * B * Hkv * nc * d) * e
+    summ_bytes = (2 * B * Hkv * L * d + 2 * B * Hkv * nc * d) * e
+    return flops, attn_bytes, summ_bytes
+
+
+def decode_counts(B, H, Hkv, d, W, C, p, e):
+    w = min(W, p + 1)
+    s = max(0, p - W + 1) // C
+    return B * H * 4 * d * (w + s), B * Hkv * (w + s) * d * 2 * e + 2 * B * H * d * e
+
+
+def source_sha(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(name, sources):
+    """HBM bytes per launch from a committed counter summary, or None when
+    missing or taken on a different kernel source."""
+    path = os.path.join(PROFILE_DIR, name)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line:
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha") != source_sha(sources):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w):
+    """The oracle on a bounded sample of the prefill workload, on this host."""
+    import oracle
+    from paper_2511_00576_amd import inputs
+
+    n_heads = int(os.environ.get("EVA_ORACLE_HEADS", "16"))
+    q, k, v = inputs.workload_qkv(w)
+    qs, ks, vs = q[:1, :n_heads], k[:1, :n_heads], v[:1, :n_heads]
+    t0 = time.perf_counter()
+    oracle.prefill(qs, ks, vs, w.W, w.C)
+    dt = time.perf_counter() - t0
+    flops = n_heads * 4 * w.d * attended(w.L, w.W, w.C)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"batch 0, heads 0-{n_heads - 1} of {w.name} (all {w.L} rows, summaries included), "
+                      f"{dt:.2f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--decode-iters", type=int, default=64, help="graph-captured decode tokens (x4 caches)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device-to-device copy (counter scaling for profiles)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path. The EVA step shards "
+              "by (batch, kv head) with no exchange; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2511_00576_amd import eva, inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    eva._lib.load()
+    dev = torch.device("cuda:0")
+    w = inputs.LLM_BF16
+    B, H, Hkv, L, d, W, C = w.B, w.H, w.Hkv, w.L, w.d, w.W, w.C
+    e = 2
+
+    print(f"# prefill workload {w.name}: generating inputs", file=sys.stderr, flush=True)
+    q, k, v = (t.to(dev) for t in inputs.workload_qkv(w))
+    Ks = torch.empty(B, Hkv, L // C, d, dtype=w.dtype, device=dev)
+    Vs = torch.empty_like(Ks)
+    O = torch.empty_like(q)
+    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L + 1, dtype=w.dtype, device=dev)
+    kn = inputs.normal((B, Hkv, d), w.seed + 100, w.dtype).to(dev)
+    vn = inputs.normal((B, Hkv, d), w.seed + 101, w.dtype).to(dev)
+    qn = inputs.normal((B, H, d), w.seed + 102, w.dtype).to(dev)
+    od = torch.empty_like(qn)
+
+    def step(ev=None):
+        if ev: ev[0].record()
+        eva.build_summaries(k, v, C, out=(Ks, Vs))
+        if ev: ev[1].record()
+        eva.prefill_attention(q, k, v, Ks, Vs, W, C, out=O)
+        if ev: ev[2].record()
+        eva.cache_fill(cache, k, v, Ks, Vs)
+        eva.cache_append(cache, kn, vn)
+        if ev: ev[3].record()
+        eva.decode_step(cache, qn, out=od)
+        if ev: ev[4].record()
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 29, dtype=torch.float16, device=dev)  # 1 GiB
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    print(f"# warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+
+    def avg(i, j):
+        return sum(ev[i].elapsed_time(ev[j]) for ev in evs) / len(evs)
+
+    ms_summ, ms_attn, ms_fill_app, ms_dec = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
+    flops, attn_bytes, summ_bytes = prefill_counts(B, H, Hkv, L, d, W, C, e)
+    attn_gbs = attn_bytes / (ms_attn * 1e-3) / 1e9
+    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
+    print(f"# step {ms_step:.3f} ms: summaries {ms_summ:.3f}, attention {ms_attn:.3f}, fill+append "
+          f"{ms_fill_app:.3f}, decode {ms_dec:.3f}", file=sys.stderr, flush=True)
+
+    traffic = read_traffic("prefill_attention_llm-bf16_traffic.txt", PREFILL_SOURCES)
+    out = {
+        "metric": "EVA prefill TFLOP/s (% MFMA peak); decode tokens/s + HBM GB/s (% peak)",
+        "value": flops / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic N(0,1), seeded",
+        "config": {"workload": w.name, "B": B, "H": H, "H_kv": Hkv, "L": L, "d": d, "W": W, "C": C,
+                   "step": "summaries + fused prefill + cache fill + append + decode"},
+        "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": attn_gbs / PEAK_HBM_GBS,
+                     "traffic": traffic,
+                     "kernel": "prefill_kernel<128, bf16> (eva_prefill_attention)"},
+        "prefill": {"attention_ms": ms_attn, "attention_tflops": attn_tflops,
+                    "attention_mfma_frac": attn_tflops / PEAK_BF16_TFLOPS,
+                    "summaries_ms": ms_summ, "summaries_gbs": summ_bytes / (ms_summ * 1e-3) / 1e9,
+                    "fill_append_ms": ms_fill_app, "decode_ms": ms_dec,
+                    "alg_flops": flops, "alg_bytes_attention": attn_bytes, "alg_bytes_summaries": summ_bytes},
+    }
+    del q, k, v, O, Ks, Vs, cache
+
+    if not args.no_decode:
+        out["decode"] = bench_decode(args, torch, eva, inputs, dev)
+
+    if not args.no_cpu_baseline:
+        print("# oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+def bench_decode(args, torch, eva, inputs, dev):
+    dw = inputs.DECODE_BF16
+    B, H, Hkv, d, W, C, ctx = dw.B, dw.H, dw.Hkv, dw.d, dw.W, dw.C, dw.context
+    print(f"# decode workload {dw.name}: building {N_CACHES} caches", file=sys.stderr, flush=True)
+    gen = torch.Generator(device=dev).manual_seed(dw.seed)
+    qh = torch.randn(B, H, ctx, d, generator=gen, device=dev).to(dw.dtype)
+    kh = torch.randn(B, Hkv, ctx, d, generator=gen, device=dev).to(dw.dtype)
+    vh = torch.randn(B, Hkv, ctx, d, generator=gen, device=dev).to(dw.dtype)
+    caches = [eva.Cache(B, H, Hkv, d, W, C, max_tokens=ctx + 1, dtype=dw.dtype, device=dev) for _ in range(N_CACHES)]
+    eva.prefill(qh, kh, vh, W, C, cache=caches[0])
+    del qh, kh, vh
+    for c in caches[1:]:
+        for name in ("k_ring", "vt_ring", "k_sum", "vt_sum"):
+            getattr(c, name).copy_(getattr(caches[0], name))
+        c.struct.n_tok = caches[0].struct.n_tok
+    kn = torch.randn(B, Hkv, d, generator=gen, device=dev).to(dw.dtype)
+    vn = torch.randn(B, Hkv, d, generator=gen, device=dev).to(dw.dtype)
+    qn = torch.randn(B, H, d, generator=gen, device=dev).to(dw.dtype)
+    od = torch.empty_like(qn)
+    torch.cuda.synchronize()
+
+    def token(c):
+        c.struct.n_tok = ctx  # re-append position ctx: same work every iteration
+        eva.cache_append(c, kn, vn)
+        eva.decode_step(c, qn, out=od)
+
+    def decode_only(c):
+        eva.decode_step(c, qn, out=od)
+
+    # eager reference for the graph replays
+    token(caches[0])
+    ref = od.clone()
+    iters = args.decode_iters * N_CACHES
+    stream = torch.cuda.Stream()
+    graphs = {}
+    for name, fn in (("token", token), ("decode", decode_only)):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(iters):
+                fn(caches[i % N_CACHES])
+        graphs[name] = g
+    for c in caches:
+        c.struct.n_tok = ctx + 1
+    res = {}
+    for name, g in graphs.items():
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        reps = 3
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / (reps * iters)
+    graph_ok = bool(torch.equal(od, ref))
+    p = ctx
+    flops, nbytes = decode_counts(B, H, Hkv, d, W, C, p, 2)
+    dec_gbs = nbytes / (res["decode"] * 1e-3) / 1e9
+    traffic = read_traffic("decode_bf16_traffic.txt", DECODE_SOURCES)
+    print(f"# decode {res['decode'] * 1e3:.1f} us/step ({dec_gbs:.0f} GB/s), append+decode "
+          f"{res['token'] * 1e3:.1f} us/token-step", file=sys.stderr, flush=True)
+    return {
+        "workload": dw.name,
+        "tokens_per_s": B / (res["token"] * 1e-3),
+        "us_per_token_step": res["token"] * 1e3,
+        "decode_us": res["decode"] * 1e3,
+        "hbm_gbs": dec_gbs,
+        "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": dec_gbs / PEAK_HBM_GBS, "traffic": traffic,
+                     "kernel": "decode_kernel<128> (eva_decode_step)"},
+        "alg_bytes": nbytes,
+        "alg_flops": flops,
+        "rotating_caches": N_CACHES,
+        "graph_matches_eager": graph_ok,
+    }
+
+
+if __name__ == "__main__":
+    main()

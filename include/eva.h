@@ -121,6 +121,27 @@ int eva_prefill(const void* Q, const void* K, const void* V, void* O,
                 void* Ksum, void* Vsum, eva_cache* cache, void* stream);
 
 /*
+ * The fused window + summary attention kernel alone (section "FlashEVA"),
+ * given summaries already built by eva_build_summaries for the same K, V, C:
+ * Ksum, Vsum [B][H_kv][L / C][d].  eva_prefill = eva_build_summaries +
+ * eva_prefill_attention (+ eva_cache_fill).  Summary pointers may be NULL
+ * when no row sees a summary (L - W < C).
+ * Errors: as eva_prefill (no cache).
+ */
+int eva_prefill_attention(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                          void* O, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                          void* stream);
+
+/*
+ * Load a decode cache from a prefilled sequence of L tokens: the last
+ * min(L, R) keys/values go to ring slots p mod R and the L / C summaries
+ * (as built by eva_build_summaries) to the summary arrays; n_tok becomes L.
+ * Errors: INVALID (malformed cache, null pointers), CAPACITY (S_max < L / C).
+ */
+int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                   int L, void* stream);
+
+/*
  * Append one token per sequence: k_new, v_new [B][H_kv][d].  The token takes
  * position p = cache->n_tok.  If that position makes chunk S = s(p) - 1 newly
  * visible (s(p) > s(p - 1)), its summary is built from the ring first, then

@@ -5,4 +5,5 @@ in include/eva.h); `eva` is the torch-facing binding, `inputs` the seeded
 synthetic workloads.  Importing the package does not load the library; the
 first call does, and raises if it is not built.
 """
-from .eva import Cache, build_summaries, cache_append, decode_step, prefill  # noqa: F401
+from .eva import (Cache, build_summaries, cache_append, cache_fill, decode_step, prefill,  # noqa: F401
+                  prefill_attention)

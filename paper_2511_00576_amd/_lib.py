@@ -21,6 +21,8 @@ EVA_F32 = 1
 SYMBOLS = (
     "eva_build_summaries",
     "eva_prefill",
+    "eva_prefill_attention",
+    "eva_cache_fill",
     "eva_cache_append",
     "eva_decode_step",
     "eva_decode_workspace_bytes",
@@ -56,6 +58,10 @@ def load():
     lib.eva_build_summaries.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
     lib.eva_prefill.restype = i
     lib.eva_prefill.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
+    lib.eva_prefill_attention.restype = i
+    lib.eva_prefill_attention.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    lib.eva_cache_fill.restype = i
+    lib.eva_cache_fill.argtypes = [cp, vp, vp, vp, vp, i, vp]
     lib.eva_cache_append.restype = i
     lib.eva_cache_append.argtypes = [cp, vp, vp, vp]
     lib.eva_decode_step.restype = i

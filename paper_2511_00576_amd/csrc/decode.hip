@@ -25,34 +25,51 @@ namespace {
 // ---------------------------------------------------------------------------
 // cache fill
 // ---------------------------------------------------------------------------
+// One workgroup moves one 32-row tile: 32 ring positions (32-aligned, so
+// they occupy 32 consecutive slots) or 32 summaries.  Keys are copied row by
+// row; values go through LDS so the transposed store writes 32 consecutive
+// slots (64 B in bf16) per feature row instead of scattered elements.
 template <int D, typename T>
-__global__ void cache_fill_kernel(CacheView c, const T* __restrict__ K, const T* __restrict__ V,
-                                  const T* __restrict__ Ks, const T* __restrict__ Vs, int L, int n_chunks) {
+__global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* __restrict__ K, const T* __restrict__ V,
+                                                         const T* __restrict__ Ks, const T* __restrict__ Vs, int L,
+                                                         int n_chunks, int ring_tiles) {
+    __shared__ T tile[32][D + 2];
     const size_t bg = blockIdx.y;
     const int first = max(0, L - c.R);
-    const int rows = L - first;
-    T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
-    T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
-    T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
-    T* vs = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
-    const T* K0 = K + bg * (size_t)L * D;
-    const T* V0 = V + bg * (size_t)L * D;
-    const T* Ks0 = Ks + bg * (size_t)n_chunks * D;
-    const T* Vs0 = Vs + bg * (size_t)n_chunks * D;
-    const long long total = (long long)(rows + n_chunks) * D;
-    for (long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x; e < total;
-         e += (long long)gridDim.x * blockDim.x) {
-        const int r = (int)(e / D), d = (int)(e % D);
-        if (r < rows) {
-            const int pos = first + r;
-            const int slot = pos % c.R;
-            kr[(size_t)slot * D + d] = K0[(size_t)pos * D + d];
-            vr[(size_t)d * c.R + slot] = V0[(size_t)pos * D + d];
-        } else {
-            const int s = r - rows;
-            ks[(size_t)s * D + d] = Ks0[(size_t)s * D + d];
-            vs[(size_t)d * c.S_max + s] = Vs0[(size_t)s * D + d];
-        }
+    const bool ring = (int)blockIdx.x < ring_tiles;
+    int r0, r1, dst0, ld_dst;  // source rows [r0, r1), destination slot/index of r0
+    const T *src_k, *src_v;
+    T *dst_k, *dst_vt;
+    if (ring) {
+        const int p0 = (first / 32 + (int)blockIdx.x) * 32;
+        r0 = max(p0, first);
+        r1 = min(p0 + 32, L);
+        dst0 = r0 % c.R;
+        ld_dst = c.R;
+        src_k = K + bg * (size_t)L * D;
+        src_v = V + bg * (size_t)L * D;
+        dst_k = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
+        dst_vt = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
+    } else {
+        r0 = ((int)blockIdx.x - ring_tiles) * 32;
+        r1 = min(r0 + 32, n_chunks);
+        dst0 = r0;
+        ld_dst = c.S_max;
+        src_k = Ks + bg * (size_t)n_chunks * D;
+        src_v = Vs + bg * (size_t)n_chunks * D;
+        dst_k = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
+        dst_vt = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+    }
+    const int rows = r1 - r0;
+    for (int e = threadIdx.x; e < rows * D; e += blockDim.x) {
+        const int r = e / D, d = e % D;
+        dst_k[(size_t)(dst0 + r) * D + d] = src_k[(size_t)(r0 + r) * D + d];
+        tile[r][d] = src_v[(size_t)(r0 + r) * D + d];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < rows * D; e += blockDim.x) {
+        const int d = e / rows, r = e % rows;
+        dst_vt[(size_t)d * ld_dst + dst0 + r] = tile[r][d];
     }
 }
 
@@ -188,20 +205,22 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
             for (int dc = 0; dc < NDC; ++dc) s[kb] = mfma_bf16(ka[kb][dc], qf[dc], s[kb]);
         }
         if (!full) {
+            // valid chunk keys are [key_lo, key_hi]: unsigned range test, no branches
+            const unsigned span = (unsigned)(key_hi - key_lo);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int key = g * 8 + kb * 4 + i;
-                    if (key < key_lo || key > key_hi) s[kb][i] = -INFINITY;
+                    const unsigned rel = (unsigned)(g * 8 + kb * 4 + i - key_lo);
+                    s[kb][i] = rel <= span ? s[kb][i] : -INFINITY;
                 }
             // stale ring slots may hold any bit pattern: zero their values
 #pragma unroll
             for (int db = 0; db < NDB; ++db)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const int key = g * 8 + j;
-                    if (key < key_lo || key > key_hi) va[db][j] = (bf16)0.f;
+                    const unsigned rel = (unsigned)(g * 8 + j - key_lo);
+                    va[db][j] = rel <= span ? va[db][j] : (bf16)0.f;
                 }
         }
         const float bias = is_sum ? a.log2C : 0.f;
@@ -316,11 +335,13 @@ template <int D, typename T>
 hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,
                              int L, hipStream_t stream) {
     const int n_chunks = L / c.C;
-    const int rows = min(L, c.R) + n_chunks;
-    const int per_bg = (rows * D + 255) / 256;
-    dim3 grid(min(per_bg, 64), c.B * c.Hkv);
+    const int first = max(0, L - c.R);
+    const int ring_tiles = (L - 1) / 32 - first / 32 + 1;
+    const int sum_tiles = (n_chunks + 31) / 32;
+    dim3 grid(ring_tiles + sum_tiles, c.B * c.Hkv);
     hipLaunchKernelGGL((cache_fill_kernel<D, T>), grid, dim3(256), 0, stream, c, static_cast<const T*>(K),
-                       static_cast<const T*>(V), static_cast<const T*>(Ks), static_cast<const T*>(Vs), L, n_chunks);
+                       static_cast<const T*>(V), static_cast<const T*>(Ks), static_cast<const T*>(Vs), L, n_chunks,
+                       ring_tiles);
     return hipGetLastError();
 }
 

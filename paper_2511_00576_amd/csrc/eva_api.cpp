@@ -135,31 +135,17 @@ int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum, in
     }));
 }
 
-int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
-                int C, int dtype, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
+int eva_prefill_attention(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                          int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
-    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
-    if ((long long)B * H_kv > 65535) return EVA_ERR_UNSUPPORTED;
     if (!Q || !K || !V || !O) return EVA_ERR_INVALID;
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return EVA_ERR_INVALID;
     const int n_chunks = L / C;
-    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
-    if (cache) {
-        st = check_cache(cache);
-        if (st != EVA_OK) return st;
-        if (cache->B != B || cache->H != H || cache->H_kv != H_kv || cache->d != d || cache->W != W ||
-            cache->C != C || cache->dtype != dtype)
-            return EVA_ERR_INVALID;
-        if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
-    }
-
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = dispatch(d, dtype, [&](auto dd, auto t) {
-        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, s);
-    });
-    if (e != hipSuccess) return EVA_ERR_HIP;
+    // a row sees summaries only when some chunk lies fully before its window
+    if (visible_summaries(L - 1, W, C) > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum)))
+        return EVA_ERR_INVALID;
 
     eva::PrefillParams p;
     p.Q = Q;
@@ -185,19 +171,54 @@ int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int
     p.n_tiles = (int)tiles;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
-    e = dispatch(d, dtype, [&](auto dd, auto t) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
         return eva::launch_prefill<decltype(dd)::value, decltype(t)>(p, s);
+    }));
+}
+
+int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum, int L,
+                   void* stream) {
+    int st = check_cache(cache);
+    if (st != EVA_OK) return st;
+    if (L < 1 || !K || !V) return EVA_ERR_INVALID;
+    const int n_chunks = L / cache->C;
+    if (n_chunks > 0 && (!Ksum || !Vsum)) return EVA_ERR_INVALID;
+    if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
+    eva::CacheView v = view_of(cache);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
+        return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, s);
     });
     if (e != hipSuccess) return EVA_ERR_HIP;
+    cache->n_tok = L;
+    return EVA_OK;
+}
 
+int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
+                int C, int dtype, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
+    if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    int st = supported(d, dtype);
+    if (st != EVA_OK) return st;
+    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (!Q || !K || !V || !O) return EVA_ERR_INVALID;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return EVA_ERR_INVALID;
+    const int n_chunks = L / C;
+    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
     if (cache) {
-        eva::CacheView v = view_of(cache);
-        e = dispatch(d, dtype, [&](auto dd, auto t) {
-            return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, s);
-        });
-        if (e != hipSuccess) return EVA_ERR_HIP;
-        cache->n_tok = L;
+        st = check_cache(cache);
+        if (st != EVA_OK) return st;
+        if (cache->B != B || cache->H != H || cache->H_kv != H_kv || cache->d != d || cache->W != W ||
+            cache->C != C || cache->dtype != dtype)
+            return EVA_ERR_INVALID;
+        if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
     }
+    st = eva_build_summaries(K, V, Ksum, Vsum, B, H_kv, L, d, C, dtype, stream);
+    if (st != EVA_OK) return st;
+    st = eva_prefill_attention(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, stream);
+    if (st != EVA_OK) return st;
+    if (cache) return eva_cache_fill(cache, K, V, Ksum, Vsum, L, stream);
     return EVA_OK;
 }
 

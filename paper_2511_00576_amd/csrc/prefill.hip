@@ -225,19 +225,31 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
             }
         }
 
-        // ---- mask (boundary blocks only) ----
+        // ---- mask (boundary blocks only), branch-free per element ----
+        // element (kb, i) of lane (g, c16) is key base + kb*16 + 4g + i
         if (!full) {
+            if (is_sum) {
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const int n = col_n[cb];
+                for (int cb = 0; cb < 2; ++cb) {
+                    const int lim = col_s[cb] - base - g * 4;  // valid iff kb*16 + i < lim
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
+                    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int key = base + kb * 16 + g * 4 + i;
-                        const bool ok = is_sum ? (key < col_s[cb]) : (key <= n && key > n - W);
-                        if (!ok) s[kb][cb][i] = -INFINITY;
-                    }
+                        for (int i = 0; i < 4; ++i)
+                            s[kb][cb][i] = (kb * 16 + i < lim) ? s[kb][cb][i] : -INFINITY;
+                }
+            } else {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const int rel = col_n[cb] - base - g * 4;  // n - key = rel - (kb*16 + i)
+#pragma unroll
+                    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const unsigned dist = (unsigned)(rel - (kb * 16 + i));  // valid iff 0 <= n-key < W
+                            s[kb][cb][i] = dist < (unsigned)W ? s[kb][cb][i] : -INFINITY;
+                        }
+                }
             }
         }
 

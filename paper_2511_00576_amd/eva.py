@@ -35,12 +35,19 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def build_summaries(K: torch.Tensor, V: torch.Tensor, C: int):
-    """Chunk summaries. K, V: [B, Hkv, L, d] -> (Ksum, Vsum): [B, Hkv, L // C, d]."""
+def build_summaries(K: torch.Tensor, V: torch.Tensor, C: int, out=None):
+    """Chunk summaries. K, V: [B, Hkv, L, d] -> (Ksum, Vsum): [B, Hkv, L // C, d].
+    `out` = (Ksum, Vsum) preallocated, else allocated here."""
     _require_device(K, V)
     B, Hkv, L, d = K.shape
-    Ks = torch.empty(B, Hkv, L // C, d, dtype=K.dtype, device=K.device)
-    Vs = torch.empty_like(Ks)
+    if out is None:
+        Ks = torch.empty(B, Hkv, L // C, d, dtype=K.dtype, device=K.device)
+        Vs = torch.empty_like(Ks)
+    else:
+        Ks, Vs = out
+        _require_device(Ks, Vs)
+        if tuple(Ks.shape) != (B, Hkv, L // C, d) or Vs.shape != Ks.shape or Ks.dtype != K.dtype:
+            raise ValueError("summary buffers must be [B, Hkv, L // C, d] in the input dtype")
     lib = _lib.load()
     _lib.check("eva_build_summaries",
                lib.eva_build_summaries(_ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), B, Hkv, L, d, C, _dtype_code(K),
@@ -117,6 +124,36 @@ def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool
     return O
 
 
+def prefill_attention(Q, K, V, Ks, Vs, W: int, C: int, out=None):
+    """The fused window + summary attention alone, given summaries from
+    build_summaries(K, V, C). Q [B, H, L, d] -> O [B, H, L, d]."""
+    _require_device(Q, K, V)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    if K.shape != (B, Hkv, L, d) or V.shape != K.shape or Q.dtype != K.dtype or V.dtype != K.dtype:
+        raise ValueError("Q [B,H,L,d], K and V [B,Hkv,L,d] of one dtype expected")
+    if Ks is not None and (tuple(Ks.shape) != (B, Hkv, L // C, d) or Vs.shape != Ks.shape):
+        raise ValueError("summaries must be [B, Hkv, L // C, d]")
+    O = torch.empty_like(Q) if out is None else out
+    _require_device(O)
+    _lib.check("eva_prefill_attention",
+               _lib.load().eva_prefill_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), _ptr(O), B, H, Hkv,
+                                                 L, d, W, C, _dtype_code(Q), _stream()))
+    return O
+
+
+def cache_fill(cache: Cache, K, V, Ks, Vs):
+    """Load the cache from a prefilled sequence (K, V [B, Hkv, L, d] and its
+    summaries); n_tok becomes L."""
+    _require_device(K, V)
+    s = cache.struct
+    B, Hkv, L, d = K.shape
+    if (B, Hkv, d) != (s.B, s.H_kv, s.d) or K.dtype != cache.dtype or V.shape != K.shape:
+        raise ValueError("K, V must be [B, Hkv, L, d] matching the cache")
+    _lib.check("eva_cache_fill",
+               _lib.load().eva_cache_fill(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), L, _stream()))
+
+
 def cache_append(cache: Cache, k_new, v_new):
     """Append one token per sequence: k_new, v_new [B, Hkv, d]."""
     _require_device(k_new, v_new)
@@ -127,13 +164,13 @@ def cache_append(cache: Cache, k_new, v_new):
                _lib.load().eva_cache_append(ctypes.byref(s), _ptr(k_new), _ptr(v_new), _stream()))
 
 
-def decode_step(cache: Cache, q, use_workspace: bool = True):
+def decode_step(cache: Cache, q, use_workspace: bool = True, out=None):
     """Attention output of the last appended position: q [B, H, d] -> o [B, H, d]."""
     _require_device(q)
     s = cache.struct
     if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
         raise ValueError("q must be [B, H, d] in the cache dtype")
-    o = torch.empty_like(q)
+    o = torch.empty_like(q) if out is None else out
     ws = cache.workspace() if use_workspace else None
     nbytes = ws.numel() * 4 if ws is not None else 0
     _lib.check("eva_decode_step",
