@@ -162,9 +162,9 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
     p.C = C;
     p.n_chunks = n_chunks;
     p.G = H / H_kv;
-    p.Gt = gcd(p.G, 4);
+    p.Gt = gcd(p.G, eva::kPrefillWaves);
     p.n_hg = p.G / p.Gt;
-    p.pos_per_wg = 32 * 4 / p.Gt;
+    p.pos_per_wg = 32 * eva::kPrefillWaves / p.Gt;
     p.n_pos_tiles = (L + p.pos_per_wg - 1) / p.pos_per_wg;
     const long long tiles = (long long)B * H_kv * p.n_hg * p.n_pos_tiles;
     if (tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;

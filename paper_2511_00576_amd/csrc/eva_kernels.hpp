@@ -7,6 +7,9 @@
 
 namespace eva {
 
+// Waves per prefill workgroup; each wave owns 32 query columns.
+constexpr int kPrefillWaves = 8;
+
 struct PrefillParams {
     const void* Q;
     const void* K;
@@ -16,9 +19,9 @@ struct PrefillParams {
     void* O;
     int B, H, Hkv, L, W, C, n_chunks;
     int G;            // H / Hkv
-    int Gt;           // heads packed per workgroup (1, 2 or 4)
+    int Gt;           // heads packed per workgroup: gcd(G, kPrefillWaves)
     int n_hg;         // G / Gt
-    int pos_per_wg;   // 32 * 4 / Gt
+    int pos_per_wg;   // 32 * kPrefillWaves / Gt
     int n_pos_tiles;  // ceil(L / pos_per_wg)
     int n_tiles;      // B * Hkv * n_hg * n_pos_tiles
     float scale_log2; // log2(e) / sqrt(d)

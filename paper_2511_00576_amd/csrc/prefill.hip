@@ -5,19 +5,23 @@
 // per chunk summary.  The causal form needs a mask of its own (window band for
 // exact keys, "chunk lies fully before the window" for summaries); it is never
 // materialized here: each 64-key block is classified per wave, and only blocks
-// that straddle a boundary evaluate per-element compares.
+// that straddle a boundary evaluate a per-element range test.
 //
-// Work decomposition: one workgroup = 4 waves = one tile of query columns that
-// share one key/value head.  A wave owns 32 columns (two 16-column MFMA
+// Work decomposition: one workgroup = NW waves = one tile of query columns
+// that share one key/value head.  A wave owns 32 columns (two 16-column MFMA
 // blocks); with G = H / H_kv query heads per kv head the workgroup packs
-// Gt = gcd(G, 4) heads x (128 / Gt) positions, so the K/V blocks staged in LDS
-// serve every wave.  Per block: S^T = K Q^T on the matrix cores (keys are MFMA
-// rows, so every lane owns one query column and its softmax statistics stay in
-// registers), online softmax in log2 units, O^T += V^T P^T with P taken
-// straight from the S^T accumulators.
+// Gt = gcd(G, NW) heads x (32 NW / Gt) positions, so every K/V block staged in
+// LDS serves all NW waves.  Per block: S^T = K Q^T on the matrix cores (keys
+// are MFMA rows, so each lane owns one query column and its softmax
+// statistics stay in registers), online softmax in log2 units, O^T += V^T P^T
+// with P taken straight from the S^T accumulators.
 //
-// Pipeline: the next block's K/V are loaded from HBM into registers while the
-// current block is computed from LDS (one LDS stage, register double buffer).
+// Staging: K/V blocks go HBM -> LDS with global_load_lds_dwordx4 (no register
+// round trip) into an NS-deep ring of LDS stages; block j+NS-1 is requested
+// while block j is computed, with one barrier per block and an explicit
+// vmcnt wait for exactly the block about to be read.  Rows are stored
+// unpadded with an XOR swizzle of their 16-B chunks, chosen so that the
+// 16-B K-fragment reads and the transposing V reads hit distinct banks.
 #include "eva_device.hpp"
 #include "eva_kernels.hpp"
 
@@ -29,39 +33,67 @@ constexpr int kBN = 64;      // keys per block
 constexpr int kQW = 32;      // query columns per wave
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
 
-template <int D, typename T>
-struct PLayout {
+template <int D, typename T, int NW>
+struct PCfg {
     static constexpr bool BF = sizeof(T) == 2;
-    // Row pitches (elements).  bf16: K rows are read 16 B per lane by 8-lane
-    // phases -> 272 B pitch (4-bank shift per row); V rows are read by the
-    // transposing 8 B read, 4 rows x 32 B per 16-lane group -> 8-bank shift.
-    static constexpr int KP = BF ? D + 8 : D + 4;
-    static constexpr int VP = BF ? D + 16 : D + 4;
-    static constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-B piece
-    static constexpr int PPR = D / VEC;              // pieces per row
-    static constexpr int PPT = kBN * PPR / 256;      // pieces per thread
-    static constexpr int LDS_BYTES = kBN * (KP + VP) * (int)sizeof(T);
+    static constexpr int ROWB = D * (int)sizeof(T);      // bytes per row
+    static constexpr int CPR = ROWB / 16;                // 16-B chunks per row
+    static constexpr int VEC = 16 / (int)sizeof(T);      // elements per chunk
+    static constexpr int BLK = kBN * ROWB;               // bytes per 64-row block
+    static constexpr int NI = BLK / 1024 / NW;           // DMA instructions / wave / array
+    static_assert(NI >= 1, "block too small for the workgroup");
+    static constexpr int NI_TOTAL = 2 * NI;              // K and V
 };
+
+// Chunk swizzles (position = logical chunk ^ swz(row)).  K rows are read as
+// 16-B fragments by 16 lanes holding 16 consecutive rows; V rows (bf16) by
+// the transposing read, 4 lanes x 8 B on each of 4-8 consecutive rows; V rows
+// (fp32) by scalar reads, 16 lanes on each of 4 rows spaced 4 apart.
+template <int CPR>
+__device__ __forceinline__ int swz_k(int r) {
+    return CPR >= 16 ? (r & 15) : ((r >> 1) & 7);
+}
+template <int CPR, bool BF>
+__device__ __forceinline__ int swz_v(int r) {
+    if constexpr (BF) return CPR >= 16 ? 2 * (r & 7) : 2 * ((r >> 1) & 3);
+    return 4 * ((r >> 2) & 3);
+}
 
 template <typename T> struct QFrag;
 template <> struct QFrag<bf16> { typedef bf16x8 type; };
 template <> struct QFrag<float> { typedef floatx4 type; };
 
-template <int D, typename T>
-__global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
-    typedef PLayout<D, T> Lay;
-    constexpr bool BF = Lay::BF;
+// s_waitcnt immediate: vmcnt(n), lgkmcnt(0), expcnt untouched.
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(N < 64, "vmcnt field is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// One global_load_lds_dwordx4: every lane moves 16 B from base + voff to
+// LDS address M0 + 16 * lane.  Issued as inline asm on purpose: the compiler
+// cannot see the LDS write, so it does not drain the whole prefetch queue
+// (vmcnt(0)) before every later LDS read; the kernel waits for exactly the
+// block it is about to read with an explicit vmcnt.  (Waits the compiler
+// derives for its own loads only become more conservative: vmcnt retires in
+// order.)
+__device__ __forceinline__ void lds_dma16(const void* base, unsigned voff, const void* lds_dst) {
+    const unsigned m0 =
+        __builtin_amdgcn_readfirstlane((unsigned)(size_t)(__attribute__((address_space(3))) const void*)lds_dst);
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(m0) : "memory");
+}
+
+template <int D, typename T, int NW, int NS>
+__global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
+    typedef PCfg<D, T, NW> Cfg;
+    constexpr bool BF = Cfg::BF;
+    constexpr int ROWB = Cfg::ROWB, CPR = Cfg::CPR, VEC = Cfg::VEC, BLK = Cfg::BLK, NI = Cfg::NI;
     constexpr int NQF = BF ? D / 32 : D / 16;  // Q fragments per 16-column block
     constexpr int NDB = D / 16;                // 16-feature output blocks
 
-    __shared__ __attribute__((aligned(16))) T lds_k[kBN * Lay::KP];
-    __shared__ __attribute__((aligned(16))) T lds_v[kBN * Lay::VP];
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[NS][2][BLK];
 
     const T* __restrict__ Q = static_cast<const T*>(a.Q);
-    const T* __restrict__ K = static_cast<const T*>(a.K);
-    const T* __restrict__ V = static_cast<const T*>(a.V);
-    const T* __restrict__ Ks = static_cast<const T*>(a.Ks);
-    const T* __restrict__ Vs = static_cast<const T*>(a.Vs);
     T* __restrict__ O = static_cast<T*>(a.O);
 
     // ---- tile decode: XCD-aware remap, heavy (late) position tiles first ----
@@ -100,10 +132,10 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
     const int ws_lo = visible_summaries(p0, W, C);
 
     const size_t bg = (size_t)b * a.Hkv + kvh;
-    const T* Kbg = K + bg * (size_t)L * D;
-    const T* Vbg = V + bg * (size_t)L * D;
-    const T* Ksbg = Ks + bg * (size_t)a.n_chunks * D;
-    const T* Vsbg = Vs + bg * (size_t)a.n_chunks * D;
+    const T* Kbg = static_cast<const T*>(a.K) + bg * (size_t)L * D;
+    const T* Vbg = static_cast<const T*>(a.V) + bg * (size_t)L * D;
+    const T* Ksbg = static_cast<const T*>(a.Ks) + bg * (size_t)a.n_chunks * D;
+    const T* Vsbg = static_cast<const T*>(a.Vs) + bg * (size_t)a.n_chunks * D;
     const size_t bh = (size_t)b * a.H + h;
 
     // per-column facts (column = query position p0 + cb*16 + c16)
@@ -133,57 +165,93 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
         }
     }
 
+    // ---- DMA plan: instruction i of this wave fills LDS bytes
+    //      [(i*NW + wave) * 1024, +1024) of each array; lane -> (row, chunk) ----
+    int dma_row[NI], dma_off[NI], dma_kcol[NI], dma_vcol[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int byte = (i * NW + wave) * 1024 + lane * 16;
+        const int r = byte / ROWB;
+        const int pos = (byte % ROWB) / 16;
+        dma_row[i] = r;
+        dma_off[i] = (i * NW + wave) * 1024;
+        dma_kcol[i] = (pos ^ swz_k<CPR>(r)) * VEC;  // source chunk landing at LDS chunk pos
+        dma_vcol[i] = (pos ^ swz_v<CPR, BF>(r)) * VEC;
+    }
+    auto issue = [&](int j) {
+        const int st = j % NS;
+        const bool is_sum = j < nsb;
+        const int base = is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
+        const int limit = is_sum ? a.n_chunks : L;
+        const T* kb = (is_sum ? Ksbg : Kbg) + (size_t)base * D;
+        const T* vb = (is_sum ? Vsbg : Vbg) + (size_t)base * D;
+        // rows past the end repeat the last valid row: finite, and masked out
+        // (keys beyond every query, summaries beyond every s(n))
+        const int last = limit - 1 - base;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int row = min(dma_row[i], last);
+            lds_dma16(kb, (unsigned)((row * D + dma_kcol[i]) * (int)sizeof(T)), &lds[st][0][dma_off[i]]);
+            lds_dma16(vb, (unsigned)((row * D + dma_vcol[i]) * (int)sizeof(T)), &lds[st][1][dma_off[i]]);
+        }
+    };
+
+    // ---- per-lane LDS read offsets (bytes within a stage array) ----
+    // K fragment (kb, dc): row kb*16 + c16, logical chunk (bf16) dc*4 + g,
+    // (fp32) g*(D/16) + f; the swizzle of row kb*16 + c16 depends on c16 only,
+    // so kb only adds kb*16*ROWB (an immediate offset).
+    constexpr int NKO = BF ? D / 32 : D / 16;
+    int k_off[NKO];
+#pragma unroll
+    for (int f = 0; f < NKO; ++f) {
+        const int chunk = BF ? f * 4 + g : g * (D / 16) + f;
+        k_off[f] = c16 * ROWB + ((chunk ^ swz_k<CPR>(c16)) << 4);
+    }
+    // V, bf16 transposing read: lane (g, 4j'+t) names row 4g+j' (+16 half,
+    // +32 kc: immediate offsets) and features 4t..4t+3 of feature block db.
+    int v_off[NDB];
+    {
+        const int v_row = g * 4 + (c16 >> 2);
+        const int v_t = c16 & 3;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+            v_off[db] = v_row * ROWB + (((db * 2 + (v_t >> 1)) ^ swz_v<CPR, BF>(v_row)) << 4) + (v_t & 1) * 8;
+    }
+
     floatx4 acc[NDB][2];
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb) acc[db][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     float m_run[2] = {-INFINITY, -INFINITY};
+    // softmax denominators: bf16 path sums the rounded weights on the matrix
+    // cores (all-ones A operand, every output row = the column sum); fp32 path
+    // keeps per-lane partial sums
+    floatx4 l_acc[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
     float l_run[2] = {0.f, 0.f};
+    const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
 
-    // ---- staging: 16-B pieces, thread tid takes pieces tid + 256 i ----
-    u32x4 kst[Lay::PPT], vst[Lay::PPT];
-    auto load_block = [&](int j) {
-        const bool is_sum = j < nsb;
-        const int base = is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
-        const int limit = is_sum ? a.n_chunks : L;
-        const T* kb = is_sum ? Ksbg : Kbg;
-        const T* vb = is_sum ? Vsbg : Vbg;
-#pragma unroll
-        for (int i = 0; i < Lay::PPT; ++i) {
-            const int p = tid + 256 * i;
-            const int row = base + p / Lay::PPR;
-            const int col = (p % Lay::PPR) * Lay::VEC;
-            if (row < limit) {
-                kst[i] = *reinterpret_cast<const u32x4*>(kb + (size_t)row * D + col);
-                vst[i] = *reinterpret_cast<const u32x4*>(vb + (size_t)row * D + col);
-            } else {
-                kst[i] = u32x4{0u, 0u, 0u, 0u};
-                vst[i] = u32x4{0u, 0u, 0u, 0u};
-            }
-        }
-    };
-    auto store_block = [&]() {
-#pragma unroll
-        for (int i = 0; i < Lay::PPT; ++i) {
-            const int p = tid + 256 * i;
-            const int r = p / Lay::PPR;
-            const int col = (p % Lay::PPR) * Lay::VEC;
-            *reinterpret_cast<u32x4*>(&lds_k[r * Lay::KP + col]) = kst[i];
-            *reinterpret_cast<u32x4*>(&lds_v[r * Lay::VP + col]) = vst[i];
-        }
-    };
+    // ---- staggered two-phase schedule ----
+    // phase 1(j): S = QK(j) and the deferred O += PV(j-1)  (matrix cores)
+    // phase 2(j): mask + online softmax of S -> P(j)         (vector ALU)
+    // Waves [0, NW/2) and [NW/2, NW) sit pairwise on the same SIMD and run
+    // one phase apart, so at every tick one wave of each pair feeds the
+    // matrix cores while the other runs its softmax.  Tick t ends with a
+    // workgroup barrier; block k+1 is requested at tick 2k and must have
+    // landed at tick 2k+2; block k's stage is read until tick 2k+3, so three
+    // stages suffice.
+    // (fp32 does its PV inside phase 2 and keeps all waves in step, which two
+    // stages cover: block k-1's last read is at tick 2k-1, its stage is
+    // refilled at tick 2k)
+    static_assert(NS >= 3 || !BF, "the deferred PV keeps three blocks in flight");
+    const int group = BF ? wave / (NW / 2) : 0;
+    floatx4 s[4][2];
+    bf16x8 pf[2][2];
+    bool s_ready = false, pv_pending = false;
 
-    load_block(0);
-    for (int j = 0; j < nb; ++j) {
-        __syncthreads();
-        store_block();
-        __syncthreads();
-        if (j + 1 < nb) load_block(j + 1);
-
-        const bool is_sum = j < nsb;
-        const int base = is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
-        bool needed, full;
+    auto block_of = [&](int j, int& base, bool& is_sum, bool& needed, bool& full) {
+        is_sum = j < nsb;
+        base = is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
         if (is_sum) {
             needed = base < ws_hi;
             full = base + kBN - 1 < ws_lo;
@@ -191,156 +259,232 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
             needed = w_active && base <= wp_last && base + kBN - 1 >= p0 - W + 1;
             full = base >= wp_last - W + 1 && base + kBN - 1 <= p0;
         }
-        if (!needed) continue;
+    };
 
-        // ---- S^T = K Q^T : s[kb][cb] holds keys base + kb*16 + 4g + i ----
-        floatx4 s[4][2];
+    // O^T += V^T P^T for block j (bf16: P packed in pf)
+    auto pv_bf16 = [&](int j) {
+        const unsigned char* vs = lds[j % NS][1];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) s[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (BF) {
-            const T* kl = lds_k + c16 * Lay::KP + g * 8;
+            for (int cb = 0; cb < 2; ++cb) l_acc[cb] = mfma_bf16(ones, pf[kc][cb], l_acc[cb]);
+        // V fragments one feature block ahead of the MFMAs that use them
+        auto load_v = [&](int db, bf16x8 (&vf)[2]) {
+            const unsigned char* vp = vs + v_off[db];
 #pragma unroll
-            for (int dc = 0; dc < D / 32; ++dc) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kl + kb * 16 * Lay::KP + dc * 32);
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) s[kb][cb] = mfma_bf16(ka, qf[cb][dc], s[kb][cb]);
-                }
+            for (int kc = 0; kc < 2; ++kc) {
+                const shortx4 lo = lds_read_tr16(reinterpret_cast<const bf16*>(vp + (kc * 32) * ROWB));
+                const shortx4 hi = lds_read_tr16(reinterpret_cast<const bf16*>(vp + (kc * 32 + 16) * ROWB));
+                vf[kc] = __builtin_bit_cast(
+                    bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1],
+                                                                          hi[2], hi[3]});
             }
-        } else {
-            const T* kl = lds_k + c16 * Lay::KP + g * (D / 4);
+        };
+        bf16x8 vf[2][2];
+        load_v(0, vf[0]);
 #pragma unroll
-            for (int f = 0; f < NQF; ++f) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const floatx4 ka = *reinterpret_cast<const floatx4*>(kl + kb * 16 * Lay::KP + f * 4);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-#pragma unroll
-                        for (int cb = 0; cb < 2; ++cb) s[kb][cb] = mfma_f32(ka[e], qf[cb][f][e], s[kb][cb]);
-                }
-            }
-        }
-
-        // ---- mask (boundary blocks only), branch-free per element ----
-        // element (kb, i) of lane (g, c16) is key base + kb*16 + 4g + i
-        if (!full) {
-            if (is_sum) {
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    const int lim = col_s[cb] - base - g * 4;  // valid iff kb*16 + i < lim
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            s[kb][cb][i] = (kb * 16 + i < lim) ? s[kb][cb][i] : -INFINITY;
-                }
-            } else {
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    const int rel = col_n[cb] - base - g * 4;  // n - key = rel - (kb*16 + i)
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const unsigned dist = (unsigned)(rel - (kb * 16 + i));  // valid iff 0 <= n-key < W
-                            s[kb][cb][i] = dist < (unsigned)W ? s[kb][cb][i] : -INFINITY;
-                        }
-                }
-            }
-        }
-
-        // ---- online softmax (log2 units), lazy rescaling ----
-        const float bias = is_sum ? a.log2C : 0.f;
-        float bmax[2];
-        bool need[2];
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][cb][i]);
-            mx = xgroup_max(mx);
-            bmax[cb] = mx * a.scale_log2 + bias;  // -inf stays -inf
-            need[cb] = bmax[cb] > m_run[cb] + kTau;
-        }
-        if (__ballot(need[0] || need[1]) != 0) {
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const float m_new = need[cb] ? bmax[cb] : m_run[cb];
-                const float alpha = need[cb] ? fast_exp2(m_run[cb] - m_new) : 1.f;
-                l_run[cb] *= alpha;
-#pragma unroll
-                for (int db = 0; db < NDB; ++db) acc[db][cb] *= alpha;
-                m_run[cb] = m_new;
-            }
-        }
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            const float off = bias - (m_run[cb] == -INFINITY ? 0.f : m_run[cb]);
-            float ls = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float p = fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, off));
-                    s[kb][cb][i] = p;
-                    ls += p;
-                }
-            l_run[cb] += ls;
-        }
-
-        // ---- O^T += V^T P^T ----
-        if constexpr (BF) {
-            bf16x8 pf[2][2];
+        for (int db = 0; db < NDB; ++db) {
+            if (db + 1 < NDB) load_v(db + 1, vf[(db + 1) & 1]);
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
+                for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_bf16(vf[db & 1][kc], pf[kc][cb], acc[db][cb]);
+        }
+    };
+
+    if (nb > 0) issue(0);
+    const int n_ticks = 2 * nb + 2;
+    for (int t = 0; t < n_ticks; ++t) {
+        // even ticks: block t/2 (requested at tick t-2, the only one in
+        // flight) must have landed; always: this wave's LDS reads are done
+        asm volatile("" ::: "memory");
+        if ((t & 1) == 0)
+            wait_vm_lgkm0<0>();
+        else
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        if ((t & 1) == 0 && t / 2 + 1 < nb) issue(t / 2 + 1);
+
+        const int ph = t - group;
+        if (ph < 0) continue;
+        const int j = ph >> 1;
+
+        if ((ph & 1) == 0) {
+            // ---------------- phase 1(j) ----------------
+            __builtin_amdgcn_s_setprio(1);
+            if constexpr (BF) {
+                if (pv_pending) pv_bf16(j - 1);
+                pv_pending = false;
+            }
+            s_ready = false;
+            if (j < nb) {
+                int base;
+                bool is_sum, needed, full;
+                block_of(j, base, is_sum, needed, full);
+                if (needed) {
+                    s_ready = true;
+                    const unsigned char* ks = lds[j % NS][0];
+                    // S^T = K Q^T : s[kb][cb] holds keys base + kb*16 + 4g + i
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        pf[kc][cb][i] = to_bf16(s[2 * kc][cb][i]);
-                        pf[kc][cb][4 + i] = to_bf16(s[2 * kc + 1][cb][i]);
+                    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                        for (int cb = 0; cb < 2; ++cb) s[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+                    if constexpr (BF) {
+                        // K fragments one feature step ahead of their MFMAs
+                        bf16x8 kf[2][4];
+#pragma unroll
+                        for (int kb = 0; kb < 4; ++kb)
+                            kf[0][kb] = *reinterpret_cast<const bf16x8*>(ks + k_off[0] + kb * 16 * ROWB);
+#pragma unroll
+                        for (int dc = 0; dc < D / 32; ++dc) {
+                            if (dc + 1 < D / 32) {
+#pragma unroll
+                                for (int kb = 0; kb < 4; ++kb)
+                                    kf[(dc + 1) & 1][kb] =
+                                        *reinterpret_cast<const bf16x8*>(ks + k_off[dc + 1] + kb * 16 * ROWB);
+                            }
+#pragma unroll
+                            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                                for (int cb = 0; cb < 2; ++cb)
+                                    s[kb][cb] = mfma_bf16(kf[dc & 1][kb], qf[cb][dc], s[kb][cb]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int f = 0; f < NQF; ++f) {
+                            const unsigned char* kp = ks + k_off[f];
+#pragma unroll
+                            for (int kb = 0; kb < 4; ++kb) {
+                                const floatx4 ka = *reinterpret_cast<const floatx4*>(kp + kb * 16 * ROWB);
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                                    for (int cb = 0; cb < 2; ++cb)
+                                        s[kb][cb] = mfma_f32(ka[e], qf[cb][f][e], s[kb][cb]);
+                            }
+                        }
                     }
-            // transposing read: lane (g, 4j'+t) names V row 4g+j', features 4t..4t+3
-            const T* vl = lds_v + (g * 4 + (c16 >> 2)) * Lay::VP + (c16 & 3) * 4;
-#pragma unroll
-            for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc) {
-                    const shortx4 lo = lds_read_tr16(vl + (kc * 32) * Lay::VP + db * 16);
-                    const shortx4 hi = lds_read_tr16(vl + (kc * 32 + 16) * Lay::VP + db * 16);
-                    const bf16x8 va = __builtin_bit_cast(
-                        bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3],
-                                                                              hi[0], hi[1], hi[2], hi[3]});
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_bf16(va, pf[kc][cb], acc[db][cb]);
                 }
             }
-        } else {
+            __builtin_amdgcn_s_setprio(0);
+        } else if (s_ready) {
+            // ---------------- phase 2(j) ----------------
+            int base;
+            bool is_sum, needed, full;
+            block_of(j, base, is_sum, needed, full);
+
+            // mask (boundary blocks only), branch-free per element;
+            // element (kb, i) of lane (g, c16) is key base + kb*16 + 4g + i
+            if (!full) {
+                if (is_sum) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+                    for (int cb = 0; cb < 2; ++cb) {
+                        const int lim = col_s[cb] - base - g * 4;  // valid iff kb*16 + i < lim
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const T* vr = lds_v + (kb * 16 + g * 4 + i) * Lay::VP + c16;
+                        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                    for (int db = 0; db < NDB; ++db) {
-                        const float va = vr[db * 16];
+                            for (int i = 0; i < 4; ++i)
+                                s[kb][cb][i] = (kb * 16 + i < lim) ? s[kb][cb][i] : -INFINITY;
+                    }
+                } else {
 #pragma unroll
-                        for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_f32(va, s[kb][cb][i], acc[db][cb]);
+                    for (int cb = 0; cb < 2; ++cb) {
+                        const int rel = col_n[cb] - base - g * 4;  // n - key = rel - (kb*16 + i)
+#pragma unroll
+                        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const unsigned dist = (unsigned)(rel - (kb * 16 + i));  // valid iff 0 <= n-key < W
+                                s[kb][cb][i] = dist < (unsigned)W ? s[kb][cb][i] : -INFINITY;
+                            }
                     }
                 }
+            }
+
+            // online softmax (log2 units), lazy rescaling
+            const float bias = is_sum ? a.log2C : 0.f;
+            float bmax[2];
+            bool need[2];
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][cb][i]);
+                mx = xgroup_max(mx);
+                bmax[cb] = mx * a.scale_log2 + bias;  // -inf stays -inf
+                need[cb] = bmax[cb] > m_run[cb] + kTau;
+            }
+            if (__ballot(need[0] || need[1]) != 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const float m_new = need[cb] ? bmax[cb] : m_run[cb];
+                    const float alpha = need[cb] ? fast_exp2(m_run[cb] - m_new) : 1.f;
+                    l_run[cb] *= alpha;
+                    l_acc[cb] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < NDB; ++db) acc[db][cb] *= alpha;
+                    m_run[cb] = m_new;
+                }
+            }
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                const float off = bias - (m_run[cb] == -INFINITY ? 0.f : m_run[cb]);
+                float ls = 0.f;
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float p = fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, off));
+                        s[kb][cb][i] = p;
+                        if constexpr (!BF) ls += p;
+                    }
+                if constexpr (!BF) l_run[cb] += ls;
+            }
+
+            if constexpr (BF) {
+                // P(j) rounded to bf16 for the deferred PV of phase 1(j+1)
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            pf[kc][cb][i] = to_bf16(s[2 * kc][cb][i]);
+                            pf[kc][cb][4 + i] = to_bf16(s[2 * kc + 1][cb][i]);
+                        }
+                pv_pending = true;
+            } else {
+                // fp32: O^T += V^T P^T right away; element (key kb*16 + 4g + i,
+                // feature db*16 + c16), row swizzle depends on g only
+                const unsigned char* vs = lds[j % NS][1];
+                const int vsw = swz_v<CPR, BF>(g * 4);
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int row = kb * 16 + g * 4 + i;
+#pragma unroll
+                        for (int db = 0; db < NDB; ++db) {
+                            const int off = row * ROWB + (((db * 4 + (c16 >> 2)) ^ vsw) << 4) + (c16 & 3) * 4;
+                            const float va = *reinterpret_cast<const float*>(vs + off);
+#pragma unroll
+                            for (int cb = 0; cb < 2; ++cb)
+                                acc[db][cb] = mfma_f32(va, s[kb][cb][i], acc[db][cb]);
+                        }
+                    }
+            }
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // ---- epilogue: O = acc / l ----
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
-        const float lt = xgroup_sum(l_run[cb]);
+        const float lt = BF ? l_acc[cb][0] : xgroup_sum(l_run[cb]);
         const int n = col_n[cb];
         if (n >= L) continue;
         const float inv = 1.f / lt;
@@ -362,7 +506,13 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams a) {
 
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
-    hipLaunchKernelGGL((prefill_kernel<D, T>), dim3(p.n_tiles), dim3(256), 0, stream, p);
+    if constexpr (sizeof(T) == 2) {
+        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 3>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
+                           stream, p);
+    } else {
+        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 2>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
+                           stream, p);
+    }
     return hipGetLastError();
 }
 
