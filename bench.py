@@ -95,16 +95,16 @@ def cpu_baseline(w):
     import oracle
     from paper_2511_00576_amd import inputs
 
-    n_heads = int(os.environ.get("EVA_ORACLE_HEADS", "16"))
+    n_batch = 2  # two of the eight sequences, every head, every row
     q, k, v = inputs.workload_qkv(w)
-    qs, ks, vs = q[:1, :n_heads], k[:1, :n_heads], v[:1, :n_heads]
+    qs, ks, vs = q[:n_batch], k[:n_batch], v[:n_batch]
     t0 = time.perf_counter()
     oracle.prefill(qs, ks, vs, w.W, w.C)
     dt = time.perf_counter() - t0
-    flops = n_heads * 4 * w.d * attended(w.L, w.W, w.C)
+    flops = n_batch * w.H * 4 * w.d * attended(w.L, w.W, w.C)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"batch 0, heads 0-{n_heads - 1} of {w.name} (all {w.L} rows, summaries included), "
-                      f"{dt:.2f} s wall"}
+            "sample": f"batch elements 0-{n_batch - 1} of {w.name} (all {w.H} heads, all {w.L} rows, "
+                      f"summaries included), {dt:.2f} s wall"}
 
 
 def main():
@@ -115,6 +115,9 @@ def main():
     ap.add_argument("--decode-iters", type=int, default=64, help="graph-captured decode tokens (x4 caches)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--decode-eager", action="store_true",
+                    help="launch the decode iterations one by one instead of replaying a captured graph "
+                         "(for per-dispatch counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device-to-device copy (counter scaling for profiles)")
     args = ap.parse_args()
@@ -262,6 +265,11 @@ def bench_decode(args, torch, eva, inputs, dev):
     token(caches[0])
     ref = od.clone()
     iters = args.decode_iters * N_CACHES
+    if args.decode_eager:
+        for i in range(iters):
+            token(caches[i % N_CACHES])
+        torch.cuda.synchronize()
+        return {"workload": dw.name, "eager_iterations": iters, "graph_matches_eager": None}
     stream = torch.cuda.Stream()
     graphs = {}
     for name, fn in (("token", token), ("decode", decode_only)):
