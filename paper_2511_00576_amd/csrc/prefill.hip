@@ -22,6 +22,8 @@
 // vmcnt wait for exactly the block about to be read.  Rows are stored
 // unpadded with an XOR swizzle of their 16-B chunks, chosen so that the
 // 16-B K-fragment reads and the transposing V reads hit distinct banks.
+#include <type_traits>
+
 #include "eva_device.hpp"
 #include "eva_kernels.hpp"
 
@@ -237,13 +239,13 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
     // Waves [0, NW/2) and [NW/2, NW) sit pairwise on the same SIMD and run
     // one phase apart, so at every tick one wave of each pair feeds the
     // matrix cores while the other runs its softmax.  Tick t ends with a
-    // workgroup barrier; block k+1 is requested at tick 2k and must have
-    // landed at tick 2k+2; block k's stage is read until tick 2k+3, so three
-    // stages suffice.
-    // (fp32 does its PV inside phase 2 and keeps all waves in step, which two
-    // stages cover: block k-1's last read is at tick 2k-1, its stage is
-    // refilled at tick 2k)
-    static_assert(NS >= 3 || !BF, "the deferred PV keeps three blocks in flight");
+    // workgroup barrier.  Block k is read from tick 2k (K) until tick 2k+3
+    // (V, deferred PV of the second group), so the request for block k+AHEAD
+    // may go out at tick 2k into the stage of block k+AHEAD-NS if that block's
+    // last read, tick 2(k+AHEAD-NS)+3, is before 2k: AHEAD <= NS-2.  (fp32 does
+    // its PV inside phase 2 and keeps all waves in step: last read at 2k+1,
+    // AHEAD <= NS-1.)
+    static_assert(NS >= 3 || !BF, "the deferred PV needs at least three stages");
     const int group = BF ? wave / (NW / 2) : 0;
     floatx4 s[4][2];
     bf16x8 pf[2][2];
@@ -261,51 +263,97 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
         }
     };
 
-    // O^T += V^T P^T for block j (bf16: P packed in pf)
-    auto pv_bf16 = [&](int j) {
-        const unsigned char* vs = lds[j % NS][1];
+    // bf16 phase 1 as one straight-line sequence: the deferred PV of the
+    // previous block (V from LDS stage vs) interleaved with QK of this block
+    // (K from stage ks); each fragment read is issued at least one step (12
+    // MFMAs) before its use.  DP/DQ select the parts present, at compile time,
+    // so no branch splits the sequence.
+    auto phase1_bf16 = [&](auto dp, auto dq, const unsigned char* ks, const unsigned char* vs) {
+        constexpr bool DP = decltype(dp)::value, DQ = decltype(dq)::value;
+        constexpr int NDC = D / 32;
+        bf16x8 kf[2][4];
+        bf16x8 vf[3][2];
+        auto load_k = [&](int dc, bf16x8 (&f)[4]) {
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) l_acc[cb] = mfma_bf16(ones, pf[kc][cb], l_acc[cb]);
-        // V fragments one feature block ahead of the MFMAs that use them
-        auto load_v = [&](int db, bf16x8 (&vf)[2]) {
+            for (int kb = 0; kb < 4; ++kb) f[kb] = *reinterpret_cast<const bf16x8*>(ks + k_off[dc] + kb * 16 * ROWB);
+        };
+        auto load_v = [&](int db, bf16x8 (&vf2)[2]) {
             const unsigned char* vp = vs + v_off[db];
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 const shortx4 lo = lds_read_tr16(reinterpret_cast<const bf16*>(vp + (kc * 32) * ROWB));
                 const shortx4 hi = lds_read_tr16(reinterpret_cast<const bf16*>(vp + (kc * 32 + 16) * ROWB));
-                vf[kc] = __builtin_bit_cast(
+                vf2[kc] = __builtin_bit_cast(
                     bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1],
                                                                           hi[2], hi[3]});
             }
         };
-        bf16x8 vf[2][2];
-        load_v(0, vf[0]);
+        if constexpr (DQ) {
+            load_k(0, kf[0]);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-            if (db + 1 < NDB) load_v(db + 1, vf[(db + 1) & 1]);
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) s[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        if constexpr (DP) {
+            load_v(0, vf[0]);
+            load_v(1, vf[1]);
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_bf16(vf[db & 1][kc], pf[kc][cb], acc[db][cb]);
+                for (int cb = 0; cb < 2; ++cb) l_acc[cb] = mfma_bf16(ones, pf[kc][cb], l_acc[cb]);
+        }
+        constexpr int NSTEP = DP ? NDB : NDC;
+#pragma unroll
+        for (int st = 0; st < NSTEP; ++st) {
+            if constexpr (DQ) {
+                if (st + 1 < NDC) load_k(st + 1, kf[(st + 1) & 1]);
+            }
+            if constexpr (DP) {
+                if (st + 2 < NDB) load_v(st + 2, vf[(st + 2) % 3]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (DP) {
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb) acc[st][cb] = mfma_bf16(vf[st % 3][kc], pf[kc][cb], acc[st][cb]);
+            }
+            if constexpr (DQ) {
+                if (st < NDC) {
+#pragma unroll
+                    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                        for (int cb = 0; cb < 2; ++cb)
+                            s[kb][cb] = mfma_bf16(kf[st & 1][kb], __builtin_bit_cast(bf16x8, qf[cb][st]), s[kb][cb]);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
-    if (nb > 0) issue(0);
+    constexpr int AHEAD = BF ? NS - 2 : NS - 1;
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k)
+        if (k < nb) issue(k);
     const int n_ticks = 2 * nb + 2;
     for (int t = 0; t < n_ticks; ++t) {
-        // even ticks: block t/2 (requested at tick t-2, the only one in
-        // flight) must have landed; always: this wave's LDS reads are done
+        // even ticks: block t/2 must have landed; the blocks requested after it
+        // may stay in flight.  Always: this wave's LDS reads are done.
         asm volatile("" ::: "memory");
-        if ((t & 1) == 0)
-            wait_vm_lgkm0<0>();
-        else
+        if ((t & 1) == 0) {
+            const int later = min(AHEAD - 1, nb - 1 - t / 2);
+            if (AHEAD >= 2 && later >= 1)
+                wait_vm_lgkm0<(AHEAD >= 2 ? Cfg::NI_TOTAL : 0)>();
+            else
+                wait_vm_lgkm0<0>();
+        } else {
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        }
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
-        if ((t & 1) == 0 && t / 2 + 1 < nb) issue(t / 2 + 1);
+        if ((t & 1) == 0 && t / 2 + AHEAD < nb) issue(t / 2 + AHEAD);
 
         const int ph = t - group;
         if (ph < 0) continue;
@@ -314,57 +362,41 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
         if ((ph & 1) == 0) {
             // ---------------- phase 1(j) ----------------
             __builtin_amdgcn_s_setprio(1);
-            if constexpr (BF) {
-                if (pv_pending) pv_bf16(j - 1);
-                pv_pending = false;
-            }
-            s_ready = false;
+            bool qk = false;
+            int base_j = 0;
             if (j < nb) {
-                int base;
-                bool is_sum, needed, full;
-                block_of(j, base, is_sum, needed, full);
-                if (needed) {
-                    s_ready = true;
-                    const unsigned char* ks = lds[j % NS][0];
-                    // S^T = K Q^T : s[kb][cb] holds keys base + kb*16 + 4g + i
+                bool is_sum, full;
+                block_of(j, base_j, is_sum, qk, full);
+            }
+            s_ready = qk;
+            const unsigned char* ks = lds[j % NS][0];
+            if constexpr (BF) {
+                const unsigned char* vs = lds[(j + NS - 1) % NS][1];
+                const std::true_type yes;
+                const std::false_type no;
+                if (pv_pending && qk)
+                    phase1_bf16(yes, yes, ks, vs);
+                else if (pv_pending)
+                    phase1_bf16(yes, no, ks, vs);
+                else if (qk)
+                    phase1_bf16(no, yes, ks, vs);
+                pv_pending = false;
+            } else if (qk) {
+                // S^T = K Q^T : s[kb][cb] holds keys base + kb*16 + 4g + i
 #pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
+                for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                        for (int cb = 0; cb < 2; ++cb) s[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-                    if constexpr (BF) {
-                        // K fragments one feature step ahead of their MFMAs
-                        bf16x8 kf[2][4];
+                    for (int cb = 0; cb < 2; ++cb) s[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                        for (int kb = 0; kb < 4; ++kb)
-                            kf[0][kb] = *reinterpret_cast<const bf16x8*>(ks + k_off[0] + kb * 16 * ROWB);
+                for (int f = 0; f < NQF; ++f) {
+                    const unsigned char* kp = ks + k_off[f];
 #pragma unroll
-                        for (int dc = 0; dc < D / 32; ++dc) {
-                            if (dc + 1 < D / 32) {
+                    for (int kb = 0; kb < 4; ++kb) {
+                        const floatx4 ka = *reinterpret_cast<const floatx4*>(kp + kb * 16 * ROWB);
 #pragma unroll
-                                for (int kb = 0; kb < 4; ++kb)
-                                    kf[(dc + 1) & 1][kb] =
-                                        *reinterpret_cast<const bf16x8*>(ks + k_off[dc + 1] + kb * 16 * ROWB);
-                            }
+                        for (int e = 0; e < 4; ++e)
 #pragma unroll
-                            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                                for (int cb = 0; cb < 2; ++cb)
-                                    s[kb][cb] = mfma_bf16(kf[dc & 1][kb], qf[cb][dc], s[kb][cb]);
-                        }
-                    } else {
-#pragma unroll
-                        for (int f = 0; f < NQF; ++f) {
-                            const unsigned char* kp = ks + k_off[f];
-#pragma unroll
-                            for (int kb = 0; kb < 4; ++kb) {
-                                const floatx4 ka = *reinterpret_cast<const floatx4*>(kp + kb * 16 * ROWB);
-#pragma unroll
-                                for (int e = 0; e < 4; ++e)
-#pragma unroll
-                                    for (int cb = 0; cb < 2; ++cb)
-                                        s[kb][cb] = mfma_f32(ka[e], qf[cb][f][e], s[kb][cb]);
-                            }
-                        }
+                            for (int cb = 0; cb < 2; ++cb) s[kb][cb] = mfma_f32(ka[e], qf[cb][f][e], s[kb][cb]);
                     }
                 }
             }
@@ -507,7 +539,7 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
     if constexpr (sizeof(T) == 2) {
-        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 3>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
+        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 4>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
                            stream, p);
     } else {
         hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 2>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
