@@ -34,7 +34,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 N_CACHES = 4
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
+PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill_mfma.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
 DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
 
 
@@ -214,7 +214,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": attn_gbs / PEAK_HBM_GBS,
                      "traffic": traffic,
-                     "kernel": "prefill_kernel<128, bf16> (eva_prefill_attention)"},
+                     "kernel": "prefill_mfma_kernel<128> (eva_prefill_attention, bf16)"},
         "prefill": {"attention_ms": ms_attn, "attention_tflops": attn_tflops,
                     "attention_mfma_frac": attn_tflops / PEAK_BF16_TFLOPS,
                     "summaries_ms": ms_summ, "summaries_gbs": summ_bytes / (ms_summ * 1e-3) / 1e9,

@@ -5,6 +5,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/eva.h"
 #include "eva_device.hpp"
 #include "eva_kernels.hpp"
@@ -162,9 +164,13 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
     p.C = C;
     p.n_chunks = n_chunks;
     p.G = H / H_kv;
-    p.Gt = gcd(p.G, eva::kPrefillWaves);
+    // workgroup geometry of the kernel that runs: bf16 -> pipelined kernel,
+    // fp32 -> two-phase kernel
+    const int waves = dtype == EVA_BF16 ? eva::kMfmaWaves : eva::kPrefillWaves;
+    const int cols = dtype == EVA_BF16 ? 16 * eva::kMfmaColBlocks : 32;
+    p.Gt = gcd(p.G, waves);
     p.n_hg = p.G / p.Gt;
-    p.pos_per_wg = 32 * eva::kPrefillWaves / p.Gt;
+    p.pos_per_wg = cols * waves / p.Gt;
     p.n_pos_tiles = (L + p.pos_per_wg - 1) / p.pos_per_wg;
     const long long tiles = (long long)B * H_kv * p.n_hg * p.n_pos_tiles;
     if (tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
@@ -173,7 +179,10 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
     p.log2C = (float)log2((double)C);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
-        return eva::launch_prefill<decltype(dd)::value, decltype(t)>(p, s);
+        if constexpr (std::is_same<decltype(t), eva::bf16>::value)
+            return eva::launch_prefill_mfma<decltype(dd)::value>(p, s);
+        else
+            return eva::launch_prefill<decltype(dd)::value, decltype(t)>(p, s);
     }));
 }
 

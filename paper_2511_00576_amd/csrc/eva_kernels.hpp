@@ -9,6 +9,9 @@ namespace eva {
 
 // Waves per prefill workgroup; each wave owns 32 query columns.
 constexpr int kPrefillWaves = 8;
+// Pipelined bf16 prefill: waves per workgroup and 16-column blocks per wave.
+constexpr int kMfmaWaves = 8;
+constexpr int kMfmaColBlocks = 2;
 
 struct PrefillParams {
     const void* Q;
@@ -30,6 +33,10 @@ struct PrefillParams {
 
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
+
+// bf16 only; tile geometry for kMfmaWaves waves of 16 kMfmaColBlocks columns.
+template <int D>
+hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream);
 
 template <int D, typename T>
 hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,

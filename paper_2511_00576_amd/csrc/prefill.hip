@@ -1,4 +1,6 @@
-// Fused window + summary EVA prefill for gfx950.
+// Fused window + summary EVA prefill for gfx950: two-phase kernel, built for
+// fp32 (the bf16 path runs the pipelined kernel of prefill_mfma.hip; the
+// template keeps its bf16 branches, which that kernel superseded).
 //
 // FlashEVA (section "FlashEVA") rewrites EVA as one softmax attention over an
 // augmented key set: the exact keys of the query's local window plus one key
@@ -548,8 +550,6 @@ hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
     return hipGetLastError();
 }
 
-template hipError_t launch_prefill<64, bf16>(const PrefillParams&, hipStream_t);
-template hipError_t launch_prefill<128, bf16>(const PrefillParams&, hipStream_t);
 template hipError_t launch_prefill<64, float>(const PrefillParams&, hipStream_t);
 template hipError_t launch_prefill<128, float>(const PrefillParams&, hipStream_t);
 

@@ -1,0 +1,572 @@
+// Fused window + summary EVA prefill for gfx950, bf16: software-pipelined
+// waves.
+//
+// The attention is the one of the fused FlashEVA formulation (section
+// "FlashEVA"): one softmax per query over the exact keys of its local window
+// and one key per chunk summary that lies fully before the window, the
+// summaries carrying a +ln C logit offset.
+//
+// Work decomposition: a workgroup is NW waves (two per SIMD) sharing one K/V
+// head; each wave owns CW = 16 NCB query columns (NCB MFMA column blocks), so
+// the workgroup covers NW CW columns = Gt heads x (NW CW / Gt) positions.
+// K/V 64-row blocks are staged HBM -> LDS by global_load_lds_dwordx4 into an
+// NS-stage ring and read by every wave; one workgroup barrier per block.
+//
+// Per wave and block j one straight-line region runs S^T(j+1) = K Q^T and
+// then O^T += V^T P^T(j) in two 32-key halves on the matrix cores, with the
+// exponentials of S(j) for the half the next product needs interleaved in the
+// same instruction stream, so the matrix cores never wait for the softmax of
+// the block they multiply.  Softmax runs in log2 units with a lazy running
+// maximum: exponentials use the stored maximum, and the cross-lane maximum
+// and the rescale of the accumulators only run when some lane sees a score
+// more than 2^8 above it.
+//
+// Masks.  Blocks entirely inside every column's visible range need none.  A
+// window block crossing the causal diagonal or the lower window edge gets one
+// of twelve bias patterns (0 / -inf, held in LDS) added to each 16 x 16 score
+// tile: the pattern depends only on the lane and on W mod 16, the choice per
+// tile only on wave-uniform offsets.  Summary blocks straddling s(n) are
+// masked per element.
+#include <type_traits>
+
+#include "eva_device.hpp"
+#include "eva_kernels.hpp"
+
+namespace eva {
+
+namespace {
+
+constexpr int kBN = 64;      // keys per block
+constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
+constexpr int kNPat = 12;    // bias patterns: 3 lower-edge x 4 upper-edge states
+
+template <int D, int NW, int NCB, int NS>
+struct MCfg {
+    static constexpr int ROWB = D * 2;         // bytes per row
+    static constexpr int CPR = ROWB / 16;      // 16-B chunks per row
+    static constexpr int BLK = kBN * ROWB;     // bytes per 64-row block
+    static constexpr int NI = BLK / 1024 / NW; // DMA instructions / wave / array
+    static_assert(NI >= 1, "block too small for the workgroup");
+    static constexpr int NI_TOTAL = 2 * NI;
+    static constexpr int NDC = D / 32;         // contraction steps of S = K Q^T
+    static constexpr int NDB = D / 16;         // 16-feature output blocks
+    static constexpr int CW = 16 * NCB;        // query columns per wave
+};
+
+// Chunk swizzles (stored chunk = logical chunk ^ swz(row)): 16-B K fragment
+// reads by 16 lanes on 16 consecutive rows, and transposing V reads by 4 lanes
+// x 8 B on each of 4 consecutive rows, both land on distinct banks.
+template <int CPR>
+__device__ __forceinline__ int mswz_k(int r) {
+    return CPR >= 16 ? (r & 15) : ((r >> 1) & 7);
+}
+template <int CPR>
+__device__ __forceinline__ int mswz_v(int r) {
+    return CPR >= 16 ? 2 * (r & 7) : 2 * ((r >> 1) & 3);
+}
+
+// s_waitcnt immediate: vmcnt(n), lgkmcnt(0), expcnt untouched.
+template <int N>
+__device__ __forceinline__ void mwait_vm_lgkm0() {
+    static_assert(N < 64, "vmcnt field is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// One global_load_lds_dwordx4 (lane i: 16 B from base + voff to LDS M0 + 16 i),
+// as inline asm so the compiler does not drain every outstanding DMA before
+// each later LDS read; the kernel waits for exactly the block it needs.
+__device__ __forceinline__ void mlds_dma16(const void* base, unsigned voff, const void* lds_dst) {
+    const unsigned m0 =
+        __builtin_amdgcn_readfirstlane((unsigned)(size_t)(__attribute__((address_space(3))) const void*)lds_dst);
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(m0) : "memory");
+}
+
+// Lower-edge state of a 16 x 16 tile whose row offset (query - key at lane
+// offset zero) is c, a multiple of 16: 0 all valid, 1 none, 2 diagonal.
+__device__ __forceinline__ int lower_state(int c) { return c >= 16 ? 0 : (c < 0 ? 1 : 2); }
+// Upper-edge state for e = W - 1 - c: 0 all valid, 1 none, 2 / 3 partial with
+// e = e1 (>= 0) or e = e1 - 16 (< 0), e1 = (W - 1) mod 16.
+__device__ __forceinline__ int upper_state(int e) { return e >= 15 ? 0 : (e < -15 ? 1 : (e >= 0 ? 2 : 3)); }
+
+template <int D, int NW, int NCB, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
+void prefill_mfma_kernel(PrefillParams a) {
+    typedef MCfg<D, NW, NCB, NS> Cfg;
+    constexpr int ROWB = Cfg::ROWB, CPR = Cfg::CPR, BLK = Cfg::BLK, NI = Cfg::NI;
+    constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, CW = Cfg::CW, NIT = Cfg::NI_TOTAL;
+    constexpr int AHEAD = NS - 1;  // blocks requested ahead of the one computed
+    static_assert(NS >= 3 && (NS & (NS - 1)) == 0, "ring of a power-of-two number of stages, at least 3");
+
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[NS][2][BLK];
+    __shared__ floatx4 pat[kNPat][64];
+    __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];  // sink of requests past the last block
+
+    const int L = a.L, W = a.W, C = a.C;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+
+    // ---- tile decode: XCD-aware remap, heavy (late) position tiles first ----
+    int id = blockIdx.x;
+    {
+        const int per = a.n_tiles / 8;
+        if (id < per * 8) id = (id % 8) * per + id / 8;
+    }
+    const int pt = a.n_pos_tiles - 1 - id % a.n_pos_tiles;
+    int rest = id / a.n_pos_tiles;
+    const int hg = rest % a.n_hg;
+    rest /= a.n_hg;
+    const int kvh = rest % a.Hkv;
+    const int b = rest / a.Hkv;
+
+    const int h = kvh * a.G + hg * a.Gt + (wave % a.Gt);
+    const int n0 = pt * a.pos_per_wg;
+    const int p0 = n0 + (wave / a.Gt) * CW;
+    const int n_hi = min(n0 + a.pos_per_wg - 1, L - 1);
+
+    // blocks the workgroup stages: summaries [0, s(n_hi)), then the window band
+    const int nsb = (visible_summaries(n_hi, W, C) + kBN - 1) / kBN;
+    const int kb0 = max(0, n0 - W + 1) / kBN;
+    const int nb = nsb + (n_hi / kBN - kb0 + 1);
+
+    // what this wave needs
+    const bool w_active = p0 < L;
+    const int wp_last = min(p0 + CW - 1, L - 1);
+    const int ws_hi = w_active ? visible_summaries(wp_last, W, C) : 0;
+    const int ws_lo = visible_summaries(p0, W, C);
+
+    // ---- request plan.  Block j's rows come from the summaries (j < nsb) or
+    // from the window band; with the band's base pointer shifted back by nsb
+    // blocks both are "base + j blocks", and the rows valid in block j are
+    // (limit - 64 j), limit being n_chunks or L shifted the same way.
+    const size_t bg = (size_t)b * a.Hkv + kvh;
+    const uintptr_t ks_base = (uintptr_t)a.Ks + bg * (size_t)a.n_chunks * ROWB;
+    const uintptr_t vs_base = (uintptr_t)a.Vs + bg * (size_t)a.n_chunks * ROWB;
+    const uintptr_t kw_base = (uintptr_t)a.K + bg * (size_t)L * ROWB + (uintptr_t)((intptr_t)(kb0 - nsb) * BLK);
+    const uintptr_t vw_base = (uintptr_t)a.V + bg * (size_t)L * ROWB + (uintptr_t)((intptr_t)(kb0 - nsb) * BLK);
+    const int sum_limit = a.n_chunks;
+    const int win_limit = L - (kb0 - nsb) * kBN;
+    // per lane: instruction i of this wave fills LDS bytes
+    // [(i*NW + wave) * 1024, +1024) of each array; lane -> (row, chunk)
+    int dma_row[NI], dma_koff[NI], dma_voff[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int byte = (i * NW + wave) * 1024 + lane * 16;
+        const int r = byte / ROWB;
+        const int pos = (byte % ROWB) / 16;
+        dma_row[i] = r;
+        dma_koff[i] = ((pos ^ mswz_k<CPR>(r)) << 4) - r * ROWB;  // added to row * ROWB
+        dma_voff[i] = ((pos ^ mswz_v<CPR>(r)) << 4) - r * ROWB;
+    }
+    // part q of block j's request: K for even q, V for odd q, instruction q/2;
+    // blocks past the last one go to a dummy LDS area, so that every wave has
+    // the same number of requests in flight at every wait
+    struct Req {
+        uintptr_t k, v;
+        int last;        // last valid row of the block
+        unsigned stage;  // LDS byte address of the block's stage
+    };
+    auto request = [&](int j) {
+        Req r;
+        const bool sum = j < nsb;
+        const bool real = j < nb;
+        const uintptr_t off = (uintptr_t)j * BLK;
+        r.k = (sum ? ks_base : kw_base) + off;
+        r.v = (sum ? vs_base : vw_base) + off;
+        r.last = min((sum ? sum_limit : win_limit) - j * kBN, kBN) - 1;
+        if (!real) {
+            r.k = (uintptr_t)a.K;  // any valid row
+            r.v = (uintptr_t)a.V;
+            r.last = 0;
+        }
+        r.stage = real ? (unsigned)(size_t)(__attribute__((address_space(3))) void*)&lds[j & (NS - 1)][0][0]
+                       : (unsigned)(size_t)(__attribute__((address_space(3))) void*)dummy;
+        return r;
+    };
+    auto issue_part = [&](const Req& r, int q) {
+        const int i = q >> 1;
+        const bool is_v = q & 1;
+        const int row = min(dma_row[i], r.last);
+        const unsigned voff = (unsigned)(row * ROWB + (is_v ? dma_voff[i] : dma_koff[i]) + dma_row[i] * ROWB);
+        // the dummy area takes every part at the same address
+        const unsigned dst = r.stage == (unsigned)(size_t)(__attribute__((address_space(3))) void*)dummy
+                                 ? r.stage
+                                 : r.stage + (is_v ? BLK : 0) + (i * NW + wave) * 1024;
+        asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(is_v ? r.v : r.k),
+                     "{m0}"(__builtin_amdgcn_readfirstlane(dst))
+                     : "memory");
+    };
+
+    // ---- bias patterns: pattern (lo, up) at lane (g, c16), element i is the
+    //      mask of query c16 vs key 4g + i of a tile with the given edge states
+    if (wave == 0) {
+        const int e1 = (W - 1) & 15;
+#pragma unroll
+        for (int p = 0; p < kNPat; ++p) {
+            const int lo = p / 4, up = p % 4;
+            floatx4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int x = c16 - 4 * g - i;  // query - key inside the tile
+                const bool lo_ok = lo == 0 || (lo == 2 && x >= 0);
+                const bool up_ok = up == 0 || (up == 2 && x <= e1) || (up == 3 && x <= e1 - 16);
+                v[i] = (lo_ok && up_ok) ? 0.f : -INFINITY;
+            }
+            pat[p][lane] = v;
+        }
+    }
+
+    auto col_n = [&](int cb) { return p0 + cb * 16 + c16; };
+
+    // ---- Q fragments (B operand of S^T = K Q^T): features dc*32 + 8g .. +7.
+    // Columns past L read row L-1: finite, and their outputs are not stored.
+    const bf16* __restrict__ Q = static_cast<const bf16*>(a.Q);
+    const size_t bh = (size_t)b * a.H + h;
+    bf16x8 qf[NCB][NDC];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+        const bf16* qrow = Q + (bh * L + (size_t)min(col_n(cb), L - 1)) * D;
+#pragma unroll
+        for (int f = 0; f < NDC; ++f) qf[cb][f] = *reinterpret_cast<const bf16x8*>(qrow + f * 32 + g * 8);
+    }
+
+    // ---- LDS read offsets ----
+    // K fragment (kb, dc): row kb*16 + c16, logical chunk dc*4 + g; offset
+    // k0 ^ (dc << 6) (kb adds an immediate kb*16*ROWB).  V transposing read:
+    // lane (g, 4j'+t) names row 4g+j' (+16 half, +32 kc), features 4t..4t+3
+    // of feature block db (logical chunk 2 db + t/2); offset v0 ^ (db << 5).
+    const int k0 = c16 * ROWB + ((g ^ mswz_k<CPR>(c16)) << 4);
+    int v0;
+    {
+        const int v_row = g * 4 + (c16 >> 2);
+        const int v_t = c16 & 3;
+        v0 = v_row * ROWB + (((v_t >> 1) ^ mswz_v<CPR>(v_row)) << 4) + (v_t & 1) * 8;
+    }
+    auto kfrag = [&](const unsigned char* ks, int kb, int dc) {
+        return *reinterpret_cast<const bf16x8*>(ks + (k0 ^ (dc << 6)) + kb * 16 * ROWB);
+    };
+    auto vfrag = [&](const unsigned char* vs, int db, int kc) {
+        const unsigned char* vp = vs + (v0 ^ (db << 5)) + kc * 32 * ROWB;
+        const shortx4 lo = lds_read_tr16(reinterpret_cast<const bf16*>(vp));
+        const shortx4 hi = lds_read_tr16(reinterpret_cast<const bf16*>(vp + 16 * ROWB));
+        return __builtin_bit_cast(
+            bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+    };
+
+    floatx4 acc[NDB][NCB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // running maxima (log2 units, identical on the four lanes of a column) and
+    // denominators: row sums of the bf16-rounded weights on the matrix cores
+    // (all-ones A operand, every output row holds the column sum)
+    float m_run[NCB];
+    floatx4 l_acc[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+        m_run[cb] = -INFINITY;
+        l_acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
+    floatx4 s0[4][NCB], s1[4][NCB];  // scores of two consecutive blocks
+    bf16x8 pf[2][NCB];               // P^T of the current block, per 32-key half
+    float lm[NCB], alpha[NCB];
+    bool pending = false;            // rescale owed to the accumulators
+
+    // block classification for this wave
+    struct Blk {
+        int base;
+        bool is_sum, needed, full;
+    };
+    auto block_of = [&](int j) {
+        Blk k;
+        k.is_sum = j < nsb;
+        k.base = k.is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
+        if (k.is_sum) {
+            k.needed = k.base < ws_hi;
+            k.full = k.base + kBN - 1 < ws_lo;
+        } else {
+            k.needed = w_active && k.base <= wp_last && k.base + kBN - 1 >= p0 - W + 1;
+            k.full = k.base >= wp_last - W + 1 && k.base + kBN - 1 <= p0;
+        }
+        return k;
+    };
+    // window block crossing an edge: every score tile gets its bias pattern
+    // added (0 or -inf per element)
+    auto add_bias = [&](floatx4 (&sd)[4][NCB], int base) {
+        const int delta = p0 - base;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int c = delta + 16 * (cb - kb);
+                sd[kb][cb] += pat[lower_state(c) * 4 + upper_state(W - 1 - c)][lane];
+            }
+    };
+    auto lane_max = [&](floatx4 (&sc)[4][NCB]) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[kb][cb][i]);
+            lm[cb] = mx;
+        }
+    };
+    // summary block straddling s(n): key base + kb*16 + 4g + i valid iff < s(n)
+    auto mask_sum = [&](floatx4 (&sc)[4][NCB], int base) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            const int lim = visible_summaries(col_n(cb), W, C) - base - g * 4;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sc[kb][cb][i] = (kb * 16 + i < lim) ? sc[kb][cb][i] : -INFINITY;
+        }
+    };
+    // lazy maximum update once the scores of a block are known; returns
+    // whether the accumulators must be rescaled by alpha
+    auto update_max = [&](float bias) -> bool {
+        bool need = false;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) need |= lm[cb] * a.scale_log2 + bias > m_run[cb] + kTau;
+        if (__ballot(need) == 0) return false;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            const float bm = xgroup_max(lm[cb]) * a.scale_log2 + bias;
+            const bool up = bm > m_run[cb] + kTau;
+            alpha[cb] = up ? fast_exp2(m_run[cb] - bm) : 1.f;
+            m_run[cb] = up ? bm : m_run[cb];
+        }
+        return true;
+    };
+    auto rescale = [&]() {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            l_acc[cb] *= alpha[cb];
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) acc[db][cb] *= alpha[cb];
+        }
+    };
+    // wait until a block landed (LATER blocks requested after it may stay in
+    // flight), then make it visible to the whole workgroup; every wave's
+    // reads of the stage about to be refilled are done as well
+    auto sync_block = [&](auto later_tag) {
+        constexpr int LATER = decltype(later_tag)::value;
+        asm volatile("" ::: "memory");
+        mwait_vm_lgkm0<LATER * NIT>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+    // ---- prologue: blocks 0 .. AHEAD-1 requested (after the queries), S^T of
+    //      block 0.  The product runs whether or not this wave needs block 0,
+    //      so that the wait for the queries sits here on every path.
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) {
+        const Req r = request(k);
+#pragma unroll
+        for (int q = 0; q < NIT; ++q) issue_part(r, q);
+    }
+    sync_block(std::integral_constant<int, AHEAD - 1>{});  // also the patterns
+    Blk kc = block_of(0);
+    {
+        const unsigned char* ks = lds[0][0];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) s0[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        bf16x8 kf[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) kf[0][kb] = kfrag(ks, kb, 0);
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc) {
+            if (dc + 1 < NDC) {
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) kf[(dc + 1) & 1][kb] = kfrag(ks, kb, dc + 1);
+            }
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) s0[kb][cb] = mfma_bf16(kf[dc & 1][kb], qf[cb][dc], s0[kb][cb]);
+        }
+        if (kc.needed) {
+            if (kc.is_sum && !kc.full) mask_sum(s0, kc.base);
+            if (!kc.is_sum && !kc.full) add_bias(s0, kc.base);
+            lane_max(s0);
+            update_max(kc.is_sum ? a.log2C : 0.f);  // acc is zero: no rescale owed
+        }
+    }
+
+    // ---- iteration j: S^T(j+1) and O^T += V^T P^T(j) ----
+    auto iteration = [&](int j, floatx4 (&sc)[4][NCB], floatx4 (&sn)[4][NCB]) {
+        // block j+1 landed (the AHEAD-2 blocks after it may stay in flight);
+        // the block requested in this iteration refills the stage of block
+        // j-1, whose last reads were before this barrier
+        sync_block(std::integral_constant<int, AHEAD - 2>{});
+        if (pending) {
+            rescale();
+            pending = false;
+        }
+        const Req req = request(j + AHEAD);
+        const bool has_next = j + 1 < nb;
+        Blk kn{0, false, false, true};
+        if (has_next) kn = block_of(j + 1);
+        const bool do_pv = kc.needed;
+        const bool do_qk = has_next && kn.needed;
+        const float bias_c = kc.is_sum ? a.log2C : 0.f;
+        const unsigned char* ks = lds[(j + 1) & (NS - 1)][0];
+        const unsigned char* vs = lds[j & (NS - 1)][1];
+        if (!do_pv && !do_qk) {
+            // nothing of blocks j, j+1 for this wave: only its share of the request
+#pragma unroll
+            for (int q = 0; q < NIT; ++q) issue_part(req, q);
+            kc = kn;
+            return;
+        }
+
+        // One straight-line region, as a sequence of steps, each with one LDS
+        // operand fragment and the matrix-core work on it:
+        //   A (4 NDC steps): S^T(j+1), key tile kb, contraction step dc  | exponentials, half 0 of S(j)
+        //   B (NDB steps):   O^T += V^T P^T, feature block db, keys 0..31 | exponentials, half 1 of S(j)
+        //   C (NDB steps):   same for keys 32..63                        | lane maxima of S(j+1)
+        // Fragments are requested PF steps ahead; a scheduling fence between
+        // steps keeps that distance (and the register count) fixed.  The
+        // parts of this iteration's request are spread over the region.  The
+        // region is the same code whether or not this wave needs block j or
+        // j+1 (alternative variants cost the register allocator dearly): a
+        // block the wave does not need gets zero weights (offset -inf) in its
+        // PV, and scores nobody needs are not used.
+        constexpr int NA = 4 * NDC;   // steps of part A
+        constexpr int N = NA + 2 * NDB;
+        constexpr int PF = 2;         // prefetch distance in steps
+        constexpr int EH = NCB * 8;   // exponentials per half block and lane
+        constexpr int MV = NCB * 16;  // scores per block and lane
+        float off[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+            off[cb] = do_pv ? bias_c - (m_run[cb] == -INFINITY ? 0.f : m_run[cb]) : -INFINITY;
+        // P^T half hf: contraction row 8g + e is key (2hf)*16 + 4g + e for
+        // e < 4, (2hf+1)*16 + 4g + e - 4 above (the V^T read uses the same order)
+        auto ex = [&](int hf, int ef) {
+            const int cb = ef / 8, e = ef % 8;
+            const float sv = sc[2 * hf + (e >> 2)][cb][e & 3];
+            pf[hf][cb][e] = to_bf16(fast_exp2(fmaf(sv, a.scale_log2, off[cb])));
+        };
+        auto mx = [&](int v) {
+            const int cb = v / 16, kb = (v % 16) / 4, i = v % 4;
+            lm[cb] = fmaxf(lm[cb], sn[kb][cb][i]);
+        };
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) lm[cb] = -INFINITY;
+        bf16x8 op[PF + 1];  // fragment ring
+        auto load = [&](int k) {
+            if (k < NA)
+                op[k % (PF + 1)] = kfrag(ks, k % 4, k / 4);
+            else
+                op[k % (PF + 1)] = vfrag(vs, (k - NA) % NDB, (k - NA) / NDB);
+        };
+        auto fetch = [&](int k) {
+            if (k + PF < N) load(k + PF);
+        };
+#pragma unroll
+        for (int k = 0; k < PF; ++k) load(k);
+#pragma unroll
+        for (int q = 0; q < NIT / 2; ++q) issue_part(req, q);
+#pragma unroll
+        for (int k = 0; k < NA; ++k) {
+            fetch(k);
+            const int kb = k % 4, dc = k / 4;
+            const bf16x8 f = op[k % (PF + 1)];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb)
+                sn[kb][cb] = mfma_bf16(f, qf[cb][dc], dc == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : sn[kb][cb]);
+#pragma unroll
+            for (int ef = k * EH / NA; ef < (k + 1) * EH / NA; ++ef) ex(0, ef);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int q = NIT / 2; q < 3 * NIT / 4; ++q) issue_part(req, q);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) l_acc[cb] = mfma_bf16(ones, pf[0][cb], l_acc[cb]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const int k = NA + db;
+            fetch(k);
+            const bf16x8 f = op[k % (PF + 1)];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(f, pf[0][cb], acc[db][cb]);
+#pragma unroll
+            for (int ef = db * EH / NDB; ef < (db + 1) * EH / NDB; ++ef) ex(1, ef);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int q = 3 * NIT / 4; q < NIT; ++q) issue_part(req, q);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) l_acc[cb] = mfma_bf16(ones, pf[1][cb], l_acc[cb]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const int k = NA + NDB + db;
+            fetch(k);
+            const bf16x8 f = op[k % (PF + 1)];
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(f, pf[1][cb], acc[db][cb]);
+#pragma unroll
+            for (int v = db * MV / NDB; v < (db + 1) * MV / NDB; ++v) mx(v);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (do_qk) {
+            // boundary blocks: masks after the product, then the lane maxima again
+            if (!kn.full) {
+                if (kn.is_sum)
+                    mask_sum(sn, kn.base);
+                else
+                    add_bias(sn, kn.base);
+                lane_max(sn);
+            }
+            pending = update_max(kn.is_sum ? a.log2C : 0.f);
+        }
+        kc = kn;
+    };
+    int j = 0;
+    for (; j + 1 < nb; j += 2) {
+        iteration(j, s0, s1);
+        iteration(j + 1, s1, s0);
+    }
+    if (j < nb) iteration(j, s0, s1);
+    if (pending) rescale();
+
+    // ---- epilogue: O = acc / l ----
+    bf16* __restrict__ O = static_cast<bf16*>(a.O);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+        const int n = col_n(cb);
+        if (n >= L) continue;
+        const float inv = 1.f / l_acc[cb][0];
+        bf16* orow = O + (bh * L + (size_t)n) * D;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const floatx4 v = acc[db][cb] * inv;
+            u32x2 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+            *reinterpret_cast<u32x2*>(orow + db * 16 + g * 4) = w;
+        }
+    }
+    // no request may still be writing LDS when the workgroup ends
+    mwait_vm_lgkm0<0>();
+}
+
+}  // namespace
+
+template <int D>
+hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
+    hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWaves, kMfmaColBlocks, 4>), dim3(p.n_tiles),
+                       dim3(kMfmaWaves * 64), 0, stream, p);
+    return hipGetLastError();
+}
+
+template hipError_t launch_prefill_mfma<64>(const PrefillParams&, hipStream_t);
+template hipError_t launch_prefill_mfma<128>(const PrefillParams&, hipStream_t);
+
+}  // namespace eva
