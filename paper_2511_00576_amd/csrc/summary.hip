@@ -31,6 +31,111 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel(const T* __res
     }
 }
 
+// Register-resident variant for chunks of exactly ROWS * RPS rows: every
+// thread requests all of its key and value rows up front (one memory latency
+// per chunk instead of one per pass), keeps them in registers, and the three
+// passes of the summary run on those registers.
+template <int D, typename T, int ROWS>
+__global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* __restrict__ K, const T* __restrict__ V,
+                                                                      T* __restrict__ Ks, T* __restrict__ Vs, int L,
+                                                                      int n_chunks) {
+    constexpr int TPR = D / 8;
+    constexpr int RPS = kSummaryThreads / TPR;
+    constexpr int C = ROWS * RPS;
+    constexpr int VW = sizeof(T) == 2 ? 1 : 2;  // 16-B words per 8 elements
+    __shared__ float red[summary_red_floats<D>()];
+    const int chunk = blockIdx.x;
+    const size_t bg = blockIdx.y;
+    const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
+    const size_t row0 = bg * (size_t)L + (size_t)chunk * C;
+    const T* kp = K + (row0 + r0) * D + cc * 8;
+    const T* vp = V + (row0 + r0) * D + cc * 8;
+
+    u32x4 kw[ROWS][VW], vw[ROWS][VW];
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i)
+#pragma unroll
+        for (int w = 0; w < VW; ++w) {
+            kw[i][w] = *reinterpret_cast<const u32x4*>(kp + (size_t)i * RPS * D + w * (8 / VW));
+            vw[i][w] = *reinterpret_cast<const u32x4*>(vp + (size_t)i * RPS * D + w * (8 / VW));
+        }
+    auto unpack = [&](const u32x4 (&x)[VW], float out[8]) {
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                out[2 * e] = bf16_lo(x[0][e]);
+                out[2 * e + 1] = bf16_hi(x[0][e]);
+            }
+        } else {
+#pragma unroll
+            for (int w = 0; w < VW; ++w)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) out[w * 4 + e] = __uint_as_float(x[w][e]);
+        }
+    };
+
+    // pass 1: mean key
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] += k[e];
+    }
+    reduce_rows8<TPR>(kh, red);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kh[e] *= 1.0f / (float)C;
+
+    // pass 2: scores (log2 units); the TPR threads of a row hold its full score
+    const float sc = kLog2e * rsqrtf((float)D);
+    float s[ROWS];
+    float amax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x += kh[e] * k[e];
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
+        s[i] = x * sc;
+        amax = fmaxf(amax, s[i]);
+    }
+    amax = block_max(amax, red);
+
+    // pass 3: softmax-weighted values
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float v[8];
+        unpack(vw[i], v);
+        const float p = fast_exp2(s[i] - amax);
+        psum += p;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += p * v[e];
+    }
+    // psum: the threads of a row group summed the same rows; reduce over rows
+#pragma unroll
+    for (int off = TPR; off < 64; off <<= 1) psum += __shfl_xor(psum, off, 64);
+    if ((t & 63) == 0) red[5 * TPR * 8 + (t >> 6)] = psum;
+    __syncthreads();
+    const float den = red[5 * TPR * 8] + red[5 * TPR * 8 + 1] + red[5 * TPR * 8 + 2] + red[5 * TPR * 8 + 3];
+    __syncthreads();
+    reduce_rows8<TPR>(acc, red);
+    if (t < TPR) {
+        const float inv = 1.0f / den;
+        const size_t out = (bg * n_chunks + chunk) * D + t * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            Ks[out + e] = from_f32<T>(kh[e]);
+            Vs[out + e] = from_f32<T>(acc[e] * inv);
+        }
+    }
+}
+
 }  // namespace
 
 template <int D, typename T>
@@ -38,6 +143,32 @@ hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, in
                             hipStream_t stream) {
     const int n_chunks = L / C;
     if (n_chunks == 0) return hipSuccess;
+    constexpr int RPS = kSummaryThreads / (D / 8);
+    if (C % RPS == 0 && C / RPS <= 8) {
+        const dim3 grid(n_chunks, BH);
+        const T* k = static_cast<const T*>(K);
+        const T* v = static_cast<const T*>(V);
+        switch (C / RPS) {
+            case 1:
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 1>), grid, dim3(kSummaryThreads), 0, stream, k, v,
+                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                return hipGetLastError();
+            case 2:
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 2>), grid, dim3(kSummaryThreads), 0, stream, k, v,
+                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                return hipGetLastError();
+            case 4:
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 4>), grid, dim3(kSummaryThreads), 0, stream, k, v,
+                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                return hipGetLastError();
+            case 8:
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 8>), grid, dim3(kSummaryThreads), 0, stream, k, v,
+                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                return hipGetLastError();
+            default:
+                break;
+        }
+    }
     const size_t lds = (size_t)(C + summary_red_floats<D>()) * sizeof(float);
     hipLaunchKernelGGL((summary_kernel<D, T>), dim3(n_chunks, BH), dim3(kSummaryThreads), lds, stream,
                        static_cast<const T*>(K), static_cast<const T*>(V), static_cast<T*>(Ks),
