@@ -538,6 +538,10 @@ void prefill_mfma_kernel(PrefillParams a) {
     if (j < nb) iteration(j, s0, s1);
     if (pending) rescale();
 
+    // No request may still be writing LDS when the workgroup ends: wait for
+    // them before the stores, which need not complete before the end.
+    mwait_vm_lgkm0<0>();
+
     // ---- epilogue: O = acc / l ----
     bf16* __restrict__ O = static_cast<bf16*>(a.O);
 #pragma unroll
@@ -553,8 +557,6 @@ void prefill_mfma_kernel(PrefillParams a) {
             *reinterpret_cast<u32x2*>(orow + db * 16 + g * 4) = w;
         }
     }
-    // no request may still be writing LDS when the workgroup ends
-    mwait_vm_lgkm0<0>();
 }
 
 }  // namespace
