@@ -166,7 +166,9 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
     p.G = H / H_kv;
     // workgroup geometry of the kernel that runs: bf16 -> pipelined kernel,
     // fp32 -> two-phase kernel
-    const int waves = dtype == EVA_BF16 ? eva::kMfmaWaves : eva::kPrefillWaves;
+    const int waves = dtype != EVA_BF16              ? eva::kPrefillWaves
+                      : eva::prefill_mfma_narrow(p.G) ? eva::kMfmaWavesNarrow
+                                                      : eva::kMfmaWavesWide;
     const int cols = dtype == EVA_BF16 ? 16 * eva::kMfmaColBlocks : 32;
     p.Gt = gcd(p.G, waves);
     p.n_hg = p.G / p.Gt;

@@ -9,9 +9,14 @@ namespace eva {
 
 // Waves per prefill workgroup; each wave owns 32 query columns.
 constexpr int kPrefillWaves = 8;
-// Pipelined bf16 prefill: waves per workgroup and 16-column blocks per wave.
-constexpr int kMfmaWaves = 8;
+// Pipelined bf16 prefill: 16-column blocks per wave (32 query columns), and
+// waves per workgroup of its two configurations: 8 waves on 64-key blocks
+// (one workgroup per CU), or 4 waves on 32-key blocks (two workgroups per CU,
+// half the positions per tile: used when every kv head has one query head).
 constexpr int kMfmaColBlocks = 2;
+constexpr int kMfmaWavesWide = 8;
+constexpr int kMfmaWavesNarrow = 4;
+inline bool prefill_mfma_narrow(int G) { return G == 1; }
 
 struct PrefillParams {
     const void* Q;
@@ -34,7 +39,7 @@ struct PrefillParams {
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
 
-// bf16 only; tile geometry for kMfmaWaves waves of 16 kMfmaColBlocks columns.
+// bf16 only; tile geometry for the configuration prefill_mfma_narrow(G) picks.
 template <int D>
 hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream);
 

@@ -6,11 +6,16 @@
 // and one key per chunk summary that lies fully before the window, the
 // summaries carrying a +ln C logit offset.
 //
-// Work decomposition: a workgroup is NW waves (two per SIMD) sharing one K/V
-// head; each wave owns CW = 16 NCB query columns (NCB MFMA column blocks), so
-// the workgroup covers NW CW columns = Gt heads x (NW CW / Gt) positions.
-// K/V 64-row blocks are staged HBM -> LDS by global_load_lds_dwordx4 into an
-// NS-stage ring and read by every wave; one workgroup barrier per block.
+// Work decomposition: a workgroup is NW waves sharing one K/V head; each wave
+// owns CW = 16 NCB query columns (NCB MFMA column blocks), so the workgroup
+// covers NW CW columns = Gt heads x (NW CW / Gt) positions.  K/V blocks of BN
+// rows are staged HBM -> LDS by global_load_lds_dwordx4 into an NS-stage ring
+// and read by every wave; one workgroup barrier per block.  Two
+// configurations: 8 waves on 64-key blocks (141 KB of LDS, one workgroup per
+// CU), and 4 waves on 32-key blocks (77 KB, two workgroups per CU, whose
+// barriers and prologues then overlap), used when each kv head serves one
+// query head, where its half-size position tiles also waste fewer blocks at
+// the window's edges.  Either way two waves share each SIMD.
 //
 // Per wave and block j one straight-line region runs S^T(j+1) = K Q^T and
 // then O^T += V^T P^T(j) in two 32-key halves on the matrix cores, with the
@@ -36,15 +41,17 @@ namespace eva {
 
 namespace {
 
-constexpr int kBN = 64;      // keys per block
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr int kNPat = 12;    // bias patterns: 3 lower-edge x 4 upper-edge states
 
-template <int D, int NW, int NCB, int NS>
+template <int D, int NW, int NCB, int NS, int BN>
 struct MCfg {
+    static_assert(BN == 32 || BN == 64, "blocks of 32 or 64 keys");
     static constexpr int ROWB = D * 2;         // bytes per row
     static constexpr int CPR = ROWB / 16;      // 16-B chunks per row
-    static constexpr int BLK = kBN * ROWB;     // bytes per 64-row block
+    static constexpr int BLK = BN * ROWB;      // bytes per block of BN rows
+    static constexpr int NKB = BN / 16;        // 16-key score tiles per block
+    static constexpr int NKC = BN / 32;        // 32-key halves of the value product
     static constexpr int NI = BLK / 1024 / NW; // DMA instructions / wave / array
     static_assert(NI >= 1, "block too small for the workgroup");
     static constexpr int NI_TOTAL = 2 * NI;
@@ -88,10 +95,11 @@ __device__ __forceinline__ int lower_state(int c) { return c >= 16 ? 0 : (c < 0 
 // e = e1 (>= 0) or e = e1 - 16 (< 0), e1 = (W - 1) mod 16.
 __device__ __forceinline__ int upper_state(int e) { return e >= 15 ? 0 : (e < -15 ? 1 : (e >= 0 ? 2 : 3)); }
 
-template <int D, int NW, int NCB, int NS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
+template <int D, int NW, int NCB, int NS, int BN, int WPE>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void prefill_mfma_kernel(PrefillParams a) {
-    typedef MCfg<D, NW, NCB, NS> Cfg;
+    typedef MCfg<D, NW, NCB, NS, BN> Cfg;
+    constexpr int kBN = BN, NKB = Cfg::NKB, NKC = Cfg::NKC;
     constexpr int ROWB = Cfg::ROWB, CPR = Cfg::CPR, BLK = Cfg::BLK, NI = Cfg::NI;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, CW = Cfg::CW, NIT = Cfg::NI_TOTAL;
     constexpr int AHEAD = NS - 1;  // blocks requested ahead of the one computed
@@ -269,8 +277,8 @@ void prefill_mfma_kernel(PrefillParams a) {
         l_acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
-    floatx4 s0[4][NCB], s1[4][NCB];  // scores of two consecutive blocks
-    bf16x8 pf[2][NCB];               // P^T of the current block, per 32-key half
+    floatx4 s0[NKB][NCB], s1[NKB][NCB];  // scores of two consecutive blocks
+    bf16x8 pf[NKC][NCB];             // P^T of the current block, per 32-key half
     float lm[NCB], alpha[NCB];
     bool pending = false;            // rescale owed to the accumulators
 
@@ -294,34 +302,34 @@ void prefill_mfma_kernel(PrefillParams a) {
     };
     // window block crossing an edge: every score tile gets its bias pattern
     // added (0 or -inf per element)
-    auto add_bias = [&](floatx4 (&sd)[4][NCB], int base) {
+    auto add_bias = [&](floatx4 (&sd)[NKB][NCB], int base) {
         const int delta = p0 - base;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int c = delta + 16 * (cb - kb);
                 sd[kb][cb] += pat[lower_state(c) * 4 + upper_state(W - 1 - c)][lane];
             }
     };
-    auto lane_max = [&](floatx4 (&sc)[4][NCB]) {
+    auto lane_max = [&](floatx4 (&sc)[NKB][NCB]) {
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
             float mx = -INFINITY;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[kb][cb][i]);
             lm[cb] = mx;
         }
     };
     // summary block straddling s(n): key base + kb*16 + 4g + i valid iff < s(n)
-    auto mask_sum = [&](floatx4 (&sc)[4][NCB], int base) {
+    auto mask_sum = [&](floatx4 (&sc)[NKB][NCB], int base) {
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
             const int lim = visible_summaries(col_n(cb), W, C) - base - g * 4;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) sc[kb][cb][i] = (kb * 16 + i < lim) ? sc[kb][cb][i] : -INFINITY;
         }
@@ -375,20 +383,20 @@ void prefill_mfma_kernel(PrefillParams a) {
     {
         const unsigned char* ks = lds[0][0];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) s0[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
         bf16x8 kf[2][4];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kf[0][kb] = kfrag(ks, kb, 0);
+        for (int kb = 0; kb < NKB; ++kb) kf[0][kb] = kfrag(ks, kb, 0);
 #pragma unroll
         for (int dc = 0; dc < NDC; ++dc) {
             if (dc + 1 < NDC) {
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) kf[(dc + 1) & 1][kb] = kfrag(ks, kb, dc + 1);
+                for (int kb = 0; kb < NKB; ++kb) kf[(dc + 1) & 1][kb] = kfrag(ks, kb, dc + 1);
             }
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb) s0[kb][cb] = mfma_bf16(kf[dc & 1][kb], qf[cb][dc], s0[kb][cb]);
         }
@@ -401,7 +409,7 @@ void prefill_mfma_kernel(PrefillParams a) {
     }
 
     // ---- iteration j: S^T(j+1) and O^T += V^T P^T(j) ----
-    auto iteration = [&](int j, floatx4 (&sc)[4][NCB], floatx4 (&sn)[4][NCB]) {
+    auto iteration = [&](int j, floatx4 (&sc)[NKB][NCB], floatx4 (&sn)[NKB][NCB]) {
         // block j+1 landed (the AHEAD-2 blocks after it may stay in flight);
         // the block requested in this iteration refills the stage of block
         // j-1, whose last reads were before this barrier
@@ -439,11 +447,11 @@ void prefill_mfma_kernel(PrefillParams a) {
         // j+1 (alternative variants cost the register allocator dearly): a
         // block the wave does not need gets zero weights (offset -inf) in its
         // PV, and scores nobody needs are not used.
-        constexpr int NA = 4 * NDC;   // steps of part A
-        constexpr int N = NA + 2 * NDB;
-        constexpr int PF = 2;         // prefetch distance in steps
-        constexpr int EH = NCB * 8;   // exponentials per half block and lane
-        constexpr int MV = NCB * 16;  // scores per block and lane
+        constexpr int NA = NKB * NDC;  // steps of part A
+        constexpr int N = NA + NKC * NDB;
+        constexpr int PF = 2;          // prefetch distance in steps
+        constexpr int EH = NCB * 8;    // exponentials per 32-key half and lane
+        constexpr int MV = NCB * NKB * 4;  // scores per block and lane
         float off[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
@@ -456,7 +464,7 @@ void prefill_mfma_kernel(PrefillParams a) {
             pf[hf][cb][e] = to_bf16(fast_exp2(fmaf(sv, a.scale_log2, off[cb])));
         };
         auto mx = [&](int v) {
-            const int cb = v / 16, kb = (v % 16) / 4, i = v % 4;
+            const int cb = v / (NKB * 4), kb = (v % (NKB * 4)) / 4, i = v % 4;
             lm[cb] = fmaxf(lm[cb], sn[kb][cb][i]);
         };
 #pragma unroll
@@ -464,7 +472,7 @@ void prefill_mfma_kernel(PrefillParams a) {
         bf16x8 op[PF + 1];  // fragment ring
         auto load = [&](int k) {
             if (k < NA)
-                op[k % (PF + 1)] = kfrag(ks, k % 4, k / 4);
+                op[k % (PF + 1)] = kfrag(ks, k % NKB, k / NKB);
             else
                 op[k % (PF + 1)] = vfrag(vs, (k - NA) % NDB, (k - NA) / NDB);
         };
@@ -478,7 +486,7 @@ void prefill_mfma_kernel(PrefillParams a) {
 #pragma unroll
         for (int k = 0; k < NA; ++k) {
             fetch(k);
-            const int kb = k % 4, dc = k / 4;
+            const int kb = k % NKB, dc = k / NKB;
             const bf16x8 f = op[k % (PF + 1)];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
@@ -498,24 +506,31 @@ void prefill_mfma_kernel(PrefillParams a) {
             const bf16x8 f = op[k % (PF + 1)];
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(f, pf[0][cb], acc[db][cb]);
+            if constexpr (NKC == 2) {
 #pragma unroll
-            for (int ef = db * EH / NDB; ef < (db + 1) * EH / NDB; ++ef) ex(1, ef);
+                for (int ef = db * EH / NDB; ef < (db + 1) * EH / NDB; ++ef) ex(1, ef);
+            } else {
+#pragma unroll
+                for (int v = db * MV / NDB; v < (db + 1) * MV / NDB; ++v) mx(v);
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int q = 3 * NIT / 4; q < NIT; ++q) issue_part(req, q);
+        if constexpr (NKC == 2) {
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) l_acc[cb] = mfma_bf16(ones, pf[1][cb], l_acc[cb]);
+            for (int cb = 0; cb < NCB; ++cb) l_acc[cb] = mfma_bf16(ones, pf[NKC - 1][cb], l_acc[cb]);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-            const int k = NA + NDB + db;
-            fetch(k);
-            const bf16x8 f = op[k % (PF + 1)];
+            for (int db = 0; db < NDB; ++db) {
+                const int k = NA + NDB + db;
+                fetch(k);
+                const bf16x8 f = op[k % (PF + 1)];
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(f, pf[1][cb], acc[db][cb]);
+                for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(f, pf[NKC - 1][cb], acc[db][cb]);
 #pragma unroll
-            for (int v = db * MV / NDB; v < (db + 1) * MV / NDB; ++v) mx(v);
-            __builtin_amdgcn_sched_barrier(0);
+                for (int v = db * MV / NDB; v < (db + 1) * MV / NDB; ++v) mx(v);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         if (do_qk) {
             // boundary blocks: masks after the product, then the lane maxima again
@@ -563,8 +578,15 @@ void prefill_mfma_kernel(PrefillParams a) {
 
 template <int D>
 hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
-    hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWaves, kMfmaColBlocks, 4>), dim3(p.n_tiles),
-                       dim3(kMfmaWaves * 64), 0, stream, p);
+    if (prefill_mfma_narrow(p.G)) {
+        // 4 waves x 32 columns, 32-key blocks: 77 KB of LDS, two workgroups per CU
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2>), dim3(p.n_tiles),
+                           dim3(kMfmaWavesNarrow * 64), 0, stream, p);
+    } else {
+        // 8 waves x 32 columns, 64-key blocks: 141 KB of LDS, one workgroup per CU
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesWide, kMfmaColBlocks, 4, 64, 2>), dim3(p.n_tiles),
+                           dim3(kMfmaWavesWide * 64), 0, stream, p);
+    }
     return hipGetLastError();
 }
 
