@@ -168,6 +168,95 @@ int eva_decode_step(const eva_cache* cache, const void* q, void* o,
 /* Workspace that lets eva_decode_step split rows across workgroups. */
 size_t eva_decode_workspace_bytes(const eva_cache* cache);
 
+/*
+ * Ragged decode cache: batched generation where every sequence of the batch
+ * holds its own number of tokens (section "Inference throughput and Memory
+ * usage": many sequences generated in parallel after a prompt; prompts of
+ * different lengths make the batch ragged).  The arrays and their layouts are
+ * those of eva_cache; what differs is that the token counts live in device
+ * memory and are read and advanced by the kernels themselves, so a generation
+ * step carries no host-side state and a captured graph of it can be replayed.
+ *   n_tok    device int32 [B]: tokens held by sequence b (set by
+ *            eva_rcache_fill, advanced by eva_rcache_append)
+ *   arrive   device int32 [B]: the library's per-sequence arrival counters;
+ *            the caller zeroes them once, every call leaves them zero
+ *   max_tok  host: the most tokens any sequence may hold.  S_max must hold
+ *            the summaries of a sequence of max_tok tokens (S_max >=
+ *            floor((max_tok - W) / C) when max_tok > W).  A sequence that is
+ *            full ignores further appends (its n_tok stays max_tok).
+ * Sequence b's position p lives in ring slot p mod R of row (b, kv head),
+ * exactly as in eva_cache.  Requirements on R and S_max as for eva_cache.
+ */
+typedef struct eva_rcache {
+    int B, H, H_kv, d, W, C;
+    int dtype;        /* eva_dtype; decode needs EVA_BF16 */
+    int R;
+    int S_max;
+    int max_tok;
+    int* n_tok;
+    int* arrive;
+    void* k_ring;
+    void* vt_ring;
+    void* k_sum;
+    void* vt_sum;
+} eva_rcache;
+
+/*
+ * Load a ragged cache from a right-padded prefill: K, V [B][H_kv][L][d] and
+ * their summaries Ksum, Vsum [B][H_kv][L / C][d] (eva_build_summaries over
+ * the padded batch; causality makes every row and every complete chunk below
+ * a sequence's own length independent of the padding).  lens is device int32
+ * [B], the valid length of each sequence; a length is clamped to
+ * [0, min(L, max_tok)].  For each b the last min(len, R) positions go to the
+ * ring, summaries c < len / C to the summary arrays, and n_tok[b] = len.
+ * Errors: INVALID (malformed cache, null pointers, L < 1), CAPACITY
+ * (S_max < min(L, max_tok) / C).
+ */
+int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                    int L, const int* lens, void* stream);
+
+/*
+ * Append one token to every active sequence: k_new, v_new [B][H_kv][d].
+ * Sequence b's token takes position p = n_tok[b]; if p makes chunk
+ * s(p) - 1 newly visible, that summary is first built from the ring (as in
+ * eva_cache_append), then the token is written and n_tok[b] becomes p + 1.
+ * `active` is device int32 [B] (nonzero = append) or NULL for all; inactive
+ * and full sequences are left unchanged.
+ * Errors: INVALID (malformed cache, null pointers).
+ */
+int eva_rcache_append(const eva_rcache* cache, const void* k_new, const void* v_new, const int* active,
+                      void* stream);
+
+/*
+ * One decode step of every active sequence: q [B][H][d] holds, for each b,
+ * the query of position n_tok[b] - 1 (its token appended last); o [B][H][d]
+ * receives the EVA attention output over that sequence's window and visible
+ * summaries, the result of eva_decode_step for a cache holding n_tok[b]
+ * tokens.  Rows of inactive sequences and of sequences holding no token are
+ * not written.  `ws` as in eva_decode_step, sized by
+ * eva_rdecode_workspace_bytes (splits are chosen for the longest sequence a
+ * cache of max_tok tokens may hold).
+ * Errors: INVALID (malformed cache, null pointers), UNSUPPORTED (dtype other
+ * than EVA_BF16).
+ */
+int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
+                     size_t ws_bytes, void* stream);
+
+/* Workspace that lets eva_rdecode_step split rows across workgroups. */
+size_t eva_rdecode_workspace_bytes(const eva_rcache* cache);
+
+/*
+ * T generation steps (section "Inference throughput and Memory usage"): for
+ * t = 0 .. T-1, append token t of every active sequence and decode it.
+ *   q, o  [T][B][H][d];  k, v  [T][B][H_kv][d]
+ * Equivalent to T calls of eva_rcache_append(k[t], v[t]) followed by
+ * eva_rdecode_step(q[t]) -> o[t]; all launches are enqueued on `stream`
+ * before the call returns (the caller may capture them into a graph).
+ * Errors: as eva_rcache_append and eva_rdecode_step; INVALID for T < 1.
+ */
+int eva_generate(const eva_rcache* cache, const void* q, const void* k, const void* v, void* o, int T,
+                 const int* active, void* ws, size_t ws_bytes, void* stream);
+
 /* Static description of an eva_status value. */
 const char* eva_status_string(int status);
 

@@ -26,6 +26,11 @@ SYMBOLS = (
     "eva_cache_append",
     "eva_decode_step",
     "eva_decode_workspace_bytes",
+    "eva_rcache_fill",
+    "eva_rcache_append",
+    "eva_rdecode_step",
+    "eva_rdecode_workspace_bytes",
+    "eva_generate",
     "eva_status_string",
 )
 
@@ -35,6 +40,17 @@ class EvaCacheStruct(ctypes.Structure):
         ("B", ctypes.c_int), ("H", ctypes.c_int), ("H_kv", ctypes.c_int), ("d", ctypes.c_int),
         ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("R", ctypes.c_int),
         ("S_max", ctypes.c_int), ("n_tok", ctypes.c_longlong),
+        ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
+        ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
+    ]
+
+
+class EvaRCacheStruct(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int), ("H", ctypes.c_int), ("H_kv", ctypes.c_int), ("d", ctypes.c_int),
+        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("R", ctypes.c_int),
+        ("S_max", ctypes.c_int), ("max_tok", ctypes.c_int),
+        ("n_tok", ctypes.c_void_p), ("arrive", ctypes.c_void_p),
         ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
         ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
     ]
@@ -68,6 +84,17 @@ def load():
     lib.eva_decode_step.argtypes = [cp, vp, vp, vp, sz, vp]
     lib.eva_decode_workspace_bytes.restype = sz
     lib.eva_decode_workspace_bytes.argtypes = [cp]
+    rp = ctypes.POINTER(EvaRCacheStruct)
+    lib.eva_rcache_fill.restype = i
+    lib.eva_rcache_fill.argtypes = [rp, vp, vp, vp, vp, i, vp, vp]
+    lib.eva_rcache_append.restype = i
+    lib.eva_rcache_append.argtypes = [rp, vp, vp, vp, vp]
+    lib.eva_rdecode_step.restype = i
+    lib.eva_rdecode_step.argtypes = [rp, vp, vp, vp, vp, sz, vp]
+    lib.eva_rdecode_workspace_bytes.restype = sz
+    lib.eva_rdecode_workspace_bytes.argtypes = [rp]
+    lib.eva_generate.restype = i
+    lib.eva_generate.argtypes = [rp, vp, vp, vp, vp, i, vp, vp, sz, vp]
     lib.eva_status_string.restype = ctypes.c_char_p
     lib.eva_status_string.argtypes = [i]
     _lib = lib

@@ -29,13 +29,27 @@ namespace {
 // they occupy 32 consecutive slots) or 32 summaries.  Keys are copied row by
 // row; values go through LDS so the transposed store writes 32 consecutive
 // slots (64 B in bf16) per feature row instead of scattered elements.
+// Source arrays have L rows (K, V) and n_chunks rows (Ks, Vs) per (b, g).
+// With `lens` each sequence copies only its own valid prefix: the tiles are
+// counted from that sequence's first ring position, and tiles past its
+// length do nothing.
 template <int D, typename T>
 __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* __restrict__ K, const T* __restrict__ V,
                                                          const T* __restrict__ Ks, const T* __restrict__ Vs, int L,
-                                                         int n_chunks, int ring_tiles) {
+                                                         int n_chunks, int ring_tiles, const int* __restrict__ lens,
+                                                         RaggedState rs) {
     __shared__ T tile[32][D + 2];
     const size_t bg = blockIdx.y;
-    const int first = max(0, L - c.R);
+    int len = L;
+    if (lens) {
+        const int b = (int)blockIdx.y / c.Hkv;
+        len = min(max(lens[b], 0), min(L, rs.max_tok));
+        if (blockIdx.x == 0 && (int)blockIdx.y % c.Hkv == 0 && threadIdx.x == 0) {
+            rs.n_tok[b] = len;
+            rs.arrive[b] = 0;
+        }
+    }
+    const int first = max(0, len - c.R);
     const bool ring = (int)blockIdx.x < ring_tiles;
     int r0, r1, dst0, ld_dst;  // source rows [r0, r1), destination slot/index of r0
     const T *src_k, *src_v;
@@ -43,7 +57,7 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
     if (ring) {
         const int p0 = (first / 32 + (int)blockIdx.x) * 32;
         r0 = max(p0, first);
-        r1 = min(p0 + 32, L);
+        r1 = min(p0 + 32, len);
         dst0 = r0 % c.R;
         ld_dst = c.R;
         src_k = K + bg * (size_t)L * D;
@@ -52,7 +66,7 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
         dst_vt = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
     } else {
         r0 = ((int)blockIdx.x - ring_tiles) * 32;
-        r1 = min(r0 + 32, n_chunks);
+        r1 = min(r0 + 32, len / c.C);
         dst0 = r0;
         ld_dst = c.S_max;
         src_k = Ks + bg * (size_t)n_chunks * D;
@@ -60,7 +74,7 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
         dst_k = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
         dst_vt = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
     }
-    const int rows = r1 - r0;
+    const int rows = max(r1 - r0, 0);
     for (int e = threadIdx.x; e < rows * D; e += blockDim.x) {
         const int r = e / D, d = e % D;
         dst_k[(size_t)(dst0 + r) * D + d] = src_k[(size_t)(r0 + r) * D + d];
@@ -108,11 +122,93 @@ __global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView
 }
 
 // ---------------------------------------------------------------------------
+// ragged append (one workgroup per (b, kv head); positions from device memory)
+// ---------------------------------------------------------------------------
+// Index of the chunk summary that becomes visible at position p (the first
+// position whose window starts past the chunk's end), or -1.
+__device__ inline int summary_due(int p, int W, int C) {
+    const int start = p - W + 1;
+    return (start > 0 && start % C == 0) ? start / C - 1 : -1;
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheView c, RaggedState rs,
+                                                                        const T* __restrict__ k_new,
+                                                                        const T* __restrict__ v_new) {
+    extern __shared__ float smem[];
+    __shared__ int sh_p;
+    const size_t bg = blockIdx.x;
+    const int b = (int)blockIdx.x / c.Hkv;
+    if (rs.active && rs.active[b] == 0) return;
+    if (threadIdx.x == 0) sh_p = rs.n_tok[b];
+    __syncthreads();
+    const int p = sh_p;
+    if (p >= rs.max_tok) return;  // full: every workgroup of the sequence agrees
+    T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
+    T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
+    const int s_new = summary_due(p, c.W, c.C);
+    if (s_new >= 0 && s_new < c.S_max) {
+        RingChunk<D, T> src{kr, vr, (long long)s_new * c.C, c.R};
+        float kh[8], vh[8];
+        chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
+        const int t = threadIdx.x;
+        if (t < D / 8) {
+            T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
+            T* vs = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                ks[(size_t)s_new * D + t * 8 + i] = from_f32<T>(kh[i]);
+                vs[(size_t)(t * 8 + i) * c.S_max + s_new] = from_f32<T>(vh[i]);
+            }
+        }
+        __syncthreads();  // every read of the chunk precedes the slot overwrite below
+    }
+    const int slot = p % c.R;
+    for (int d = threadIdx.x; d < D; d += blockDim.x) {
+        kr[(size_t)slot * D + d] = k_new[bg * D + d];
+        vr[(size_t)d * c.R + slot] = v_new[bg * D + d];
+    }
+    // Every workgroup of sequence b read n_tok[b] before arriving, so the
+    // last to arrive may advance it; it also re-arms the counter.
+    if (threadIdx.x == 0) {
+        if (atomicAdd(&rs.arrive[b], 1) == c.Hkv - 1) {
+            rs.arrive[b] = 0;
+            rs.n_tok[b] = p + 1;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // decode step
 // ---------------------------------------------------------------------------
 constexpr int kDecWaves = 4;
 
-template <int D>
+// Query position and chunk ranges of one decode row.
+struct DecodeGeom {
+    int p, n_sum, win_lo, n_sum_chunks, n_win_chunks, first_win_chunk;
+};
+
+// Geometry of sequence b: from the host-computed fields (uniform cache) or
+// from the sequence's own token count (ragged cache).  valid = false when
+// the sequence takes no part in this step or holds no token.
+template <bool RAGGED>
+__device__ inline DecodeGeom decode_geom(const DecodeParams& a, int b, bool& valid) {
+    DecodeGeom g{a.p, a.n_sum, a.win_lo, a.n_sum_chunks, a.n_win_chunks, a.first_win_chunk};
+    valid = true;
+    if constexpr (RAGGED) {
+        const int n = min(a.n_tok[b], a.max_tok);
+        valid = n > 0 && !(a.active && a.active[b] == 0);
+        g.p = n - 1;
+        g.win_lo = max(0, g.p - a.c.W + 1);
+        g.n_sum = min(g.win_lo / a.c.C, a.c.S_max);  // s(p)
+        g.n_sum_chunks = (g.n_sum + 31) / 32;
+        g.first_win_chunk = g.win_lo / 32;
+        g.n_win_chunks = g.p / 32 - g.first_win_chunk + 1;
+    }
+    return g;
+}
+
+template <int D, bool RAGGED>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     typedef bf16 T;
     constexpr int NDC = D / 32;  // 32-feature contraction steps
@@ -126,6 +222,9 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     const int hg = blockIdx.y % a.n_hg;
     const int b = blockIdx.z;
     const CacheView& c = a.c;
+    bool valid;
+    const DecodeGeom geo = decode_geom<RAGGED>(a, b, valid);
+    if (!valid) return;  // uniform across the workgroup
     const size_t bg = (size_t)b * c.Hkv + kvh;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 4, c16 = lane & 15;
@@ -153,7 +252,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     for (int db = 0; db < NDB; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    const int n_chunks = a.n_sum_chunks + a.n_win_chunks;
+    const int n_chunks = geo.n_sum_chunks + geo.n_win_chunks;
     const int worker = split * kDecWaves + wave;
     const int n_workers = a.splits * kDecWaves;
     // key row of the A operand for S^T block kb (row c16 of the 16-row block):
@@ -161,7 +260,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     const int krow0 = (c16 >> 2) * 8 + (c16 & 3);
 
     for (int ch = worker; ch < n_chunks; ch += n_workers) {
-        const bool is_sum = ch < a.n_sum_chunks;
+        const bool is_sum = ch < geo.n_sum_chunks;
         const T* kbase;
         const T* vbase;  // element (d, key) at vbase + d * vstride + key
         int vstride, key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
@@ -171,15 +270,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
             vbase = vsum + r0;
             vstride = c.S_max;
             key_lo = 0;
-            key_hi = min(31, a.n_sum - 1 - r0);
+            key_hi = min(31, geo.n_sum - 1 - r0);
         } else {
-            const int pos0 = (a.first_win_chunk + ch - a.n_sum_chunks) * 32;
+            const int pos0 = (geo.first_win_chunk + ch - geo.n_sum_chunks) * 32;
             const int slot0 = pos0 % c.R;
             kbase = kring + (size_t)slot0 * D;
             vbase = vring + slot0;
             vstride = c.R;
-            key_lo = max(0, a.win_lo - pos0);
-            key_hi = min(31, a.p - pos0);
+            key_lo = max(0, geo.win_lo - pos0);
+            key_hi = min(31, geo.p - pos0);
         }
         const bool full = key_lo == 0 && key_hi == 31;
 
@@ -304,13 +403,16 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     }
 }
 
-template <int D>
+template <int D, bool RAGGED>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
     typedef bf16 T;
     const int kvh = blockIdx.y / a.n_hg;
     const int hg = blockIdx.y % a.n_hg;
     const int b = blockIdx.z;
     const CacheView& c = a.c;
+    bool valid;
+    decode_geom<RAGGED>(a, b, valid);
+    if (!valid) return;  // no partials were written for this sequence
     const int ncols = min(16, a.G - hg * 16);
     const float* base = a.ws + (((size_t)b * c.Hkv + kvh) * a.n_hg + hg) * a.splits * 16 * (D + 2);
     for (int e = threadIdx.x; e < ncols * D; e += blockDim.x) {
@@ -333,15 +435,22 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
 
 template <int D, typename T>
 hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,
-                             int L, hipStream_t stream) {
+                             int L, const int* lens, const RaggedState& r, hipStream_t stream) {
     const int n_chunks = L / c.C;
-    const int first = max(0, L - c.R);
-    const int ring_tiles = (L - 1) / 32 - first / 32 + 1;
+    int ring_tiles;
+    if (lens) {
+        // any length up to L: min(L, R) positions from an arbitrary start
+        // touch at most min(L, R) / 32 + 1 aligned 32-position tiles
+        ring_tiles = min(L, c.R) / 32 + 1;
+    } else {
+        const int first = max(0, L - c.R);
+        ring_tiles = (L - 1) / 32 - first / 32 + 1;
+    }
     const int sum_tiles = (n_chunks + 31) / 32;
     dim3 grid(ring_tiles + sum_tiles, c.B * c.Hkv);
     hipLaunchKernelGGL((cache_fill_kernel<D, T>), grid, dim3(256), 0, stream, c, static_cast<const T*>(K),
                        static_cast<const T*>(V), static_cast<const T*>(Ks), static_cast<const T*>(Vs), L, n_chunks,
-                       ring_tiles);
+                       ring_tiles, lens, r);
     return hipGetLastError();
 }
 
@@ -355,24 +464,48 @@ hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void
 }
 
 template <int D, typename T>
-hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
-    static_assert(sizeof(T) == 2, "decode runs on bf16 caches");
-    dim3 grid(p.splits, p.c.Hkv * p.n_hg, p.c.B);
-    hipLaunchKernelGGL((decode_kernel<D>), grid, dim3(256), 0, stream, p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.splits == 1) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(1, p.c.Hkv * p.n_hg, p.c.B), dim3(256), 0, stream, p);
+hipError_t launch_rcache_append(const CacheView& c, const RaggedState& r, const void* k_new, const void* v_new,
+                                hipStream_t stream) {
+    // any sequence may owe a summary this step
+    const size_t lds = (size_t)(c.C + summary_red_floats<D>()) * sizeof(float);
+    hipLaunchKernelGGL((rcache_append_kernel<D, T>), dim3(c.B * c.Hkv), dim3(kSummaryThreads), lds, stream, c, r,
+                       static_cast<const T*>(k_new), static_cast<const T*>(v_new));
     return hipGetLastError();
 }
 
-template hipError_t launch_cache_fill<64, bf16>(const CacheView&, const void*, const void*, const void*, const void*,
-                                                int, hipStream_t);
-template hipError_t launch_cache_fill<128, bf16>(const CacheView&, const void*, const void*, const void*,
-                                                 const void*, int, hipStream_t);
-template hipError_t launch_cache_fill<64, float>(const CacheView&, const void*, const void*, const void*,
-                                                 const void*, int, hipStream_t);
-template hipError_t launch_cache_fill<128, float>(const CacheView&, const void*, const void*, const void*,
-                                                  const void*, int, hipStream_t);
+template <int D, bool RAGGED>
+hipError_t launch_decode_impl(const DecodeParams& p, hipStream_t stream) {
+    dim3 grid(p.splits, p.c.Hkv * p.n_hg, p.c.B);
+    hipLaunchKernelGGL((decode_kernel<D, RAGGED>), grid, dim3(256), 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.splits == 1) return e;
+    hipLaunchKernelGGL((decode_combine_kernel<D, RAGGED>), dim3(1, p.c.Hkv * p.n_hg, p.c.B), dim3(256), 0, stream,
+                       p);
+    return hipGetLastError();
+}
+
+template <int D, typename T>
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
+    static_assert(sizeof(T) == 2, "decode runs on bf16 caches");
+    return p.n_tok ? launch_decode_impl<D, true>(p, stream) : launch_decode_impl<D, false>(p, stream);
+}
+
+#define EVA_FILL(D, T)                                                                                      \
+    template hipError_t launch_cache_fill<D, T>(const CacheView&, const void*, const void*, const void*, \
+                                                const void*, int, const int*, const RaggedState&, hipStream_t);
+EVA_FILL(64, bf16)
+EVA_FILL(128, bf16)
+EVA_FILL(64, float)
+EVA_FILL(128, float)
+#undef EVA_FILL
+#define EVA_RAPPEND(D, T)                                                                                 \
+    template hipError_t launch_rcache_append<D, T>(const CacheView&, const RaggedState&, const void*, \
+                                                   const void*, hipStream_t);
+EVA_RAPPEND(64, bf16)
+EVA_RAPPEND(128, bf16)
+EVA_RAPPEND(64, float)
+EVA_RAPPEND(128, float)
+#undef EVA_RAPPEND
 template hipError_t launch_cache_append<64, bf16>(const CacheView&, const void*, const void*, int, hipStream_t);
 template hipError_t launch_cache_append<128, bf16>(const CacheView&, const void*, const void*, int, hipStream_t);
 template hipError_t launch_cache_append<64, float>(const CacheView&, const void*, const void*, int, hipStream_t);

@@ -95,6 +95,54 @@ int decode_splits(int units, int n_chunks) {
     return s < 1 ? 1 : s;
 }
 
+int check_rcache(const eva_rcache* c) {
+    if (!c) return EVA_ERR_INVALID;
+    if (c->B < 1 || c->H < 1 || c->H_kv < 1 || c->H % c->H_kv != 0 || c->W < 1 || c->C < 1 || c->C > kMaxChunk)
+        return EVA_ERR_INVALID;
+    int st = supported(c->d, c->dtype);
+    if (st != EVA_OK) return st;
+    if (!c->k_ring || !c->vt_ring || !c->k_sum || !c->vt_sum || !c->n_tok || !c->arrive) return EVA_ERR_INVALID;
+    if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
+        return EVA_ERR_INVALID;
+    if (c->max_tok < 1) return EVA_ERR_INVALID;
+    if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
+    if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
+    // the last summary a sequence of max_tok tokens makes due
+    if (visible_summaries(c->max_tok - 1, c->W, c->C) > c->S_max) return EVA_ERR_CAPACITY;
+    if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    return EVA_OK;
+}
+
+eva::CacheView rview_of(const eva_rcache* c) {
+    eva::CacheView v;
+    v.B = c->B;
+    v.H = c->H;
+    v.Hkv = c->H_kv;
+    v.W = c->W;
+    v.C = c->C;
+    v.R = c->R;
+    v.S_max = c->S_max;
+    v.n_tok = 0;  // per-sequence counts live in device memory
+    v.k_ring = c->k_ring;
+    v.vt_ring = c->vt_ring;
+    v.k_sum = c->k_sum;
+    v.vt_sum = c->vt_sum;
+    return v;
+}
+
+eva::RaggedState rstate_of(const eva_rcache* c, const int* active) {
+    return eva::RaggedState{c->n_tok, c->arrive, active, c->max_tok};
+}
+
+// Most 32-row chunks a decode row of a ragged cache can touch: the summaries
+// of a sequence at max_tok tokens plus a window starting anywhere in a tile.
+int rdecode_max_chunks(const eva_rcache* c) {
+    int n_sum = visible_summaries(c->max_tok - 1, c->W, c->C);
+    if (n_sum > c->S_max) n_sum = c->S_max;
+    const int win = c->W < c->max_tok ? c->W : c->max_tok;
+    return (n_sum + 31) / 32 + (win + 30) / 32 + 1;
+}
+
 int decode_chunks(const eva_cache* c, long long p, int* n_sum_out, int* win_lo_out, int* n_sum_chunks,
                   int* n_win_chunks) {
     const int n_sum = visible_summaries(p, c->W, c->C);
@@ -198,8 +246,9 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
     if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
     eva::CacheView v = view_of(cache);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    const eva::RaggedState none{};
     hipError_t e = dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
-        return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, s);
+        return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, nullptr, none, s);
     });
     if (e != hipSuccess) return EVA_ERR_HIP;
     cache->n_tok = L;
@@ -293,9 +342,107 @@ int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, si
     p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
     p.log2C = (float)log2((double)cache->C);
+    p.n_tok = nullptr;
+    p.active = nullptr;
+    p.max_tok = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
     return hip_status(e);
+}
+
+// ---------------------------------------------------------------------------
+// ragged caches
+// ---------------------------------------------------------------------------
+
+int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                    int L, const int* lens, void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (L < 1 || !K || !V || !lens) return EVA_ERR_INVALID;
+    if (!aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
+    const int n_chunks = L / cache->C;
+    if (n_chunks > 0 && (!Ksum || !Vsum)) return EVA_ERR_INVALID;
+    if (cache->S_max < (L < cache->max_tok ? L : cache->max_tok) / cache->C) return EVA_ERR_CAPACITY;
+    eva::CacheView v = rview_of(cache);
+    const eva::RaggedState r = rstate_of(cache, nullptr);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
+        return eva::launch_cache_fill<decltype(dd)::value, decltype(t)>(v, K, V, Ksum, Vsum, L, lens, r, s);
+    }));
+}
+
+int eva_rcache_append(const eva_rcache* cache, const void* k_new, const void* v_new, const int* active,
+                      void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (!k_new || !v_new) return EVA_ERR_INVALID;
+    eva::CacheView v = rview_of(cache);
+    const eva::RaggedState r = rstate_of(cache, active);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
+        return eva::launch_rcache_append<decltype(dd)::value, decltype(t)>(v, r, k_new, v_new, s);
+    }));
+}
+
+size_t eva_rdecode_workspace_bytes(const eva_rcache* cache) {
+    if (check_rcache(cache) != EVA_OK) return 0;
+    const int G = cache->H / cache->H_kv;
+    const int n_hg = (G + 15) / 16;
+    const int units = cache->B * cache->H_kv * n_hg;
+    const int splits = decode_splits(units, rdecode_max_chunks(cache));
+    if (splits == 1) return 0;
+    return (size_t)units * splits * 16 * (cache->d + 2) * sizeof(float);
+}
+
+int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
+                     size_t ws_bytes, void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
+
+    eva::DecodeParams p{};
+    p.c = rview_of(cache);
+    p.q = q;
+    p.o = o;
+    p.G = cache->H / cache->H_kv;
+    p.n_hg = (p.G + 15) / 16;
+    const int units = cache->B * cache->H_kv * p.n_hg;
+    p.splits = decode_splits(units, rdecode_max_chunks(cache));
+    const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
+    if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
+    p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
+    p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
+    p.log2C = (float)log2((double)cache->C);
+    p.n_tok = cache->n_tok;
+    p.active = active;
+    p.max_tok = cache->max_tok;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    return hip_status(e);
+}
+
+int eva_generate(const eva_rcache* cache, const void* q, const void* k, const void* v, void* o, int T,
+                 const int* active, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (T < 1 || !q || !k || !v || !o) return EVA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return EVA_ERR_INVALID;
+    const size_t es = 2;  // bf16
+    const size_t q_step = (size_t)cache->B * cache->H * cache->d * es;
+    const size_t kv_step = (size_t)cache->B * cache->H_kv * cache->d * es;
+    const char* qc = static_cast<const char*>(q);
+    const char* kc = static_cast<const char*>(k);
+    const char* vc = static_cast<const char*>(v);
+    char* oc = static_cast<char*>(o);
+    for (int t = 0; t < T; ++t) {
+        st = eva_rcache_append(cache, kc + t * kv_step, vc + t * kv_step, active, stream);
+        if (st != EVA_OK) return st;
+        st = eva_rdecode_step(cache, qc + t * q_step, oc + t * q_step, active, ws, ws_bytes, stream);
+        if (st != EVA_OK) return st;
+    }
+    return EVA_OK;
 }
 
 }  // extern "C"

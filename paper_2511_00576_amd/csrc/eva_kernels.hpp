@@ -56,17 +56,34 @@ struct CacheView {
     void* vt_sum;
 };
 
+// Per-sequence state of a ragged cache, all in device memory.
+struct RaggedState {
+    int* n_tok;         // [B] tokens held by each sequence
+    int* arrive;        // [B] arrival counters of the append kernel (zero between launches)
+    const int* active;  // [B] nonzero = the sequence takes part in this step; nullptr = all
+    int max_tok;        // most tokens a sequence may hold
+};
+
 // Copy the last min(L, R) positions of K/V into the ring and the L / C
-// summaries (row-major Ks/Vs) into the cache arrays.
+// summaries (row-major Ks/Vs) into the cache arrays.  With `lens` (device
+// [B], ragged caches) sequence b uses its own length min(lens[b], L,
+// r.max_tok) instead of L and the kernel also sets r.n_tok / r.arrive.
 template <int D, typename T>
 hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,
-                             int L, hipStream_t stream);
+                             int L, const int* lens, const RaggedState& r, hipStream_t stream);
 
 // Build summary `s_new` from ring rows (when s_new >= 0), then write the token
 // at position p = c.n_tok.
 template <int D, typename T>
 hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int s_new,
                                hipStream_t stream);
+
+// Ragged append: every (b, kv head) workgroup reads p = r.n_tok[b] itself,
+// builds the summary that becomes due at p, writes the token, and the last
+// of the sequence's H_kv workgroups advances r.n_tok[b].
+template <int D, typename T>
+hipError_t launch_rcache_append(const CacheView& c, const RaggedState& r, const void* k_new, const void* v_new,
+                                hipStream_t stream);
 
 struct DecodeParams {
     CacheView c;
@@ -84,6 +101,11 @@ struct DecodeParams {
     int G;
     float scale_log2;
     float log2C;
+    // ragged caches: per-sequence counts in device memory (nullptr for a
+    // uniform cache, whose geometry is the host-computed fields above)
+    const int* n_tok;
+    const int* active;
+    int max_tok;
 };
 
 template <int D, typename T>

@@ -176,3 +176,111 @@ def decode_step(cache: Cache, q, use_workspace: bool = True, out=None):
     _lib.check("eva_decode_step",
                _lib.load().eva_decode_step(ctypes.byref(s), _ptr(q), _ptr(o), _ptr(ws), nbytes, _stream()))
     return o
+
+
+class RaggedCache:
+    """Decode cache whose sequences hold different numbers of tokens (see
+    eva_rcache in eva.h).  Same arrays as Cache; the per-sequence token counts
+    `n_tok` [B] (int32) and the library's arrival counters live on the device,
+    so steps need no host-side state.  `max_tokens` bounds every sequence."""
+
+    def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None, fill=None):
+        if R is None:
+            R = -(-(W + C - 1) // 32) * 32
+        S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
+        mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
+            (lambda *s: torch.empty(*s, dtype=dtype, device=device))
+        self.k_ring = mk(B, Hkv, R, d)
+        self.vt_ring = mk(B, Hkv, d, R)
+        self.k_sum = mk(B, Hkv, S_max, d)
+        self.vt_sum = mk(B, Hkv, d, S_max)
+        self.n_tok = torch.zeros(B, dtype=torch.int32, device=device)
+        self.arrive = torch.zeros(B, dtype=torch.int32, device=device)
+        self.dtype = dtype
+        self.struct = _lib.EvaRCacheStruct(B, H, Hkv, d, W, C, _DTYPES[dtype], R, S_max, max_tokens,
+                                           self.n_tok.data_ptr(), self.arrive.data_ptr(),
+                                           self.k_ring.data_ptr(), self.vt_ring.data_ptr(),
+                                           self.k_sum.data_ptr(), self.vt_sum.data_ptr())
+        n = _lib.load().eva_rdecode_workspace_bytes(ctypes.byref(self.struct))
+        self.ws = torch.empty((n + 3) // 4, dtype=torch.float32, device=device) if n else None
+
+    @property
+    def R(self) -> int:
+        return int(self.struct.R)
+
+    @property
+    def S_max(self) -> int:
+        return int(self.struct.S_max)
+
+    def _ws_args(self, use_workspace):
+        if use_workspace and self.ws is not None:
+            return _ptr(self.ws), self.ws.numel() * 4
+        return ctypes.c_void_p(0), 0
+
+
+def _active_ptr(active):
+    if active is None:
+        return ctypes.c_void_p(0)
+    _require_device(active)
+    if active.dtype != torch.int32:
+        raise ValueError("active must be an int32 device tensor [B]")
+    return _ptr(active)
+
+
+def rcache_fill(cache: RaggedCache, K, V, Ks, Vs, lens):
+    """Load a ragged cache from a right-padded prefill: K, V [B, Hkv, L, d] and
+    their summaries; lens (int32 device [B]) are the valid lengths."""
+    _require_device(K, V, lens)
+    s = cache.struct
+    B, Hkv, L, d = K.shape
+    if (B, Hkv, d) != (s.B, s.H_kv, s.d) or K.dtype != cache.dtype or V.shape != K.shape:
+        raise ValueError("K, V must be [B, Hkv, L, d] matching the cache")
+    if lens.dtype != torch.int32 or tuple(lens.shape) != (B,):
+        raise ValueError("lens must be an int32 device tensor [B]")
+    _lib.check("eva_rcache_fill",
+               _lib.load().eva_rcache_fill(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), L, _ptr(lens),
+                                           _stream()))
+
+
+def rcache_append(cache: RaggedCache, k_new, v_new, active=None):
+    """Append one token to each active sequence: k_new, v_new [B, Hkv, d]."""
+    _require_device(k_new, v_new)
+    s = cache.struct
+    if tuple(k_new.shape) != (s.B, s.H_kv, s.d) or v_new.shape != k_new.shape or k_new.dtype != cache.dtype:
+        raise ValueError("k_new, v_new must be [B, Hkv, d] in the cache dtype")
+    _lib.check("eva_rcache_append",
+               _lib.load().eva_rcache_append(ctypes.byref(s), _ptr(k_new), _ptr(v_new), _active_ptr(active),
+                                             _stream()))
+
+
+def rdecode_step(cache: RaggedCache, q, active=None, out=None, use_workspace=True):
+    """Output of each active sequence's last appended position: q [B, H, d].
+    Rows of inactive or empty sequences keep the contents of `out`."""
+    _require_device(q)
+    s = cache.struct
+    if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
+        raise ValueError("q must be [B, H, d] in the cache dtype")
+    o = torch.zeros_like(q) if out is None else out
+    ws, nbytes = cache._ws_args(use_workspace)
+    _lib.check("eva_rdecode_step",
+               _lib.load().eva_rdecode_step(ctypes.byref(s), _ptr(q), _ptr(o), _active_ptr(active), ws, nbytes,
+                                            _stream()))
+    return o
+
+
+def generate(cache: RaggedCache, q, k, v, active=None, out=None, use_workspace=True):
+    """T generation steps: q [T, B, H, d], k, v [T, B, Hkv, d] -> o [T, B, H, d]
+    (token t of every active sequence appended, then decoded)."""
+    _require_device(q, k, v)
+    s = cache.struct
+    T = q.shape[0]
+    if tuple(q.shape) != (T, s.B, s.H, s.d) or tuple(k.shape) != (T, s.B, s.H_kv, s.d) or v.shape != k.shape:
+        raise ValueError("q [T, B, H, d], k and v [T, B, Hkv, d] expected")
+    if q.dtype != cache.dtype or k.dtype != cache.dtype or v.dtype != cache.dtype:
+        raise ValueError("q, k, v must be in the cache dtype")
+    o = torch.zeros_like(q) if out is None else out
+    ws, nbytes = cache._ws_args(use_workspace)
+    _lib.check("eva_generate",
+               _lib.load().eva_generate(ctypes.byref(s), _ptr(q), _ptr(k), _ptr(v), _ptr(o), T, _active_ptr(active),
+                                        ws, nbytes, _stream()))
+    return o

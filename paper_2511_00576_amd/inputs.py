@@ -54,6 +54,35 @@ DECODE_BF16 = DecodeWorkload("decode-bf16 B64 H32/8 d128 ctx8192 W512 C128", 64,
                              torch.bfloat16, 4)
 
 
+@dataclass(frozen=True)
+class GenerateWorkload:
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    d: int
+    W: int
+    C: int
+    prompt_min: int  # prompt lengths are uniform in [prompt_min, prompt_max]
+    prompt_max: int
+    steps: int       # tokens generated per sequence
+    dtype: torch.dtype
+    seed: int
+
+
+# Batched generation after a prompt: 32 sequences with prompts of 1024 to
+# 3072 tokens (mean 2048), 1024 tokens generated each, the method's main
+# window / chunk setting (W = 256, C = 16).
+GENERATE_BF16 = GenerateWorkload("generate-bf16 B32 H32/8 d128 W256 C16 prompt1024-3072 gen1024", 32, 32, 8, 128,
+                                 256, 16, 1024, 3072, 1024, torch.bfloat16, 6)
+
+
+def prompt_lengths(w: GenerateWorkload) -> list:
+    """Seeded ragged prompt lengths of a generation workload."""
+    g = torch.Generator().manual_seed(w.seed + 500)
+    return torch.randint(w.prompt_min, w.prompt_max + 1, (w.B,), generator=g).tolist()
+
+
 def normal(shape, seed: int, dtype=torch.float32, generator=None) -> torch.Tensor:
     g = generator if generator is not None else torch.Generator().manual_seed(seed)
     return torch.randn(*shape, generator=g, dtype=torch.float32).to(dtype)

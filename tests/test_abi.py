@@ -130,3 +130,58 @@ def test_summaries_rejects(lib):
     assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 64, 32, 4, 0, None) == _lib.EVA_ERR_UNSUPPORTED
     # fewer tokens than one chunk: nothing to do, no pointer needed
     assert f(None, None, None, None, 1, 1, 3, 64, 4, 0, None) == _lib.EVA_OK
+
+
+def make_rcache(**kw):
+    a = dict(B=2, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, R=32, S_max=32, max_tok=100,
+             n_tok=0x50000, arrive=0x60000, k_ring=0x10000, vt_ring=0x20000, k_sum=0x30000, vt_sum=0x40000)
+    a.update(kw)
+    return _lib.EvaRCacheStruct(a["B"], a["H"], a["H_kv"], a["d"], a["W"], a["C"], a["dtype"], a["R"], a["S_max"],
+                                a["max_tok"], a["n_tok"], a["arrive"], a["k_ring"], a["vt_ring"], a["k_sum"],
+                                a["vt_sum"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_tok=0), _lib.EVA_ERR_INVALID),        # per-sequence counts are required
+    (dict(arrive=0), _lib.EVA_ERR_INVALID),
+    (dict(max_tok=0), _lib.EVA_ERR_INVALID),
+    (dict(R=48), _lib.EVA_ERR_INVALID),
+    (dict(W=30, C=4), _lib.EVA_ERR_CAPACITY),     # R = 32 < W + C - 1
+    # W = 8, C = 4, max_tok = 8 + 33 * 4: the last position makes summary 33 due
+    (dict(max_tok=8 + 33 * 4), _lib.EVA_ERR_CAPACITY),
+    (dict(H=5), _lib.EVA_ERR_INVALID),
+    (dict(d=96), _lib.EVA_ERR_UNSUPPORTED),
+])
+def test_rcache_validation(lib, kw, code):
+    c = make_rcache(**kw)
+    assert lib.eva_rcache_append(ctypes.byref(c), FAKE, FAKE, None, None) == code
+    assert lib.eva_rdecode_step(ctypes.byref(c), FAKE, FAKE, None, None, 0, None) == code
+    assert lib.eva_rdecode_workspace_bytes(ctypes.byref(c)) == 0
+
+
+def test_rcache_capacity_boundary(lib):
+    # max_tok = 7 + 32 * 4 + 1: the last position p = 135 has s(p) = 32 = S_max
+    c = make_rcache(max_tok=8 + 32 * 4)
+    assert lib.eva_rcache_append(ctypes.byref(c), None, FAKE, None, None) == _lib.EVA_ERR_INVALID
+
+
+def test_rcache_fill_rejects(lib):
+    c = make_rcache()
+    f = lib.eva_rcache_fill
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, 64, None, None) == _lib.EVA_ERR_INVALID  # no lens
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, 0, FAKE, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.byref(c), FAKE, FAKE, None, FAKE, 64, FAKE, None) == _lib.EVA_ERR_INVALID
+    # 33 complete chunks of a sequence that may keep all of them: S_max = 32 is short
+    big = make_rcache(max_tok=4 * 33, W=8 + 4 * 33, R=160)
+    assert f(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, 4 * 33, FAKE, None) == _lib.EVA_ERR_CAPACITY
+
+
+def test_rdecode_and_generate_reject(lib):
+    c = make_rcache(dtype=_lib.EVA_F32)
+    assert lib.eva_rdecode_step(ctypes.byref(c), FAKE, FAKE, None, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    c = make_rcache()
+    g = lib.eva_generate
+    assert g(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, 0, None, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert g(ctypes.byref(c), FAKE, None, FAKE, FAKE, 4, None, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert g(ctypes.byref(c), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE, 4, None, None, 0,
+             None) == _lib.EVA_ERR_INVALID
