@@ -7,6 +7,11 @@ prefill workload (B=8, H=H_kv=32, L=4096, d=128, W=256, C=64, bf16):
 Each part is bracketed by HIP events on the stream the kernels run on.
 value = algorithmic prefill FLOPs per step / step time (TFLOP/s).
 
+The generation workload (32 sequences, prompts of 1024-3072 tokens, H=32,
+H_kv=8, d=128, W=256, C=16) is run for its 1024 generated tokens over 8 layer
+caches (one generation step = append + decode in each layer; 8 layers keep
+the working set above the Infinity Cache), one step captured as a HIP graph.
+
 The decode workload (64 sequences, H=32, H_kv=8, d=128, 8192-token context
 held as a 512-token window plus 60 chunk summaries of 128 tokens) is timed in
 the same run: append + decode per token, over 4 rotating caches so the
@@ -33,6 +38,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 N_CACHES = 4
+N_LAYERS = 8
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill_mfma.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
 DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
@@ -118,6 +124,9 @@ def main():
     ap.add_argument("--decode-eager", action="store_true",
                     help="launch the decode iterations one by one instead of replaying a captured graph "
                          "(for per-dispatch counter runs)")
+    ap.add_argument("--no-generate", action="store_true")
+    ap.add_argument("--gen-layers", type=int, default=N_LAYERS,
+                    help="layer caches a generation step visits (working set beyond the Infinity Cache)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device-to-device copy (counter scaling for profiles)")
     args = ap.parse_args()
@@ -225,6 +234,8 @@ def main():
 
     if not args.no_decode:
         out["decode"] = bench_decode(args, torch, eva, inputs, dev)
+    if not args.no_generate:
+        out["generate"] = bench_generate(args, torch, eva, inputs, dev)
 
     if not args.no_cpu_baseline:
         print("# oracle baseline", file=sys.stderr, flush=True)
@@ -312,6 +323,121 @@ def bench_decode(args, torch, eva, inputs, dev):
         "alg_bytes": nbytes,
         "alg_flops": flops,
         "rotating_caches": N_CACHES,
+        "graph_matches_eager": graph_ok,
+    }
+
+
+def generation_counts(lens, B, H, Hkv, d, W, C, e):
+    """Decode bytes and FLOPs of one step of every sequence at lengths `lens`
+    (tokens held, the decoded query at position len - 1)."""
+    nbytes = 2 * B * H * d * e
+    flops = 0
+    for n in lens:
+        p = n - 1
+        rows = min(W, p + 1) + max(0, p - W + 1) // C
+        nbytes += Hkv * rows * d * 2 * e
+        flops += H * 4 * d * rows
+    return flops, nbytes
+
+
+def bench_generate(args, torch, eva, inputs, dev):
+    """Ragged batched generation: per step, every layer cache appends one token
+    per sequence (building the summaries that fall due) and decodes it."""
+    gw = inputs.GENERATE_BF16
+    B, H, Hkv, d, W, C, T = gw.B, gw.H, gw.Hkv, gw.d, gw.W, gw.C, gw.steps
+    n_layers = args.gen_layers
+    lens = inputs.prompt_lengths(gw)
+    Lp = max(lens)
+    print(f"# generation workload {gw.name}: {n_layers} layer caches, prompts {min(lens)}-{Lp}",
+          file=sys.stderr, flush=True)
+    gen = torch.Generator(device=dev).manual_seed(gw.seed)
+    qh = torch.randn(B, H, Lp, d, generator=gen, device=dev).to(gw.dtype)
+    kh = torch.randn(B, Hkv, Lp, d, generator=gen, device=dev).to(gw.dtype)
+    vh = torch.randn(B, Hkv, Lp, d, generator=gen, device=dev).to(gw.dtype)
+    _, Ks, Vs = eva.prefill(qh, kh, vh, W, C, return_summaries=True)
+    del qh
+    lens_d = torch.tensor(lens, dtype=torch.int32, device=dev)
+    caches = [eva.RaggedCache(B, H, Hkv, d, W, C, max_tokens=Lp + T + 1, dtype=gw.dtype, device=dev)
+              for _ in range(n_layers)]
+
+    def fill_all():
+        for c in caches:
+            eva.rcache_fill(c, kh, vh, Ks, Vs, lens_d)
+
+    qn = torch.randn(B, H, d, generator=gen, device=dev).to(gw.dtype)
+    kn = torch.randn(B, Hkv, d, generator=gen, device=dev).to(gw.dtype)
+    vn = torch.randn(B, Hkv, d, generator=gen, device=dev).to(gw.dtype)
+    outs = [torch.zeros_like(qn) for _ in range(n_layers)]
+
+    def gen_step():
+        for c, o in zip(caches, outs):
+            eva.rcache_append(c, kn, vn)
+            eva.rdecode_step(c, qn, out=o)
+
+    def dec_step():
+        for c, o in zip(caches, outs):
+            eva.rdecode_step(c, qn, out=o)
+
+    # eager reference of the first step
+    fill_all()
+    gen_step()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    stream = torch.cuda.Stream()
+    graphs = {}
+    fill_all()
+    torch.cuda.synchronize()
+    for name, fn in (("step", gen_step), ("decode", dec_step)):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            fn()
+        graphs[name] = g
+    # capture launched nothing: the caches still hold the prompts
+    assert caches[0].n_tok.cpu().tolist() == lens
+    graphs["step"].replay()
+    torch.cuda.synchronize()
+    graph_ok = all(torch.equal(o, r) for o, r in zip(outs, ref))
+
+    # whole generation: T steps from the prompts
+    fill_all()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(T):
+        graphs["step"].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_gen = e0.elapsed_time(e1)
+    final = caches[0].n_tok.cpu().tolist()
+    assert final == [n + T for n in lens], "generation did not advance every sequence"
+    # decode kernel alone at the final lengths
+    reps = 64
+    graphs["decode"].replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        graphs["decode"].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us_dec = e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
+    flops, nbytes = generation_counts(final, B, H, Hkv, d, W, C, 2)
+    dec_gbs = nbytes / (us_dec * 1e-6) / 1e9
+    us_layer_step = ms_gen * 1e3 / (T * n_layers)
+    print(f"# generation {us_layer_step:.1f} us per layer-step (append + decode), decode alone {us_dec:.1f} us "
+          f"({dec_gbs:.0f} GB/s) at the final lengths", file=sys.stderr, flush=True)
+    return {
+        "workload": gw.name,
+        "layers": n_layers,
+        "tokens_per_s_per_layer": B / (us_layer_step * 1e-6),
+        "us_per_layer_step": us_layer_step,
+        "generation_ms": ms_gen,
+        "decode_us_final_lengths": us_dec,
+        "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": dec_gbs / PEAK_HBM_GBS,
+                     "kernel": "decode_kernel<128, ragged> (eva_rdecode_step)"},
+        "alg_bytes_decode_final": nbytes,
+        "alg_flops_decode_final": flops,
         "graph_matches_eager": graph_ok,
     }
 

@@ -70,12 +70,14 @@ typedef enum { EVA_BF16 = 0, EVA_F32 = 1 } eva_dtype;
  *
  * The struct is caller-owned host memory; the four arrays are caller-owned
  * device memory of the cache's dtype.  Position p of (b, g) lives in ring slot
- * p mod R.  Values are stored transposed (feature-major) so the decode kernel
- * can feed them to the matrix cores straight from HBM:
- *   k_ring   [B][H_kv][R][d]         keys, row per slot
- *   vt_ring  [B][H_kv][d][R]         values, transposed
- *   k_sum    [B][H_kv][S_max][d]     summary keys
- *   vt_sum   [B][H_kv][d][S_max]     summary values, transposed
+ * p mod R.  Values are stored transposed (feature-major) in tiles of 32 slots
+ * so the decode kernel can feed them to the matrix cores straight from HBM,
+ * each tile's keys and values being two contiguous blocks:
+ *   k_ring   [B][H_kv][R][d]           keys, row per slot
+ *   vt_ring  [B][H_kv][R/32][d][32]    values: slot s, feature f at
+ *                                      [s/32][f][s%32]
+ *   k_sum    [B][H_kv][S_max][d]       summary keys
+ *   vt_sum   [B][H_kv][S_max/32][d][32] summary values, tiled the same way
  * Requirements: R >= W + C - 1 and R a multiple of 32; S_max a multiple of 32.
  * n_tok counts the tokens the cache has absorbed (the same for every
  * sequence of the batch); the library updates it.

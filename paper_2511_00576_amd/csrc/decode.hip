@@ -2,9 +2,10 @@
 // chunk summary that becomes due), and the bandwidth-bound decode step.
 //
 // Cache layout (per (b, kv head)): keys row-major by ring slot [R][D], values
-// transposed [D][R]; summary keys [S_max][D], summary values [D][S_max].
-// Position p lives in slot p mod R; R is a multiple of 32 so a 32-aligned run
-// of positions is a 32-aligned run of slots.
+// transposed per 32-slot tile [R/32][D][32]; summary keys [S_max][D], summary
+// values [S_max/32][D][32].  Position p lives in slot p mod R; R is a
+// multiple of 32 so a 32-aligned run of positions is one tile of slots, and
+// its keys and values are two contiguous 32*D blocks.
 //
 // Decode works on 32-row chunks: summary chunks (rows of the summary arrays)
 // and window chunks (32-aligned position runs of the ring).  Per chunk a wave
@@ -27,8 +28,8 @@ namespace {
 // ---------------------------------------------------------------------------
 // One workgroup moves one 32-row tile: 32 ring positions (32-aligned, so
 // they occupy 32 consecutive slots) or 32 summaries.  Keys are copied row by
-// row; values go through LDS so the transposed store writes 32 consecutive
-// slots (64 B in bf16) per feature row instead of scattered elements.
+// row; values go through LDS so the transposed store writes the tile's
+// contiguous [D][32] block instead of scattered elements.
 // Source arrays have L rows (K, V) and n_chunks rows (Ks, Vs) per (b, g).
 // With `lens` each sequence copies only its own valid prefix: the tiles are
 // counted from that sequence's first ring position, and tiles past its
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
     }
     const int first = max(0, len - c.R);
     const bool ring = (int)blockIdx.x < ring_tiles;
-    int r0, r1, dst0, ld_dst;  // source rows [r0, r1), destination slot/index of r0
+    int r0, r1, dst0;  // source rows [r0, r1), destination slot/index of r0
     const T *src_k, *src_v;
     T *dst_k, *dst_vt;
     if (ring) {
@@ -59,7 +60,6 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
         r0 = max(p0, first);
         r1 = min(p0 + 32, len);
         dst0 = r0 % c.R;
-        ld_dst = c.R;
         src_k = K + bg * (size_t)L * D;
         src_v = V + bg * (size_t)L * D;
         dst_k = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
@@ -68,7 +68,6 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
         r0 = ((int)blockIdx.x - ring_tiles) * 32;
         r1 = min(r0 + 32, len / c.C);
         dst0 = r0;
-        ld_dst = c.S_max;
         src_k = Ks + bg * (size_t)n_chunks * D;
         src_v = Vs + bg * (size_t)n_chunks * D;
         dst_k = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
@@ -83,7 +82,7 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
     __syncthreads();
     for (int e = threadIdx.x; e < rows * D; e += blockDim.x) {
         const int d = e / rows, r = e % rows;
-        dst_vt[(size_t)d * ld_dst + dst0 + r] = tile[r][d];
+        dst_vt[vt_index<D>(d, dst0 + r)] = tile[r][d];
     }
 }
 
@@ -109,7 +108,7 @@ __global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 ks[(size_t)s_new * D + t * 8 + i] = from_f32<T>(kh[i]);
-                vs[(size_t)(t * 8 + i) * c.S_max + s_new] = from_f32<T>(vh[i]);
+                vs[vt_index<D>(t * 8 + i, s_new)] = from_f32<T>(vh[i]);
             }
         }
         __syncthreads();  // every read of the chunk precedes the slot overwrite below
@@ -117,7 +116,7 @@ __global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView
     const int slot = (int)(c.n_tok % c.R);
     for (int d = threadIdx.x; d < D; d += blockDim.x) {
         kr[(size_t)slot * D + d] = k_new[bg * D + d];
-        vr[(size_t)d * c.R + slot] = v_new[bg * D + d];
+        vr[vt_index<D>(d, slot)] = v_new[bg * D + d];
     }
 }
 
@@ -158,7 +157,7 @@ __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheVie
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 ks[(size_t)s_new * D + t * 8 + i] = from_f32<T>(kh[i]);
-                vs[(size_t)(t * 8 + i) * c.S_max + s_new] = from_f32<T>(vh[i]);
+                vs[vt_index<D>(t * 8 + i, s_new)] = from_f32<T>(vh[i]);
             }
         }
         __syncthreads();  // every read of the chunk precedes the slot overwrite below
@@ -166,7 +165,7 @@ __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheVie
     const int slot = p % c.R;
     for (int d = threadIdx.x; d < D; d += blockDim.x) {
         kr[(size_t)slot * D + d] = k_new[bg * D + d];
-        vr[(size_t)d * c.R + slot] = v_new[bg * D + d];
+        vr[vt_index<D>(d, slot)] = v_new[bg * D + d];
     }
     // Every workgroup of sequence b read n_tok[b] before arriving, so the
     // last to arrive may advance it; it also re-arms the counter.
@@ -182,6 +181,7 @@ __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheVie
 // decode step
 // ---------------------------------------------------------------------------
 constexpr int kDecWaves = 4;
+constexpr float kLazyTau = 8.f;  // log2 units: unscaled weights stay <= 256
 
 // Query position and chunk ranges of one decode row.
 struct DecodeGeom {
@@ -226,7 +226,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     const DecodeGeom geo = decode_geom<RAGGED>(a, b, valid);
     if (!valid) return;  // uniform across the workgroup
     const size_t bg = (size_t)b * c.Hkv + kvh;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // keeps chunk bookkeeping scalar
     const int g = lane >> 4, c16 = lane & 15;
     const int h0 = kvh * a.G + hg * 16;
     const int ncols = min(16, a.G - hg * 16);
@@ -236,64 +237,68 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     const T* ksum = static_cast<const T*>(c.k_sum) + bg * (size_t)c.S_max * D;
     const T* vsum = static_cast<const T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
 
-    // query fragments: column c16 = head h0 + c16, features dc*32 + 8g .. +7
+    // query fragments: column c16 = head h0 + c16, features dc*32 + 8g .. +7.
+    // Columns past ncols repeat the last head: every column's scores,
+    // weights and outputs depend on that column alone, and those outputs are
+    // never stored.
     bf16x8 qf[NDC];
     {
         const T* qrow = static_cast<const T*>(a.q) + ((size_t)b * c.H + h0 + min(c16, ncols - 1)) * D;
 #pragma unroll
-        for (int dc = 0; dc < NDC; ++dc) {
-            qf[dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
-            if (c16 >= ncols) qf[dc] = bf16x8{};
-        }
+        for (int dc = 0; dc < NDC; ++dc) qf[dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
     }
 
     floatx4 acc[NDB];
 #pragma unroll
     for (int db = 0; db < NDB; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // Running reference max (log2 units, per column) and row sum.  The
+    // reference moves only when a chunk's max exceeds it by more than
+    // kLazyTau, so most chunks add exp2(s - m_run) <= 2^kLazyTau without
+    // rescaling the accumulators; the final division by l_run is exact for
+    // any reference.
     float m_run = -INFINITY, l_run = 0.f;
 
     const int n_chunks = geo.n_sum_chunks + geo.n_win_chunks;
     const int worker = split * kDecWaves + wave;
     const int n_workers = a.splits * kDecWaves;
-    // key row of the A operand for S^T block kb (row c16 of the 16-row block):
-    // keys of lane group g' = c16/4 land on 8 consecutive keys 8g'..8g'+7
-    const int krow0 = (c16 >> 2) * 8 + (c16 & 3);
+    // Per-lane element offsets inside a 32-row tile.  A operand of S^T = K Q^T
+    // for key block kb: row c16 of the block is key krow0 + 4kb, so the keys
+    // of lane group g' = c16/4 land on 8 consecutive keys 8g'..8g'+7.
+    // A operand of O^T += V^T P^T: feature db*16 + c16, keys 8g .. 8g+7.
+    const int koff = ((c16 >> 2) * 8 + (c16 & 3)) * D + g * 8;
+    const int voff = c16 * 32 + g * 8;
 
     for (int ch = worker; ch < n_chunks; ch += n_workers) {
         const bool is_sum = ch < geo.n_sum_chunks;
-        const T* kbase;
-        const T* vbase;  // element (d, key) at vbase + d * vstride + key
-        int vstride, key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
+        const T* kt;  // the chunk's key tile [32][D]
+        const T* vt;  // the chunk's value tile [D][32]
+        int key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
         if (is_sum) {
             const int r0 = ch * 32;
-            kbase = ksum + (size_t)r0 * D;
-            vbase = vsum + r0;
-            vstride = c.S_max;
+            kt = ksum + (size_t)r0 * D;
+            vt = vsum + (size_t)r0 * D;
             key_lo = 0;
             key_hi = min(31, geo.n_sum - 1 - r0);
         } else {
             const int pos0 = (geo.first_win_chunk + ch - geo.n_sum_chunks) * 32;
             const int slot0 = pos0 % c.R;
-            kbase = kring + (size_t)slot0 * D;
-            vbase = vring + slot0;
-            vstride = c.R;
+            kt = kring + (size_t)slot0 * D;
+            vt = vring + (size_t)slot0 * D;
             key_lo = max(0, geo.win_lo - pos0);
             key_hi = min(31, geo.p - pos0);
         }
         const bool full = key_lo == 0 && key_hi == 31;
 
-        // all 16-B fragment loads of the chunk first: 2*NDC key + NDB value
+        // all 16-B fragment loads of the chunk before any wait: 2*NDC key + NDB value
         bf16x8 ka[2][NDC], va[NDB];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const T* krow = kbase + (size_t)(krow0 + kb * 4) * D + g * 8;
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = *reinterpret_cast<const bf16x8*>(krow + dc * 32);
-        }
-        // A operand of O^T += V^T P^T, lane (g, c16): feature db*16+c16, keys 8g..8g+7
+            for (int dc = 0; dc < NDC; ++dc)
+                ka[kb][dc] = *reinterpret_cast<const bf16x8*>(kt + koff + kb * 4 * D + dc * 32);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-            va[db] = *reinterpret_cast<const bf16x8*>(vbase + (size_t)(db * 16 + c16) * vstride + g * 8);
+        for (int db = 0; db < NDB; ++db) va[db] = *reinterpret_cast<const bf16x8*>(vt + voff + db * 16 * 32);
+        __builtin_amdgcn_sched_barrier(0);
 
         // S^T = K Q^T over the chunk: s[kb] rows = keys 8g + 4kb + i
         floatx4 s[2];
@@ -314,26 +319,35 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
                     s[kb][i] = rel <= span ? s[kb][i] : -INFINITY;
                 }
             // stale ring slots may hold any bit pattern: zero their values
+            // (keys 8g + 2i and 8g + 2i + 1 share dword i of every fragment)
+            uint32_t keep[4];
 #pragma unroll
-            for (int db = 0; db < NDB; ++db)
+            for (int i = 0; i < 4; ++i) {
+                const unsigned rel = (unsigned)(g * 8 + 2 * i - key_lo);
+                keep[i] = (rel <= span ? 0x0000ffffu : 0u) | (rel + 1 <= span ? 0xffff0000u : 0u);
+            }
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const unsigned rel = (unsigned)(g * 8 + j - key_lo);
-                    va[db][j] = rel <= span ? va[db][j] : (bf16)0.f;
-                }
+            for (int db = 0; db < NDB; ++db) {
+                u32x4 w = __builtin_bit_cast(u32x4, va[db]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[i] &= keep[i];
+                va[db] = __builtin_bit_cast(bf16x8, w);
+            }
         }
         const float bias = is_sum ? a.log2C : 0.f;
         float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
                          fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-        mx = xgroup_max(mx) * a.scale_log2 + bias;
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = fast_exp2(m_run - m_use);  // m_run = -inf -> 0
-        l_run *= alpha;
+        mx = xgroup_max(mx) * a.scale_log2 + bias;  // finite: every chunk has a valid key
+        const bool raise = mx > m_run + kLazyTau;
+        if (__builtin_amdgcn_ballot_w64(raise)) {
+            const float m_new = raise ? mx : m_run;
+            const float alpha = fast_exp2(m_run - m_new);  // first chunk: exp2(-inf) = 0
+            l_run *= alpha;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
-        m_run = m_new;
-        const float off = bias - m_use;
+            for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+            m_run = m_new;
+        }
+        const float off = bias - m_run;
         bf16x8 pf;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)

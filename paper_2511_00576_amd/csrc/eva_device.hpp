@@ -90,6 +90,15 @@ __device__ __forceinline__ shortx4 lds_read_tr16(const bf16* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(p));
 }
 
+// Transposed value arrays of the decode cache are tiled by 32 rows: row
+// (slot or summary index) r, feature f lives at element
+//   (r / 32) * 32 * D + f * 32 + r % 32,
+// so the 32 rows of a tile form one contiguous [D][32] block.
+template <int D>
+__host__ __device__ __forceinline__ size_t vt_index(int f, int r) {
+    return (size_t)(r >> 5) * (32 * D) + (size_t)f * 32 + (r & 31);
+}
+
 __device__ __forceinline__ int visible_summaries(int n, int W, int C) {
     int start = n - W + 1;
     return start > 0 ? start / C : 0;

@@ -49,11 +49,12 @@ struct RowMajorChunk {
 };
 
 // Cache ring source: row r of the chunk is position pos0 + r, stored in slot
-// (pos0 + r) mod R; keys row-major [R][D], values transposed [D][R].
+// (pos0 + r) mod R; keys row-major [R][D], values transposed per 32-slot tile
+// [R/32][D][32] (vt_index).
 template <int D, typename T>
 struct RingChunk {
     const T* k_ring;   // this (b, g): [R][D]
-    const T* vt_ring;  // this (b, g): [D][R]
+    const T* vt_ring;  // this (b, g): [R/32][D][32]
     long long pos0;
     int R;
     __device__ int slot(int r) const { return (int)((pos0 + r) % R); }
@@ -65,7 +66,7 @@ struct RingChunk {
     __device__ void load_v(int r, int cc, float out[8]) const {
         int s = slot(r);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) out[i] = to_f32(vt_ring[(size_t)(cc * 8 + i) * R + s]);
+        for (int i = 0; i < 8; ++i) out[i] = to_f32(vt_ring[vt_index<D>(cc * 8 + i, s)]);
     }
 };
 

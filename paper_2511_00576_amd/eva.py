@@ -58,8 +58,9 @@ def build_summaries(K: torch.Tensor, V: torch.Tensor, C: int, out=None):
 class Cache:
     """Window + summary decode cache in device memory (see eva_cache in eva.h).
 
-    k_ring [B, Hkv, R, d], vt_ring [B, Hkv, d, R] (values transposed),
-    k_sum [B, Hkv, S_max, d], vt_sum [B, Hkv, d, S_max].  The ring holds the
+    k_ring [B, Hkv, R, d], vt_ring [B, Hkv, R // 32, d, 32] (values transposed
+    per 32-slot tile), k_sum [B, Hkv, S_max, d], vt_sum [B, Hkv, S_max // 32, d, 32].
+    The ring holds the
     last R positions (R >= W + C - 1, a multiple of 32); S_max bounds the number
     of chunk summaries, i.e. the tokens the cache can ever absorb.
     """
@@ -72,9 +73,9 @@ class Cache:
         mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
             (lambda *s: torch.empty(*s, dtype=dtype, device=device))
         self.k_ring = mk(B, Hkv, R, d)
-        self.vt_ring = mk(B, Hkv, d, R)
+        self.vt_ring = mk(B, Hkv, R // 32, d, 32)
         self.k_sum = mk(B, Hkv, S_max, d)
-        self.vt_sum = mk(B, Hkv, d, S_max)
+        self.vt_sum = mk(B, Hkv, S_max // 32, d, 32)
         self.dtype = dtype
         self.struct = _lib.EvaCacheStruct(B, H, Hkv, d, W, C, _DTYPES[dtype], R, S_max, 0,
                                           self.k_ring.data_ptr(), self.vt_ring.data_ptr(),
@@ -191,9 +192,9 @@ class RaggedCache:
         mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
             (lambda *s: torch.empty(*s, dtype=dtype, device=device))
         self.k_ring = mk(B, Hkv, R, d)
-        self.vt_ring = mk(B, Hkv, d, R)
+        self.vt_ring = mk(B, Hkv, R // 32, d, 32)
         self.k_sum = mk(B, Hkv, S_max, d)
-        self.vt_sum = mk(B, Hkv, d, S_max)
+        self.vt_sum = mk(B, Hkv, S_max // 32, d, 32)
         self.n_tok = torch.zeros(B, dtype=torch.int32, device=device)
         self.arrive = torch.zeros(B, dtype=torch.int32, device=device)
         self.dtype = dtype
