@@ -41,7 +41,8 @@ N_CACHES = 4
 N_LAYERS = 8
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill_mfma.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
-DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
+DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp",
+                  "paper_2511_00576_amd/build.py")
 
 
 def attended(L, W, C):
@@ -127,6 +128,8 @@ def main():
     ap.add_argument("--no-generate", action="store_true")
     ap.add_argument("--gen-layers", type=int, default=N_LAYERS,
                     help="layer caches a generation step visits (working set beyond the Infinity Cache)")
+    ap.add_argument("--gen-steps", type=int, default=None,
+                    help="generated tokens per sequence (default: the workload's 1024)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device-to-device copy (counter scaling for profiles)")
     args = ap.parse_args()
@@ -266,8 +269,7 @@ def bench_decode(args, torch, eva, inputs, dev):
 
     def token(c):
         c.struct.n_tok = ctx  # re-append position ctx: same work every iteration
-        eva.cache_append(c, kn, vn)
-        eva.decode_step(c, qn, out=od)
+        eva.append_decode(c, qn, kn, vn, out=od)
 
     def decode_only(c):
         eva.decode_step(c, qn, out=od)
@@ -314,7 +316,7 @@ def bench_decode(args, torch, eva, inputs, dev):
     return {
         "workload": dw.name,
         "tokens_per_s": B / (res["token"] * 1e-3),
-        "us_per_token_step": res["token"] * 1e3,
+        "us_per_token_step": res["token"] * 1e3,  # fused append + decode (eva_append_decode)
         "decode_us": res["decode"] * 1e3,
         "hbm_gbs": dec_gbs,
         "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -344,7 +346,8 @@ def bench_generate(args, torch, eva, inputs, dev):
     """Ragged batched generation: per step, every layer cache appends one token
     per sequence (building the summaries that fall due) and decodes it."""
     gw = inputs.GENERATE_BF16
-    B, H, Hkv, d, W, C, T = gw.B, gw.H, gw.Hkv, gw.d, gw.W, gw.C, gw.steps
+    B, H, Hkv, d, W, C = gw.B, gw.H, gw.Hkv, gw.d, gw.W, gw.C
+    T = gw.steps if args.gen_steps is None else args.gen_steps
     n_layers = args.gen_layers
     lens = inputs.prompt_lengths(gw)
     Lp = max(lens)
@@ -371,8 +374,7 @@ def bench_generate(args, torch, eva, inputs, dev):
 
     def gen_step():
         for c, o in zip(caches, outs):
-            eva.rcache_append(c, kn, vn)
-            eva.rdecode_step(c, qn, out=o)
+            eva.rappend_decode(c, qn, kn, vn, out=o)
 
     def dec_step():
         for c, o in zip(caches, outs):
@@ -383,6 +385,13 @@ def bench_generate(args, torch, eva, inputs, dev):
     gen_step()
     torch.cuda.synchronize()
     ref = [o.clone() for o in outs]
+    if args.decode_eager:
+        # per-dispatch counter runs: T eager steps, no graphs
+        fill_all()
+        for _ in range(T):
+            gen_step()
+        torch.cuda.synchronize()
+        return {"workload": gw.name, "eager_steps": T, "graph_matches_eager": None}
     stream = torch.cuda.Stream()
     graphs = {}
     fill_all()
@@ -424,7 +433,7 @@ def bench_generate(args, torch, eva, inputs, dev):
     flops, nbytes = generation_counts(final, B, H, Hkv, d, W, C, 2)
     dec_gbs = nbytes / (us_dec * 1e-6) / 1e9
     us_layer_step = ms_gen * 1e3 / (T * n_layers)
-    print(f"# generation {us_layer_step:.1f} us per layer-step (append + decode), decode alone {us_dec:.1f} us "
+    print(f"# generation {us_layer_step:.1f} us per layer-step (fused append + decode), decode alone {us_dec:.1f} us "
           f"({dec_gbs:.0f} GB/s) at the final lengths", file=sys.stderr, flush=True)
     return {
         "workload": gw.name,

@@ -145,11 +145,13 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
 
 /*
  * Append one token per sequence: k_new, v_new [B][H_kv][d].  The token takes
- * position p = cache->n_tok.  If that position makes chunk S = s(p) - 1 newly
- * visible (s(p) > s(p - 1)), its summary is built from the ring first, then
- * the token is written to slot p mod R, then n_tok becomes p + 1.
- * Errors: INVALID (null pointers, malformed cache), CAPACITY (a summary
- * index >= S_max would be needed).
+ * position p = cache->n_tok.  If it is the last token of chunk
+ * S = (p + 1) / C - 1 (p + 1 a multiple of C), that chunk's summary is built
+ * from the chunk's other C - 1 rows in the ring and the token itself; the
+ * token is written to slot p mod R and n_tok becomes p + 1.  (A chunk is
+ * complete W steps before any query sees it, so building it at completion
+ * keeps it off the path of the decode steps in between.)
+ * Errors: INVALID (null pointers, malformed cache), CAPACITY (S >= S_max).
  */
 int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, void* stream);
 
@@ -167,7 +169,18 @@ int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, voi
 int eva_decode_step(const eva_cache* cache, const void* q, void* o,
                     void* ws, size_t ws_bytes, void* stream);
 
-/* Workspace that lets eva_decode_step split rows across workgroups. */
+/*
+ * Fused per-token step: eva_cache_append(k_new, v_new) followed by
+ * eva_decode_step(q) in one launch, with the same results (the decoded row
+ * reads the new token from k_new, v_new while another workgroup writes it to
+ * the ring; the summary the token completes is built beside the decode).
+ * Errors: as eva_cache_append and eva_decode_step.
+ */
+int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace that lets eva_decode_step / eva_append_decode split rows across
+ * workgroups (sized for the next position, n_tok). */
 size_t eva_decode_workspace_bytes(const eva_cache* cache);
 
 /*
@@ -183,9 +196,9 @@ size_t eva_decode_workspace_bytes(const eva_cache* cache);
  *   arrive   device int32 [B]: the library's per-sequence arrival counters;
  *            the caller zeroes them once, every call leaves them zero
  *   max_tok  host: the most tokens any sequence may hold.  S_max must hold
- *            the summaries of a sequence of max_tok tokens (S_max >=
- *            floor((max_tok - W) / C) when max_tok > W).  A sequence that is
- *            full ignores further appends (its n_tok stays max_tok).
+ *            the summaries of every chunk such a sequence completes
+ *            (S_max >= max_tok / C).  A sequence that is full ignores
+ *            further appends (its n_tok stays max_tok).
  * Sequence b's position p lives in ring slot p mod R of row (b, kv head),
  * exactly as in eva_cache.  Requirements on R and S_max as for eva_cache.
  */
@@ -219,9 +232,9 @@ int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const
 
 /*
  * Append one token to every active sequence: k_new, v_new [B][H_kv][d].
- * Sequence b's token takes position p = n_tok[b]; if p makes chunk
- * s(p) - 1 newly visible, that summary is first built from the ring (as in
- * eva_cache_append), then the token is written and n_tok[b] becomes p + 1.
+ * Sequence b's token takes position p = n_tok[b]; if it completes a chunk,
+ * that chunk's summary is built (as in eva_cache_append), the token is
+ * written and n_tok[b] becomes p + 1.
  * `active` is device int32 [B] (nonzero = append) or NULL for all; inactive
  * and full sequences are left unchanged.
  * Errors: INVALID (malformed cache, null pointers).
@@ -244,16 +257,28 @@ int eva_rcache_append(const eva_rcache* cache, const void* k_new, const void* v_
 int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
                      size_t ws_bytes, void* stream);
 
-/* Workspace that lets eva_rdecode_step split rows across workgroups. */
+/*
+ * Fused generation step of every active sequence: eva_rcache_append(k_new,
+ * v_new, active) followed by eva_rdecode_step(q, active) in one launch, with
+ * the same results.  A full sequence appends nothing and decodes its last
+ * position, as the two separate calls would.
+ * Errors: as eva_rcache_append and eva_rdecode_step.
+ */
+int eva_rappend_decode(const eva_rcache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                       const int* active, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace that lets eva_rdecode_step / eva_rappend_decode split rows across
+ * workgroups. */
 size_t eva_rdecode_workspace_bytes(const eva_rcache* cache);
 
 /*
  * T generation steps (section "Inference throughput and Memory usage"): for
  * t = 0 .. T-1, append token t of every active sequence and decode it.
  *   q, o  [T][B][H][d];  k, v  [T][B][H_kv][d]
- * Equivalent to T calls of eva_rcache_append(k[t], v[t]) followed by
- * eva_rdecode_step(q[t]) -> o[t]; all launches are enqueued on `stream`
- * before the call returns (the caller may capture them into a graph).
+ * Equivalent to T calls of eva_rappend_decode(q[t], k[t], v[t]) -> o[t]
+ * (one launch per step, two when rows are split over workgroups); all
+ * launches are enqueued on `stream` before the call returns (the caller may
+ * capture them into a graph).
  * Errors: as eva_rcache_append and eva_rdecode_step; INVALID for T < 1.
  */
 int eva_generate(const eva_rcache* cache, const void* q, const void* k, const void* v, void* o, int T,

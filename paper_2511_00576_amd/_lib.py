@@ -26,10 +26,12 @@ SYMBOLS = (
     "eva_cache_append",
     "eva_decode_step",
     "eva_decode_workspace_bytes",
+    "eva_append_decode",
     "eva_rcache_fill",
     "eva_rcache_append",
     "eva_rdecode_step",
     "eva_rdecode_workspace_bytes",
+    "eva_rappend_decode",
     "eva_generate",
     "eva_status_string",
 )
@@ -82,6 +84,8 @@ def load():
     lib.eva_cache_append.argtypes = [cp, vp, vp, vp]
     lib.eva_decode_step.restype = i
     lib.eva_decode_step.argtypes = [cp, vp, vp, vp, sz, vp]
+    lib.eva_append_decode.restype = i
+    lib.eva_append_decode.argtypes = [cp, vp, vp, vp, vp, vp, sz, vp]
     lib.eva_decode_workspace_bytes.restype = sz
     lib.eva_decode_workspace_bytes.argtypes = [cp]
     rp = ctypes.POINTER(EvaRCacheStruct)
@@ -91,6 +95,8 @@ def load():
     lib.eva_rcache_append.argtypes = [rp, vp, vp, vp, vp]
     lib.eva_rdecode_step.restype = i
     lib.eva_rdecode_step.argtypes = [rp, vp, vp, vp, vp, sz, vp]
+    lib.eva_rappend_decode.restype = i
+    lib.eva_rappend_decode.argtypes = [rp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.eva_rdecode_workspace_bytes.restype = sz
     lib.eva_rdecode_workspace_bytes.argtypes = [rp]
     lib.eva_generate.restype = i

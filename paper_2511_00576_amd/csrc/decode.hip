@@ -87,18 +87,28 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
 }
 
 // ---------------------------------------------------------------------------
-// append (one workgroup per (b, kv head))
+// append
 // ---------------------------------------------------------------------------
+// A chunk's summary is built in the step that appends the chunk's last token:
+// the chunk becomes visible only W steps later (s(n) counts chunks ending at
+// or before n - W), so the build is never on the path of the decode that
+// runs beside it.  Index of the chunk the token at position p completes, or -1.
+__device__ inline int chunk_completed(int p, int C) { return (p + 1) % C == 0 ? (p + 1) / C - 1 : -1; }
+
+// Append the token at position p of (b, g) = row bg: build the summary of the
+// chunk it completes (from the ring's other C - 1 rows of that chunk and the
+// token itself), then write the token to ring slot p mod R.  The slot holds
+// position p - R, which belongs to neither that chunk (R >= C) nor any decode
+// window (R >= W), so nothing running concurrently reads it.  Called by a
+// whole kSummaryThreads workgroup; smem holds C + summary_red_floats<D>().
 template <int D, typename T>
-__global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView c, const T* __restrict__ k_new,
-                                                                       const T* __restrict__ v_new, int s_new) {
-    extern __shared__ float smem[];
-    const size_t bg = blockIdx.x;
+__device__ void append_token(const CacheView& c, size_t bg, int p, const T* __restrict__ kn,
+                             const T* __restrict__ vn, float* smem) {
     T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
     T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
-    if (s_new >= 0) {
-        // the chunk's rows are still in the ring: positions [s_new*C, s_new*C + C)
-        RingChunk<D, T> src{kr, vr, (long long)s_new * c.C, c.R};
+    const int s_new = chunk_completed(p, c.C);
+    if (s_new >= 0 && s_new < c.S_max) {
+        RingChunkPlusNew<D, T> src{{kr, vr, (long long)s_new * c.C, c.R}, kn, vn, c.C - 1};
         float kh[8], vh[8];
         chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
         const int t = threadIdx.x;
@@ -111,25 +121,25 @@ __global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView
                 vs[vt_index<D>(t * 8 + i, s_new)] = from_f32<T>(vh[i]);
             }
         }
-        __syncthreads();  // every read of the chunk precedes the slot overwrite below
     }
-    const int slot = (int)(c.n_tok % c.R);
+    const int slot = p % c.R;
     for (int d = threadIdx.x; d < D; d += blockDim.x) {
-        kr[(size_t)slot * D + d] = k_new[bg * D + d];
-        vr[vt_index<D>(d, slot)] = v_new[bg * D + d];
+        kr[(size_t)slot * D + d] = kn[d];
+        vr[vt_index<D>(d, slot)] = vn[d];
     }
 }
 
-// ---------------------------------------------------------------------------
-// ragged append (one workgroup per (b, kv head); positions from device memory)
-// ---------------------------------------------------------------------------
-// Index of the chunk summary that becomes visible at position p (the first
-// position whose window starts past the chunk's end), or -1.
-__device__ inline int summary_due(int p, int W, int C) {
-    const int start = p - W + 1;
-    return (start > 0 && start % C == 0) ? start / C - 1 : -1;
+// Uniform cache: one workgroup per (b, kv head), position p from the host.
+template <int D, typename T>
+__global__ __launch_bounds__(kSummaryThreads) void cache_append_kernel(CacheView c, const T* __restrict__ k_new,
+                                                                       const T* __restrict__ v_new, int p) {
+    extern __shared__ float smem[];
+    const size_t bg = blockIdx.x;
+    append_token<D, T>(c, bg, p, k_new + bg * D, v_new + bg * D, smem);
 }
 
+// Ragged cache: one workgroup per (b, kv head), position p = n_tok[b] read on
+// the device; the last of the sequence's H_kv workgroups advances n_tok[b].
 template <int D, typename T>
 __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheView c, RaggedState rs,
                                                                         const T* __restrict__ k_new,
@@ -143,30 +153,7 @@ __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheVie
     __syncthreads();
     const int p = sh_p;
     if (p >= rs.max_tok) return;  // full: every workgroup of the sequence agrees
-    T* kr = static_cast<T*>(c.k_ring) + bg * (size_t)c.R * D;
-    T* vr = static_cast<T*>(c.vt_ring) + bg * (size_t)c.R * D;
-    const int s_new = summary_due(p, c.W, c.C);
-    if (s_new >= 0 && s_new < c.S_max) {
-        RingChunk<D, T> src{kr, vr, (long long)s_new * c.C, c.R};
-        float kh[8], vh[8];
-        chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
-        const int t = threadIdx.x;
-        if (t < D / 8) {
-            T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;
-            T* vs = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                ks[(size_t)s_new * D + t * 8 + i] = from_f32<T>(kh[i]);
-                vs[vt_index<D>(t * 8 + i, s_new)] = from_f32<T>(vh[i]);
-            }
-        }
-        __syncthreads();  // every read of the chunk precedes the slot overwrite below
-    }
-    const int slot = p % c.R;
-    for (int d = threadIdx.x; d < D; d += blockDim.x) {
-        kr[(size_t)slot * D + d] = k_new[bg * D + d];
-        vr[vt_index<D>(d, slot)] = v_new[bg * D + d];
-    }
+    append_token<D, T>(c, bg, p, k_new + bg * D, v_new + bg * D, smem);
     // Every workgroup of sequence b read n_tok[b] before arriving, so the
     // last to arrive may advance it; it also re-arms the counter.
     if (threadIdx.x == 0) {
@@ -183,22 +170,27 @@ __global__ __launch_bounds__(kSummaryThreads) void rcache_append_kernel(CacheVie
 constexpr int kDecWaves = 4;
 constexpr float kLazyTau = 8.f;  // log2 units: unscaled weights stay <= 256
 
-// Query position and chunk ranges of one decode row.
+// Query position and chunk ranges of one decode row.  fresh: the row's own
+// token is being appended in the same launch and is read from the inputs.
 struct DecodeGeom {
     int p, n_sum, win_lo, n_sum_chunks, n_win_chunks, first_win_chunk;
+    bool fresh;
 };
 
 // Geometry of sequence b: from the host-computed fields (uniform cache) or
-// from the sequence's own token count (ragged cache).  valid = false when
-// the sequence takes no part in this step or holds no token.
-template <bool RAGGED>
+// from the sequence's own token count n (ragged cache).  A plain decode
+// serves position n - 1; a fused append + decode appends position n (unless
+// the sequence is full) and serves it.  valid = false when the sequence takes
+// no part in this step or has no token to serve.
+template <bool RAGGED, bool APPEND>
 __device__ inline DecodeGeom decode_geom(const DecodeParams& a, int b, bool& valid) {
-    DecodeGeom g{a.p, a.n_sum, a.win_lo, a.n_sum_chunks, a.n_win_chunks, a.first_win_chunk};
+    DecodeGeom g{a.p, a.n_sum, a.win_lo, a.n_sum_chunks, a.n_win_chunks, a.first_win_chunk, APPEND};
     valid = true;
     if constexpr (RAGGED) {
         const int n = min(a.n_tok[b], a.max_tok);
-        valid = n > 0 && !(a.active && a.active[b] == 0);
-        g.p = n - 1;
+        g.fresh = APPEND && n < a.max_tok;
+        g.p = g.fresh ? n : n - 1;
+        valid = g.p >= 0 && !(a.active && a.active[b] == 0);
         g.win_lo = max(0, g.p - a.c.W + 1);
         g.n_sum = min(g.win_lo / a.c.C, a.c.S_max);  // s(p)
         g.n_sum_chunks = (g.n_sum + 31) / 32;
@@ -208,7 +200,28 @@ __device__ inline DecodeGeom decode_geom(const DecodeParams& a, int b, bool& val
     return g;
 }
 
-template <int D, bool RAGGED>
+// Ragged fused step: every workgroup of sequence b arrives once after its
+// last use of n_tok[b]; the last one re-arms the counter and advances the
+// count when a token was appended.
+template <bool RAGGED, bool APPEND>
+__device__ inline void arrive_and_advance(const DecodeParams& a, int b, const DecodeGeom& geo) {
+    if constexpr (RAGGED && APPEND) {
+        if (threadIdx.x == 0) {
+            if (atomicAdd(&a.arrive[b], 1) == a.arrivals - 1) {
+                a.arrive[b] = 0;
+                if (geo.fresh) a.n_tok[b] = geo.p + 1;
+            }
+        }
+    }
+}
+
+// Decode grid: x = split, y = kv head * head group, z = sequence.  With
+// APPEND the z range is doubled: z >= B are the appending workgroups, one
+// per (sequence, kv head) at x = 0 and head group 0 (the rest exit at once).
+// They come last in dispatch order, so they take the slots the decode
+// workgroups leave free instead of pushing decode workgroups into a second
+// round.
+template <int D, bool RAGGED, bool APPEND>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     typedef bf16 T;
     constexpr int NDC = D / 32;  // 32-feature contraction steps
@@ -220,11 +233,23 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     const int split = blockIdx.x;
     const int kvh = blockIdx.y / a.n_hg;
     const int hg = blockIdx.y % a.n_hg;
-    const int b = blockIdx.z;
     const CacheView& c = a.c;
+    const bool appender = APPEND && (int)blockIdx.z >= c.B;
+    const int b = appender ? (int)blockIdx.z - c.B : (int)blockIdx.z;
+    if (appender && (split != 0 || hg != 0)) return;  // idle: reads nothing, does not arrive
     bool valid;
-    const DecodeGeom geo = decode_geom<RAGGED>(a, b, valid);
+    const DecodeGeom geo = decode_geom<RAGGED, APPEND>(a, b, valid);
     if (!valid) return;  // uniform across the workgroup
+    const T* k_new = static_cast<const T*>(a.k_new) + ((size_t)b * c.Hkv + kvh) * D;
+    const T* v_new = static_cast<const T*>(a.v_new) + ((size_t)b * c.Hkv + kvh) * D;
+    if constexpr (APPEND) {
+        if (appender) {
+            extern __shared__ float smem[];
+            if (geo.fresh) append_token<D, T>(c, (size_t)b * c.Hkv + kvh, geo.p, k_new, v_new, smem);
+            arrive_and_advance<RAGGED, APPEND>(a, b, geo);
+            return;
+        }
+    }
     const size_t bg = (size_t)b * c.Hkv + kvh;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // keeps chunk bookkeeping scalar
@@ -248,6 +273,21 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         for (int dc = 0; dc < NDC; ++dc) qf[dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
     }
 
+    // The appended token (row p) in the fragment layouts below: its key as
+    // the A-operand fragment of the lane that holds row p, its value feature
+    // db*16 + c16 for the lanes whose 8 keys include row p.
+    // (each value half in a 32-bit register of its own: packing pairs would
+    // make the wave wait for these loads before its first chunk)
+    bf16x8 kn[NDC];
+    uint32_t vn[NDB];
+    if (APPEND && geo.fresh) {
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc) kn[dc] = *reinterpret_cast<const bf16x8*>(k_new + dc * 32 + g * 8);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+            vn[db] = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(v_new) + db * 16 + c16);
+    }
+
     floatx4 acc[NDB];
 #pragma unroll
     for (int db = 0; db < NDB; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -265,7 +305,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     // for key block kb: row c16 of the block is key krow0 + 4kb, so the keys
     // of lane group g' = c16/4 land on 8 consecutive keys 8g'..8g'+7.
     // A operand of O^T += V^T P^T: feature db*16 + c16, keys 8g .. 8g+7.
-    const int koff = ((c16 >> 2) * 8 + (c16 & 3)) * D + g * 8;
+    const int krow0 = (c16 >> 2) * 8 + (c16 & 3);
+    const int koff = krow0 * D + g * 8;
     const int voff = c16 * 32 + g * 8;
 
     for (int ch = worker; ch < n_chunks; ch += n_workers) {
@@ -273,6 +314,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         const T* kt;  // the chunk's key tile [32][D]
         const T* vt;  // the chunk's value tile [D][32]
         int key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
+        int chunk_pos0 = 0;  // first position of a window chunk
         if (is_sum) {
             const int r0 = ch * 32;
             kt = ksum + (size_t)r0 * D;
@@ -282,6 +324,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         } else {
             const int pos0 = (geo.first_win_chunk + ch - geo.n_sum_chunks) * 32;
             const int slot0 = pos0 % c.R;
+            chunk_pos0 = pos0;
             kt = kring + (size_t)slot0 * D;
             vt = vring + (size_t)slot0 * D;
             key_lo = max(0, geo.win_lo - pos0);
@@ -299,6 +342,31 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) va[db] = *reinterpret_cast<const bf16x8*>(vt + voff + db * 16 * 32);
         __builtin_amdgcn_sched_barrier(0);
+        if (APPEND && geo.fresh && !is_sum && chunk_pos0 + 32 > geo.p) {
+            // the chunk holding row p: its ring slot is stale, take the input
+            const int kp = geo.p - chunk_pos0;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const bool mine = krow0 + 4 * kb == kp;
+#pragma unroll
+                for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = mine ? kn[dc] : ka[kb][dc];
+            }
+            const uint32_t lo_here = (unsigned)(kp - g * 8) < 8u && (kp & 1) == 0 ? 1u : 0u;
+            const uint32_t hi_here = (unsigned)(kp - g * 8) < 8u && (kp & 1) == 1 ? 1u : 0u;
+            const int word = (kp - g * 8) >> 1;
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) {
+                u32x4 w = __builtin_bit_cast(u32x4, va[db]);
+                uint32_t bits = vn[db];
+                asm volatile("" : "+v"(bits));  // keeps the shift below out of the loop preheader
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (lo_here && word == i) w[i] = (w[i] & 0xffff0000u) | bits;
+                    if (hi_here && word == i) w[i] = (w[i] & 0x0000ffffu) | (bits << 16);
+                }
+                va[db] = __builtin_bit_cast(bf16x8, w);
+            }
+        }
 
         // S^T = K Q^T over the chunk: s[kb] rows = keys 8g + 4kb + i
         floatx4 s[2];
@@ -398,6 +466,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         for (int w = 0; w < kDecWaves; ++w) v += wgt[w] * red_o[w][d][col];
         out[f] = v;
     }
+    arrive_and_advance<RAGGED, APPEND>(a, b, geo);  // thread 0 (column 0) stays to here
     if (col >= ncols) return;
     if (a.splits == 1) {
         const float inv = 1.f / lsum;
@@ -417,6 +486,9 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     }
 }
 
+// Runs after the decode kernel; for a ragged fused step n_tok[b] has been
+// advanced by then, which leaves `valid` (active and serving a token) as the
+// decode kernel saw it.
 template <int D, bool RAGGED>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
     typedef bf16 T;
@@ -425,7 +497,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
     const int b = blockIdx.z;
     const CacheView& c = a.c;
     bool valid;
-    decode_geom<RAGGED>(a, b, valid);
+    decode_geom<RAGGED, false>(a, b, valid);
     if (!valid) return;  // no partials were written for this sequence
     const int ncols = min(16, a.G - hg * 16);
     const float* base = a.ws + (((size_t)b * c.Hkv + kvh) * a.n_hg + hg) * a.splits * 16 * (D + 2);
@@ -469,11 +541,10 @@ hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, c
 }
 
 template <int D, typename T>
-hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int s_new,
-                               hipStream_t stream) {
-    const size_t lds = s_new >= 0 ? (size_t)(c.C + summary_red_floats<D>()) * sizeof(float) : 0;
+hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int p, hipStream_t stream) {
+    const size_t lds = (size_t)(c.C + summary_red_floats<D>()) * sizeof(float);
     hipLaunchKernelGGL((cache_append_kernel<D, T>), dim3(c.B * c.Hkv), dim3(kSummaryThreads), lds, stream, c,
-                       static_cast<const T*>(k_new), static_cast<const T*>(v_new), s_new);
+                       static_cast<const T*>(k_new), static_cast<const T*>(v_new), p);
     return hipGetLastError();
 }
 
@@ -487,10 +558,11 @@ hipError_t launch_rcache_append(const CacheView& c, const RaggedState& r, const 
     return hipGetLastError();
 }
 
-template <int D, bool RAGGED>
+template <int D, bool RAGGED, bool APPEND>
 hipError_t launch_decode_impl(const DecodeParams& p, hipStream_t stream) {
-    dim3 grid(p.splits, p.c.Hkv * p.n_hg, p.c.B);
-    hipLaunchKernelGGL((decode_kernel<D, RAGGED>), grid, dim3(256), 0, stream, p);
+    dim3 grid(p.splits, p.c.Hkv * p.n_hg, p.c.B * (APPEND ? 2 : 1));
+    const size_t lds = APPEND ? (size_t)(p.c.C + summary_red_floats<D>()) * sizeof(float) : 0;
+    hipLaunchKernelGGL((decode_kernel<D, RAGGED, APPEND>), grid, dim3(256), lds, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.splits == 1) return e;
     hipLaunchKernelGGL((decode_combine_kernel<D, RAGGED>), dim3(1, p.c.Hkv * p.n_hg, p.c.B), dim3(256), 0, stream,
@@ -501,7 +573,9 @@ hipError_t launch_decode_impl(const DecodeParams& p, hipStream_t stream) {
 template <int D, typename T>
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
     static_assert(sizeof(T) == 2, "decode runs on bf16 caches");
-    return p.n_tok ? launch_decode_impl<D, true>(p, stream) : launch_decode_impl<D, false>(p, stream);
+    if (p.k_new)
+        return p.n_tok ? launch_decode_impl<D, true, true>(p, stream) : launch_decode_impl<D, false, true>(p, stream);
+    return p.n_tok ? launch_decode_impl<D, true, false>(p, stream) : launch_decode_impl<D, false, false>(p, stream);
 }
 
 #define EVA_FILL(D, T)                                                                                      \

@@ -107,8 +107,8 @@ int check_rcache(const eva_rcache* c) {
     if (c->max_tok < 1) return EVA_ERR_INVALID;
     if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
     if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
-    // the last summary a sequence of max_tok tokens makes due
-    if (visible_summaries(c->max_tok - 1, c->W, c->C) > c->S_max) return EVA_ERR_CAPACITY;
+    // summaries are built as chunks complete: up to max_tok / C of them
+    if (c->max_tok / c->C > c->S_max) return EVA_ERR_CAPACITY;
     if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
     return EVA_OK;
 }
@@ -142,6 +142,10 @@ int rdecode_max_chunks(const eva_rcache* c) {
     const int win = c->W < c->max_tok ? c->W : c->max_tok;
     return (n_sum + 31) / 32 + (win + 30) / 32 + 1;
 }
+
+// Index of the chunk whose last token is position p, or -1: its summary is
+// built by the step that appends p.
+int completed_chunk(long long p, int C) { return (p + 1) % C == 0 ? (int)((p + 1) / C - 1) : -1; }
 
 int decode_chunks(const eva_cache* c, long long p, int* n_sum_out, int* win_lo_out, int* n_sum_chunks,
                   int* n_win_chunks) {
@@ -287,18 +291,12 @@ int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, voi
     if (st != EVA_OK) return st;
     if (!k_new || !v_new) return EVA_ERR_INVALID;
     const long long p = cache->n_tok;
-    if (p >= 0x7fffffffLL) return EVA_ERR_CAPACITY;
-    const int s_prev = p > 0 ? visible_summaries(p - 1, cache->W, cache->C) : 0;
-    const int s_now = visible_summaries(p, cache->W, cache->C);
-    int s_new = -1;
-    if (s_now > s_prev) {
-        s_new = s_now - 1;  // s grows by at most one per token
-        if (s_new >= cache->S_max) return EVA_ERR_CAPACITY;
-    }
+    if (p >= 0x7fffffffLL - 64) return EVA_ERR_CAPACITY;
+    if (completed_chunk(p, cache->C) >= cache->S_max) return EVA_ERR_CAPACITY;
     eva::CacheView v = view_of(cache);
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = dispatch(cache->d, cache->dtype, [&](auto dd, auto t) {
-        return eva::launch_cache_append<decltype(dd)::value, decltype(t)>(v, k_new, v_new, s_new, s);
+        return eva::launch_cache_append<decltype(dd)::value, decltype(t)>(v, k_new, v_new, (int)p, s);
     });
     if (e != hipSuccess) return EVA_ERR_HIP;
     cache->n_tok = p + 1;
@@ -306,30 +304,28 @@ int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, voi
 }
 
 size_t eva_decode_workspace_bytes(const eva_cache* cache) {
-    if (check_cache(cache) != EVA_OK || cache->n_tok < 1) return 0;
+    if (check_cache(cache) != EVA_OK) return 0;
     const int G = cache->H / cache->H_kv;
     const int n_hg = (G + 15) / 16;
     int n_sum, win_lo, nsc, nwc;
-    const int n_chunks = decode_chunks(cache, cache->n_tok - 1, &n_sum, &win_lo, &nsc, &nwc);
+    // the larger of a decode at n_tok - 1 and a fused append + decode at n_tok
+    const int n_chunks = decode_chunks(cache, cache->n_tok, &n_sum, &win_lo, &nsc, &nwc);
     const int units = cache->B * cache->H_kv * n_hg;
     const int splits = decode_splits(units, n_chunks);
     if (splits == 1) return 0;
     return (size_t)units * splits * 16 * (cache->d + 2) * sizeof(float);
 }
 
-int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, size_t ws_bytes, void* stream) {
-    int st = check_cache(cache);
-    if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
-    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
-    if (cache->n_tok < 1) return EVA_ERR_INVALID;
-    if (cache->n_tok - 1 > 0x7fffffffLL - 64) return EVA_ERR_CAPACITY;
-
-    eva::DecodeParams p;
+// Decode (or fused append + decode) of position pos of a uniform cache.
+static int uniform_decode(const eva_cache* cache, long long pos, const void* q, void* o, const void* k_new,
+                          const void* v_new, void* ws, size_t ws_bytes, void* stream) {
+    if (pos > 0x7fffffffLL - 64) return EVA_ERR_CAPACITY;
+    if (cache->B > (k_new ? 32767 : 65535)) return EVA_ERR_UNSUPPORTED;  // grid z: B (x2 when appending)
+    eva::DecodeParams p{};
     p.c = view_of(cache);
     p.q = q;
     p.o = o;
-    p.p = (int)(cache->n_tok - 1);
+    p.p = (int)pos;
     const int n_chunks = decode_chunks(cache, p.p, &p.n_sum, &p.win_lo, &p.n_sum_chunks, &p.n_win_chunks);
     if (p.n_sum > cache->S_max) return EVA_ERR_CAPACITY;
     p.first_win_chunk = p.win_lo / 32;
@@ -342,12 +338,34 @@ int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, si
     p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
     p.log2C = (float)log2((double)cache->C);
-    p.n_tok = nullptr;
-    p.active = nullptr;
-    p.max_tok = 0;
+    p.k_new = k_new;
+    p.v_new = v_new;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
     return hip_status(e);
+}
+
+int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_cache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
+    if (cache->n_tok < 1) return EVA_ERR_INVALID;
+    return uniform_decode(cache, cache->n_tok - 1, q, o, nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o, void* ws,
+                      size_t ws_bytes, void* stream) {
+    int st = check_cache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !k_new || !v_new || !aligned16(q) || !aligned16(k_new)) return EVA_ERR_INVALID;
+    const long long p = cache->n_tok;
+    if (completed_chunk(p, cache->C) >= cache->S_max) return EVA_ERR_CAPACITY;
+    st = uniform_decode(cache, p, q, o, k_new, v_new, ws, ws_bytes, stream);
+    if (st != EVA_OK) return st;
+    cache->n_tok = p + 1;
+    return EVA_OK;
 }
 
 // ---------------------------------------------------------------------------
@@ -394,13 +412,10 @@ size_t eva_rdecode_workspace_bytes(const eva_rcache* cache) {
     return (size_t)units * splits * 16 * (cache->d + 2) * sizeof(float);
 }
 
-int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
-                     size_t ws_bytes, void* stream) {
-    int st = check_rcache(cache);
-    if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
-    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
-
+// Decode (k_new == nullptr) or fused append + decode of every active sequence.
+static int ragged_decode(const eva_rcache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                         const int* active, void* ws, size_t ws_bytes, void* stream) {
+    if (cache->B > (k_new ? 32767 : 65535)) return EVA_ERR_UNSUPPORTED;  // grid z: B (x2 when appending)
     eva::DecodeParams p{};
     p.c = rview_of(cache);
     p.q = q;
@@ -417,9 +432,31 @@ int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int*
     p.n_tok = cache->n_tok;
     p.active = active;
     p.max_tok = cache->max_tok;
+    p.k_new = k_new;
+    p.v_new = v_new;
+    p.arrive = cache->arrive;
+    p.arrivals = p.splits * cache->H_kv * p.n_hg + cache->H_kv;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
     return hip_status(e);
+}
+
+int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
+                     size_t ws_bytes, void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
+    return ragged_decode(cache, q, nullptr, nullptr, o, active, ws, ws_bytes, stream);
+}
+
+int eva_rappend_decode(const eva_rcache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                       const int* active, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_rcache(cache);
+    if (st != EVA_OK) return st;
+    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (!q || !o || !k_new || !v_new || !aligned16(q) || !aligned16(k_new)) return EVA_ERR_INVALID;
+    return ragged_decode(cache, q, k_new, v_new, o, active, ws, ws_bytes, stream);
 }
 
 int eva_generate(const eva_rcache* cache, const void* q, const void* k, const void* v, void* o, int T,
@@ -428,7 +465,7 @@ int eva_generate(const eva_rcache* cache, const void* q, const void* k, const vo
     if (st != EVA_OK) return st;
     if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (T < 1 || !q || !k || !v || !o) return EVA_ERR_INVALID;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return EVA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k)) return EVA_ERR_INVALID;
     const size_t es = 2;  // bf16
     const size_t q_step = (size_t)cache->B * cache->H * cache->d * es;
     const size_t kv_step = (size_t)cache->B * cache->H_kv * cache->d * es;
@@ -437,9 +474,8 @@ int eva_generate(const eva_rcache* cache, const void* q, const void* k, const vo
     const char* vc = static_cast<const char*>(v);
     char* oc = static_cast<char*>(o);
     for (int t = 0; t < T; ++t) {
-        st = eva_rcache_append(cache, kc + t * kv_step, vc + t * kv_step, active, stream);
-        if (st != EVA_OK) return st;
-        st = eva_rdecode_step(cache, qc + t * q_step, oc + t * q_step, active, ws, ws_bytes, stream);
+        st = ragged_decode(cache, qc + t * q_step, kc + t * kv_step, vc + t * kv_step, oc + t * q_step, active, ws,
+                           ws_bytes, stream);
         if (st != EVA_OK) return st;
     }
     return EVA_OK;

@@ -74,9 +74,10 @@ hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, c
 
 // Build summary `s_new` from ring rows (when s_new >= 0), then write the token
 // at position p = c.n_tok.
+// Append the token at position p (uniform cache): builds the summary of the
+// chunk the token completes, then writes the token.
 template <int D, typename T>
-hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int s_new,
-                               hipStream_t stream);
+hipError_t launch_cache_append(const CacheView& c, const void* k_new, const void* v_new, int p, hipStream_t stream);
 
 // Ragged append: every (b, kv head) workgroup reads p = r.n_tok[b] itself,
 // builds the summary that becomes due at p, writes the token, and the last
@@ -103,9 +104,15 @@ struct DecodeParams {
     float log2C;
     // ragged caches: per-sequence counts in device memory (nullptr for a
     // uniform cache, whose geometry is the host-computed fields above)
-    const int* n_tok;
+    int* n_tok;
     const int* active;
     int max_tok;
+    // fused append + decode: the appended token [B][H_kv][d] (nullptr for a
+    // plain decode); ragged caches also count arrivals per sequence
+    const void* k_new;
+    const void* v_new;
+    int* arrive;
+    int arrivals;  // workgroups per sequence that arrive: splits * H_kv * n_hg + H_kv
 };
 
 template <int D, typename T>

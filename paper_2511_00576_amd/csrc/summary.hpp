@@ -70,6 +70,33 @@ struct RingChunk {
     }
 };
 
+// A chunk completed by the token being appended: rows 0 .. C-2 are still in
+// the ring (positions pos0 .. pos0 + C - 2), row C-1 is the new token, read
+// from the caller's [D] input vectors (it is not in the ring yet).
+template <int D, typename T>
+struct RingChunkPlusNew {
+    RingChunk<D, T> ring;
+    const T* k_new;  // this (b, g): [D]
+    const T* v_new;
+    int last;        // C - 1
+    __device__ void load_k(int r, int cc, float out[8]) const {
+        if (r == last) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) out[i] = to_f32(k_new[cc * 8 + i]);
+        } else {
+            ring.load_k(r, cc, out);
+        }
+    }
+    __device__ void load_v(int r, int cc, float out[8]) const {
+        if (r == last) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) out[i] = to_f32(v_new[cc * 8 + i]);
+        } else {
+            ring.load_v(r, cc, out);
+        }
+    }
+};
+
 // Reduce an 8-vector over all threads that share the same feature chunk cc
 // (lanes l, l^TPR, l^2TPR, ... inside the wave, then the waves through LDS).
 // Returns the total in the threads of wave 0 whose row index is 0 (t < TPR),

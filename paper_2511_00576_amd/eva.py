@@ -165,6 +165,23 @@ def cache_append(cache: Cache, k_new, v_new):
                _lib.load().eva_cache_append(ctypes.byref(s), _ptr(k_new), _ptr(v_new), _stream()))
 
 
+def append_decode(cache: Cache, q, k_new, v_new, use_workspace: bool = True, out=None):
+    """Fused cache_append(k_new, v_new) + decode_step(q) in one launch."""
+    _require_device(q, k_new, v_new)
+    s = cache.struct
+    if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
+        raise ValueError("q must be [B, H, d] in the cache dtype")
+    if tuple(k_new.shape) != (s.B, s.H_kv, s.d) or v_new.shape != k_new.shape or k_new.dtype != cache.dtype:
+        raise ValueError("k_new, v_new must be [B, Hkv, d] in the cache dtype")
+    o = torch.empty_like(q) if out is None else out
+    ws = cache.workspace() if use_workspace else None
+    nbytes = ws.numel() * 4 if ws is not None else 0
+    _lib.check("eva_append_decode",
+               _lib.load().eva_append_decode(ctypes.byref(s), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o), _ptr(ws),
+                                             nbytes, _stream()))
+    return o
+
+
 def decode_step(cache: Cache, q, use_workspace: bool = True, out=None):
     """Attention output of the last appended position: q [B, H, d] -> o [B, H, d]."""
     _require_device(q)
@@ -266,6 +283,22 @@ def rdecode_step(cache: RaggedCache, q, active=None, out=None, use_workspace=Tru
     _lib.check("eva_rdecode_step",
                _lib.load().eva_rdecode_step(ctypes.byref(s), _ptr(q), _ptr(o), _active_ptr(active), ws, nbytes,
                                             _stream()))
+    return o
+
+
+def rappend_decode(cache: RaggedCache, q, k_new, v_new, active=None, out=None, use_workspace=True):
+    """Fused rcache_append + rdecode_step of every active sequence in one launch."""
+    _require_device(q, k_new, v_new)
+    s = cache.struct
+    if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
+        raise ValueError("q must be [B, H, d] in the cache dtype")
+    if tuple(k_new.shape) != (s.B, s.H_kv, s.d) or v_new.shape != k_new.shape or k_new.dtype != cache.dtype:
+        raise ValueError("k_new, v_new must be [B, Hkv, d] in the cache dtype")
+    o = torch.zeros_like(q) if out is None else out
+    ws, nbytes = cache._ws_args(use_workspace)
+    _lib.check("eva_rappend_decode",
+               _lib.load().eva_rappend_decode(ctypes.byref(s), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o),
+                                              _active_ptr(active), ws, nbytes, _stream()))
     return o
 
 

@@ -108,12 +108,26 @@ def test_decode_rejects_fp32_cache(lib):
 
 
 def test_append_capacity(lib):
-    # W = 8, C = 4: position p makes chunk s(p)-1 visible when s(p) grows;
-    # with S_max = 32 the 33rd summary (index 32) does not fit.
-    p = 8 - 1 + 33 * 4  # s(p) = floor((p - 7) / 4) = 33 -> new summary index 32
-    c = make_cache(n_tok=p)
-    assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_CAPACITY
-    assert c.n_tok == p
+    # C = 4: the token at p = 4k + 3 completes chunk k, whose summary is built
+    # by that append; with S_max = 32 chunks 32 (p = 131) and 33 (p = 135) do
+    # not fit.
+    for p in (131, 135):
+        c = make_cache(n_tok=p)
+        assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_CAPACITY
+        assert c.n_tok == p
+        assert lib.eva_append_decode(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, None, 0, None) == \
+            _lib.EVA_ERR_CAPACITY
+        assert c.n_tok == p
+
+
+def test_append_decode_rejects(lib):
+    c = make_cache(n_tok=5)
+    f = lib.eva_append_decode
+    assert f(ctypes.byref(c), FAKE, None, FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, None, None, 0, None) == _lib.EVA_ERR_INVALID
+    c = make_cache(n_tok=5, dtype=_lib.EVA_F32)
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert c.n_tok == 5
 
 
 def test_prefill_cache_mismatch(lib):
@@ -147,8 +161,8 @@ def make_rcache(**kw):
     (dict(max_tok=0), _lib.EVA_ERR_INVALID),
     (dict(R=48), _lib.EVA_ERR_INVALID),
     (dict(W=30, C=4), _lib.EVA_ERR_CAPACITY),     # R = 32 < W + C - 1
-    # W = 8, C = 4, max_tok = 8 + 33 * 4: the last position makes summary 33 due
-    (dict(max_tok=8 + 33 * 4), _lib.EVA_ERR_CAPACITY),
+    # C = 4: a sequence of 132 tokens completes 33 chunks > S_max = 32
+    (dict(max_tok=132), _lib.EVA_ERR_CAPACITY),
     (dict(H=5), _lib.EVA_ERR_INVALID),
     (dict(d=96), _lib.EVA_ERR_UNSUPPORTED),
 ])
@@ -156,13 +170,16 @@ def test_rcache_validation(lib, kw, code):
     c = make_rcache(**kw)
     assert lib.eva_rcache_append(ctypes.byref(c), FAKE, FAKE, None, None) == code
     assert lib.eva_rdecode_step(ctypes.byref(c), FAKE, FAKE, None, None, 0, None) == code
+    assert lib.eva_rappend_decode(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == code
     assert lib.eva_rdecode_workspace_bytes(ctypes.byref(c)) == 0
 
 
 def test_rcache_capacity_boundary(lib):
-    # max_tok = 7 + 32 * 4 + 1: the last position p = 135 has s(p) = 32 = S_max
-    c = make_rcache(max_tok=8 + 32 * 4)
+    # C = 4: 131 tokens complete 32 chunks = S_max, which fits
+    c = make_rcache(max_tok=131)
     assert lib.eva_rcache_append(ctypes.byref(c), None, FAKE, None, None) == _lib.EVA_ERR_INVALID
+    assert lib.eva_rappend_decode(ctypes.byref(c), FAKE, None, FAKE, FAKE, None, None, 0, None) == \
+        _lib.EVA_ERR_INVALID
 
 
 def test_rcache_fill_rejects(lib):

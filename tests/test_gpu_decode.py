@@ -30,10 +30,12 @@ def oracle_row(qrow, K, V, p, W, C):
     return oracle.attend_rows(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C)[0]
 
 
-def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1):
+def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1, fused=False):
     """Prefill L0 tokens (if L0 > 0) into a cache, then append + decode `steps`
-    tokens; compare every `check_every`-th decode output with the oracle."""
-    print(f"decode B{B} H{H}/{Hkv} d{d} W{W} C{C} L0={L0} steps={steps} fill={fill} ws={use_ws}", flush=True)
+    tokens (two calls, or the fused call); compare every `check_every`-th
+    decode output with the oracle."""
+    print(f"decode B{B} H{H}/{Hkv} d{d} W{W} C{C} L0={L0} steps={steps} fill={fill} ws={use_ws} fused={fused}",
+          flush=True)
     dtype = torch.bfloat16
     total = L0 + steps
     q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
@@ -46,8 +48,12 @@ def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, ch
     worst = 0.0
     for t in range(steps):
         p = L0 + t
-        eva.cache_append(cache, k[:, :, p].contiguous().cuda(), v[:, :, p].contiguous().cuda())
-        o = eva.decode_step(cache, q[:, :, p].contiguous().cuda(), use_workspace=use_ws)
+        kn, vn, qn = (t[:, :, p].contiguous().cuda() for t in (k, v, q))
+        if fused:
+            o = eva.append_decode(cache, qn, kn, vn, use_workspace=use_ws)
+        else:
+            eva.cache_append(cache, kn, vn)
+            o = eva.decode_step(cache, qn, use_workspace=use_ws)
         assert cache.n_tok == p + 1
         if t % check_every and t != steps - 1:
             continue
@@ -65,30 +71,71 @@ def test_decode_after_prefill_matches_next_row():
     run_sequence(2, 8, 2, 128, 64, 16, L0=300, steps=1, seed=21)
 
 
-def test_decode_many_steps_cross_chunks_and_ring_wraps():
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_many_steps_cross_chunks_and_ring_wraps(fused):
     # R = 96 slots for W = 64, C = 16: 260 steps wrap the ring ~3 times and
-    # make 16 summaries due during decode.
-    run_sequence(1, 4, 2, 128, 64, 16, L0=100, steps=260, seed=22, check_every=7)
+    # complete 16 chunks (and make 16 summaries visible) during decode.
+    run_sequence(1, 4, 2, 128, 64, 16, L0=100, steps=260, seed=22, check_every=7, fused=fused)
 
 
-def test_decode_from_empty_cache():
-    run_sequence(1, 4, 1, 64, 24, 8, L0=0, steps=120, seed=23, check_every=5)
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_from_empty_cache(fused):
+    run_sequence(1, 4, 1, 64, 24, 8, L0=0, steps=120, seed=23, check_every=5, fused=fused)
 
 
-def test_decode_nan_filled_cache():
-    run_sequence(2, 4, 2, 128, 40, 8, L0=77, steps=60, seed=24, fill=float("nan"), check_every=3)
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_nan_filled_cache(fused):
+    run_sequence(2, 4, 2, 128, 40, 8, L0=77, steps=60, seed=24, fill=float("nan"), check_every=3, fused=fused)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_window_of_one(fused):
+    # W = 1: a chunk becomes visible one step after its last token
+    run_sequence(1, 4, 2, 128, 1, 8, L0=30, steps=40, seed=28, check_every=1, fused=fused)
 
 
 @pytest.mark.parametrize("H,Hkv", [(2, 2), (32, 2), (48, 1)])
 def test_decode_head_groupings(H, Hkv):
     # G = 1, G = 16 (one full column block), G = 48 (three head groups)
     run_sequence(1, H, Hkv, 128, 48, 16, L0=200, steps=20, seed=25, check_every=6)
+    run_sequence(1, H, Hkv, 128, 48, 16, L0=200, steps=20, seed=25, check_every=6, fused=True)
 
 
 @pytest.mark.parametrize("use_ws", [True, False])
-def test_decode_split_and_unsplit(use_ws):
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_split_and_unsplit(use_ws, fused):
     # B * Hkv = 2 units: with a workspace the rows are split over many workgroups
-    run_sequence(1, 8, 2, 128, 512, 64, L0=3000, steps=3, seed=26, use_ws=use_ws)
+    run_sequence(1, 8, 2, 128, 512, 64, L0=3000, steps=3, seed=26, use_ws=use_ws, fused=fused)
+
+
+def test_fused_step_equals_two_calls():
+    # same kernels, same arithmetic order: bit-identical outputs and caches
+    B, H, Hkv, d, W, C, L0, steps = 2, 8, 2, 128, 64, 16, 150, 70
+    q, k, v = inputs.qkv(B, H, Hkv, L0 + steps, d, torch.bfloat16, seed=29)
+    caches = []
+    outs = []
+    for fused in (False, True):
+        cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L0 + steps, fill=0.0)
+        eva.prefill(q[:, :, :L0].contiguous().cuda(), k[:, :, :L0].contiguous().cuda(),
+                    v[:, :, :L0].contiguous().cuda(), W, C, cache=cache)
+        o = []
+        for t in range(steps):
+            p = L0 + t
+            kn, vn, qn = (x[:, :, p].contiguous().cuda() for x in (k, v, q))
+            if fused:
+                o.append(eva.append_decode(cache, qn, kn, vn))
+            else:
+                eva.cache_append(cache, kn, vn)
+                o.append(eva.decode_step(cache, qn))
+        caches.append(cache)
+        outs.append(torch.stack(o))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+    n_sum = (L0 + steps) // C
+    for name in ("k_ring", "vt_ring"):
+        assert torch.equal(getattr(caches[0], name), getattr(caches[1], name)), name
+    assert torch.equal(caches[0].k_sum[:, :, :n_sum], caches[1].k_sum[:, :, :n_sum])
+    assert torch.equal(caches[0].vt_sum, caches[1].vt_sum)
 
 
 def test_cache_summaries_match_oracle():

@@ -84,8 +84,9 @@ def step_inputs(q, k, v, pos):
 
 
 def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, use_ws=True, max_tokens=None,
-              check_every=1):
-    print(f"ragged B{B} H{H}/{Hkv} d{d} W{W} C{C} lens={lens} steps={steps} fill={fill} ws={use_ws}", flush=True)
+              check_every=1, fused=False):
+    print(f"ragged B{B} H{H}/{Hkv} d{d} W{W} C{C} lens={lens} steps={steps} fill={fill} ws={use_ws} "
+          f"fused={fused}", flush=True)
     total = max(lens) + steps
     q, k, v = inputs.qkv(B, H, Hkv, total, d, torch.bfloat16, seed=seed)
     if max_tokens is None:
@@ -100,8 +101,11 @@ def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, 
         active = None if active_fn is None else torch.tensor(act, dtype=torch.int32, device="cuda")
         pos = [min(n[b], total - 1) for b in range(B)]
         qs, ks, vs = (x.cuda() for x in step_inputs(q, k, v, pos))
-        eva.rcache_append(cache, ks, vs, active=active)
-        o = eva.rdecode_step(cache, qs, active=active, out=sentinel.clone(), use_workspace=use_ws)
+        if fused:
+            o = eva.rappend_decode(cache, qs, ks, vs, active=active, out=sentinel.clone(), use_workspace=use_ws)
+        else:
+            eva.rcache_append(cache, ks, vs, active=active)
+            o = eva.rdecode_step(cache, qs, active=active, out=sentinel.clone(), use_workspace=use_ws)
         for b in range(B):
             if act[b] and n[b] < max_tokens:
                 n[b] += 1
@@ -121,32 +125,42 @@ def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, 
     return cache
 
 
-def test_ragged_generation_crosses_chunks_and_wraps():
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_generation_crosses_chunks_and_wraps(fused):
     # R = 96 for W = 64, C = 16; 150 steps wrap every ring and make summaries
     # due at different steps for every sequence
-    run_steps(4, 8, 2, 128, 64, 16, lens=[100, 37, 250, 1], steps=150, seed=41, check_every=7)
+    run_steps(4, 8, 2, 128, 64, 16, lens=[100, 37, 250, 1], steps=150, seed=41, check_every=7, fused=fused)
 
 
-def test_ragged_generation_nan_cache_and_empty_prompt():
-    run_steps(3, 4, 2, 64, 40, 8, lens=[0, 77, 9], steps=70, seed=42, fill=float("nan"), check_every=3)
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_generation_nan_cache_and_empty_prompt(fused):
+    run_steps(3, 4, 2, 64, 40, 8, lens=[0, 77, 9], steps=70, seed=42, fill=float("nan"), check_every=3, fused=fused)
 
 
-def test_ragged_generation_active_mask():
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_generation_active_mask(fused):
     # sequence 1 pauses for steps 5..24, sequence 2 is active on even steps only
     def active(t, b):
         return not ((b == 1 and 5 <= t < 25) or (b == 2 and t % 2))
-    run_steps(3, 8, 2, 128, 48, 16, lens=[60, 130, 200], steps=60, seed=43, active_fn=active, check_every=4)
+    run_steps(3, 8, 2, 128, 48, 16, lens=[60, 130, 200], steps=60, seed=43, active_fn=active, check_every=4, fused=fused)
 
 
 @pytest.mark.parametrize("use_ws", [True, False])
-def test_ragged_generation_split_and_unsplit(use_ws):
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_generation_split_and_unsplit(use_ws, fused):
     # B * Hkv = 2 units: with the workspace the rows split over many workgroups
-    run_steps(2, 8, 1, 128, 256, 32, lens=[1500, 700], steps=40, seed=44, use_ws=use_ws, check_every=13)
+    run_steps(2, 8, 1, 128, 256, 32, lens=[1500, 700], steps=40, seed=44, use_ws=use_ws, check_every=13,
+              fused=fused)
 
 
-def test_ragged_full_sequences_stop_growing():
+def test_ragged_window_of_one():
+    run_steps(2, 4, 2, 128, 1, 8, lens=[20, 3], steps=30, seed=49, check_every=1, fused=True)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_full_sequences_stop_growing(fused):
     # max_tokens = 90: sequence 0 starts full, sequence 1 fills up mid-run
-    run_steps(2, 4, 2, 128, 32, 8, lens=[95, 70], steps=30, seed=45, max_tokens=90, check_every=1)
+    run_steps(2, 4, 2, 128, 32, 8, lens=[95, 70], steps=30, seed=45, max_tokens=90, check_every=1, fused=fused)
 
 
 @pytest.mark.parametrize("H,Hkv", [(32, 2), (48, 1)])
