@@ -281,6 +281,10 @@ def bench_decode(args, torch, eva, inputs, dev):
     if args.decode_eager:
         for i in range(iters):
             token(caches[i % N_CACHES])
+        for c in caches:
+            c.struct.n_tok = ctx + 1
+        for i in range(iters):
+            decode_only(caches[i % N_CACHES])
         torch.cuda.synchronize()
         return {"workload": dw.name, "eager_iterations": iters, "graph_matches_eager": None}
     stream = torch.cuda.Stream()
@@ -386,10 +390,12 @@ def bench_generate(args, torch, eva, inputs, dev):
     torch.cuda.synchronize()
     ref = [o.clone() for o in outs]
     if args.decode_eager:
-        # per-dispatch counter runs: T eager steps, no graphs
+        # per-dispatch counter runs: T eager steps, then one plain decode per
+        # layer at the final lengths; no graphs
         fill_all()
         for _ in range(T):
             gen_step()
+        dec_step()
         torch.cuda.synchronize()
         return {"workload": gw.name, "eager_steps": T, "graph_matches_eager": None}
     stream = torch.cuda.Stream()
