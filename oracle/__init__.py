@@ -30,6 +30,9 @@ def _load():
     lib.eva_ref_visible_summaries.argtypes = [ctypes.c_long, ctypes.c_long, ctypes.c_long]
     lib.eva_ref_summaries.restype = None
     lib.eva_ref_summaries.argtypes = [_dp, _dp, ctypes.c_long, ctypes.c_int, ctypes.c_long, _dp, _dp]
+    lib.eva_ref_summaries_rf.restype = None
+    lib.eva_ref_summaries_rf.argtypes = [_dp, _dp, _dp, ctypes.c_long, ctypes.c_int, ctypes.c_long, ctypes.c_double,
+                                         _dp, _dp]
     lib.eva_ref_attend_row.restype = None
     lib.eva_ref_attend_row.argtypes = [_dp, _dp, _dp, _dp, _dp, ctypes.c_long, ctypes.c_int,
                                        ctypes.c_long, ctypes.c_long, _dp]
@@ -72,6 +75,20 @@ def summaries(K, V, C: int):
     Ks = np.zeros((n_chunks, d))
     Vs = np.zeros((n_chunks, d))
     _load().eva_ref_summaries(_ptr(K), _ptr(V), L, d, C, _ptr(Ks), _ptr(Vs))
+    return Ks, Vs
+
+
+def summaries_rf(K, V, eps, C: int, lam: float = 0.1):
+    """Stochastic random-feature summaries of one sequence: K, V [L, d], eps
+    [L // C, d] (one N(0, I) draw per chunk) -> (Ksum, Vsum) [L // C, d]."""
+    K, V, eps = _f64(K), _f64(V), _f64(eps)
+    L, d = K.shape
+    n_chunks = L // C
+    assert eps.shape == (n_chunks, d)
+    Ks = np.zeros((n_chunks, d))
+    Vs = np.zeros((n_chunks, d))
+    if n_chunks:
+        _load().eva_ref_summaries_rf(_ptr(K), _ptr(V), _ptr(eps), L, d, C, float(lam), _ptr(Ks), _ptr(Vs))
     return Ks, Vs
 
 

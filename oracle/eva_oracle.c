@@ -90,6 +90,69 @@ void eva_ref_summaries(const double* K, const double* V, long L, int d, long C,
     free(a);
 }
 
+/* Stochastic random-feature summaries (section "EVA Attention": with one
+ * sample omega per chunk the chunk's value is the ratio of the sums of
+ * g_m and h_m, in which every query-dependent factor is common to all terms
+ * and cancels, leaving
+ *     vhat_c = sum_j xi(k_j, omega) v_j / sum_j xi(k_j, omega),
+ *     xi(x, omega) = exp(omega . x - |x|^2 / 2)
+ * (section "Random Feature Attention"); the sample comes from the clipped,
+ * downscaled proposal of the ablation "Impact of random feature sampling
+ * distribution": omega = mu_c + lambda * clip(eps, -1, 1), eps ~ N(0, I)
+ * given by the caller, mu_c the chunk's mean key).  The feature map acts on
+ * the scaled keys x = k / d^(1/4), the scaling under which exp(q.k/sqrt(d))
+ * is exp(q'.k'), so mu_c is the mean of the scaled keys.  The summary key is
+ * the unscaled mean key, as for the deterministic summaries.
+ * eps: [floor(L/C)][d], one draw per chunk. */
+void eva_ref_summaries_rf(const double* K, const double* V, const double* eps, long L, int d, long C,
+                          double lambda, double* Ksum, double* Vsum)
+{
+    long n_chunks = L / C;
+    double inv_root4_d = 1.0 / sqrt(sqrt((double)d));
+    double* a = (double*)malloc((size_t)C * sizeof(double));
+    double* x = (double*)malloc((size_t)d * sizeof(double));
+    double* omega = (double*)malloc((size_t)d * sizeof(double));
+    for (long c = 0; c < n_chunks; ++c) {
+        const double* Kc = K + (size_t)c * C * d;
+        const double* Vc = V + (size_t)c * C * d;
+        const double* ec = eps + (size_t)c * d;
+        double* kh = Ksum + (size_t)c * d;
+        double* vh = Vsum + (size_t)c * d;
+
+        /* mean key, and the sample: mean scaled key + lambda * clip(eps) */
+        for (int e = 0; e < d; ++e) {
+            double s = 0.0;
+            for (long j = 0; j < C; ++j) s += Kc[(size_t)j * d + e];
+            kh[e] = s / (double)C;
+            double clipped = ec[e] < -1.0 ? -1.0 : (ec[e] > 1.0 ? 1.0 : ec[e]);
+            omega[e] = kh[e] * inv_root4_d + lambda * clipped;
+        }
+        /* log xi(x_j, omega) for the scaled keys x_j */
+        double amax = -INFINITY;
+        for (long j = 0; j < C; ++j) {
+            double dot = 0.0, norm2 = 0.0;
+            for (int e = 0; e < d; ++e) {
+                x[e] = Kc[(size_t)j * d + e] * inv_root4_d;
+                dot += omega[e] * x[e];
+                norm2 += x[e] * x[e];
+            }
+            a[j] = dot - 0.5 * norm2;
+            if (a[j] > amax) amax = a[j];
+        }
+        /* ratio of xi-weighted sums (the common factor exp(amax) cancels) */
+        double den = 0.0;
+        for (long j = 0; j < C; ++j) den += exp(a[j] - amax);
+        for (int e = 0; e < d; ++e) {
+            double num = 0.0;
+            for (long j = 0; j < C; ++j) num += exp(a[j] - amax) * Vc[(size_t)j * d + e];
+            vh[e] = num / den;
+        }
+    }
+    free(a);
+    free(x);
+    free(omega);
+}
+
 /* One attention row: query q at position n against the exact keys of its
  * window and the visible chunk summaries. */
 void eva_ref_attend_row(const double* q, const double* K, const double* V,

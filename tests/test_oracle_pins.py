@@ -291,3 +291,90 @@ def test_rows_entry_matches_whole_prefill():
     rows = np.array([0, 7, 8, 11, 12, 31, 49])
     got = oracle.attend_rows(q[0, 1, rows], rows, k[0, 0], v[0, 0], Ks, Vs, W, C)
     np.testing.assert_array_equal(got, o[0, 1, rows])
+
+
+# ---------------------------------------------------------------------------
+# Stochastic random-feature summaries (section "EVA Attention", single sample
+# per chunk; xi from section "Random Feature Attention"; the clipped,
+# downscaled proposal from the ablation "Impact of random feature sampling
+# distribution")
+# ---------------------------------------------------------------------------
+
+def test_rf_summary_is_ratio_of_control_variate_sums():
+    # The chunk value of eq. (eva) with S = 1: sum_m g_m / sum_m h_m, with g_m
+    # and h_m carrying the importance weight N(w; 0, I) / (Z q(w)) and the
+    # query feature xi(q_n, w).  Evaluated literally here for an arbitrary
+    # query and weight: every query-dependent factor must cancel.
+    C, d, lam = 6, 4, 0.1
+    L = 3 * C
+    k, v, eps = 0.5 * rand((L, d), 40), rand((L, d), 41), 2.0 * rand((L // C, d), 42)
+    _, vs = oracle.summaries_rf(k, v, eps, C, lam)
+    r4 = d ** 0.25
+    xi = lambda x, w: math.exp(float(np.dot(w, x)) - 0.5 * float(np.dot(x, x)))
+    q = rand(d, 43) / r4
+    for c in range(L // C):
+        xs = k[c * C:(c + 1) * C] / r4
+        w = xs.mean(axis=0) + lam * np.clip(eps[c], -1.0, 1.0)
+        weight = math.exp(-0.5 * float(np.dot(w, w))) / (2.0 * math.pi) ** (d / 2) / (3.7 * 0.21)
+        g = sum(weight * xi(q, w) * xi(xs[j], w) * v[c * C + j] for j in range(C))
+        h = sum(weight * xi(q, w) * xi(xs[j], w) for j in range(C))
+        np.testing.assert_allclose(vs[c], g / h, rtol=1e-11, atol=1e-12)
+
+
+def test_rf_summary_without_noise_and_equal_norms_is_deterministic_summary():
+    # lambda = 0 and keys of one norm inside each chunk: the -|x|^2/2 term is
+    # common to the chunk and cancels, leaving softmax(mean . k / sqrt(d)).
+    C, d = 8, 16
+    k = rand((4 * C, d), 44)
+    k = 3.0 * k / np.linalg.norm(k, axis=1, keepdims=True)
+    v = rand((4 * C, d), 45)
+    ks, vs = oracle.summaries_rf(k, v, rand((4, d), 46), C, lam=0.0)
+    ks0, vs0 = oracle.summaries(k, v, C)
+    np.testing.assert_allclose(ks, ks0, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(vs, vs0, rtol=1e-11, atol=1e-12)
+
+
+def test_rf_summary_norm_term_closed_form():
+    # Two keys 0 and x: the sample (lambda = 0) is x/2 in scaled units, so
+    # both log-weights are 0 (x/2 . x - |x|^2/2 = 0): the value is the plain
+    # mean.  Without the norm term the second key would weigh exp(|x|^2/2)
+    # times more.
+    d = 4
+    x = np.array([[0.0, 0.0, 0.0, 0.0], [1.5, -2.0, 0.5, 1.0]])
+    v = rand((2, d), 47)
+    _, vs = oracle.summaries_rf(x, v, np.zeros((1, d)), 2, lam=0.0)
+    np.testing.assert_allclose(vs[0], v.mean(axis=0), rtol=1e-13, atol=1e-14)
+    _, vs_det = oracle.summaries(x, v, 2)
+    assert np.abs(vs_det[0] - v.mean(axis=0)).max() > 1e-3
+
+
+def test_rf_summary_clips_noise_before_scaling():
+    # omega = mean + lambda * clip(eps, -1, 1): noise beyond +-1 saturates,
+    # and lambda multiplies the clipped value (halving in-range noise and
+    # doubling lambda changes nothing).
+    C, d = 5, 8
+    k, v = rand((3 * C, d), 48), rand((3 * C, d), 49)
+    e = rand((3, d), 50)
+    big = np.sign(e) * 5.0
+    unit = np.sign(e)
+    np.testing.assert_allclose(oracle.summaries_rf(k, v, big, C, 0.3)[1], oracle.summaries_rf(k, v, unit, C, 0.3)[1],
+                               rtol=1e-13, atol=1e-14)
+    small = np.clip(e, -0.9, 0.9)
+    np.testing.assert_allclose(oracle.summaries_rf(k, v, small / 2, C, 0.4)[1],
+                               oracle.summaries_rf(k, v, small, C, 0.2)[1], rtol=1e-12, atol=1e-13)
+
+
+def test_rf_summary_noise_direction():
+    # A large lambda along +e0 favours the chunk key with the largest first
+    # feature: the value tends to that key's value.
+    d, C = 4, 4
+    k = np.zeros((C, d))
+    k[:, 0] = [-1.0, 0.0, 0.5, 2.0]
+    v = np.eye(C, d)
+    eps = np.zeros((1, d))
+    eps[0, 0] = 3.0  # clipped to 1
+    _, vs = oracle.summaries_rf(k, v, eps, C, lam=40.0)
+    assert vs[0, 3] > 0.999
+    eps[0, 0] = -3.0
+    _, vs = oracle.summaries_rf(k, v, eps, C, lam=40.0)
+    assert vs[0, 0] > 0.999
