@@ -201,11 +201,26 @@ def main():
         return sum(ev[i].elapsed_time(ev[j]) for ev in evs) / len(evs)
 
     ms_summ, ms_attn, ms_fill_app, ms_dec = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
+
+    # stochastic random-feature summaries of the same K, V (one noise draw
+    # per chunk, read once more: + n_chunks * d * 4 bytes per (b, kv head))
+    eps = torch.randn(B, Hkv, L // C, d, device=dev)
+    eva.build_summaries_rf(k, v, eps, C, lam=0.1, out=(Ks, Vs))
+    r0 = torch.cuda.Event(enable_timing=True)
+    r1 = torch.cuda.Event(enable_timing=True)
+    n_rf = max(args.steps, 1)
+    r0.record()
+    for _ in range(n_rf):
+        eva.build_summaries_rf(k, v, eps, C, lam=0.1, out=(Ks, Vs))
+    r1.record()
+    torch.cuda.synchronize()
+    ms_summ_rf = r0.elapsed_time(r1) / n_rf
     flops, attn_bytes, summ_bytes = prefill_counts(B, H, Hkv, L, d, W, C, e)
     attn_gbs = attn_bytes / (ms_attn * 1e-3) / 1e9
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
     print(f"# step {ms_step:.3f} ms: summaries {ms_summ:.3f}, attention {ms_attn:.3f}, fill+append "
-          f"{ms_fill_app:.3f}, decode {ms_dec:.3f}", file=sys.stderr, flush=True)
+          f"{ms_fill_app:.3f}, decode {ms_dec:.3f}; stochastic summaries {ms_summ_rf:.3f}", file=sys.stderr,
+          flush=True)
 
     traffic = read_traffic("prefill_attention_llm-bf16_traffic.txt", PREFILL_SOURCES)
     out = {
@@ -230,6 +245,8 @@ def main():
         "prefill": {"attention_ms": ms_attn, "attention_tflops": attn_tflops,
                     "attention_mfma_frac": attn_tflops / PEAK_BF16_TFLOPS,
                     "summaries_ms": ms_summ, "summaries_gbs": summ_bytes / (ms_summ * 1e-3) / 1e9,
+                    "summaries_rf_ms": ms_summ_rf,
+                    "summaries_rf_gbs": (summ_bytes + B * Hkv * (L // C) * d * 4) / (ms_summ_rf * 1e-3) / 1e9,
                     "fill_append_ms": ms_fill_app, "decode_ms": ms_dec,
                     "alg_flops": flops, "alg_bytes_attention": attn_bytes, "alg_bytes_summaries": summ_bytes},
     }

@@ -107,6 +107,30 @@ int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum,
                         int B, int H_kv, int L, int d, int C, int dtype, void* stream);
 
 /*
+ * Stochastic random-feature chunk summaries: the paper's single-sample
+ * estimator (section "EVA Attention", S = 1; feature map
+ * xi(x, w) = exp(w . x - |x|^2 / 2) of section "Random Feature Attention").
+ * With one sample per chunk every query-dependent factor cancels and the
+ * chunk value is sum_j xi(x_j, w) V_j / sum_j xi(x_j, w) over the chunk's
+ * scaled keys x_j = K_j / d^(1/4) (the scaling under which
+ * exp(q . k / sqrt(d)) = exp(q' . k')).  The sample is
+ *     w = mean_j x_j + lambda * clip(eps_c, -1, 1)
+ * (the clipped, downscaled proposal of the ablation "Impact of random feature
+ * sampling distribution"; the paper uses lambda = 0.1).  Ksum is the mean
+ * key, as in eva_build_summaries; lambda = 0 with keys of equal norm inside
+ * each chunk gives eva_build_summaries' result.
+ *   eps  device fp32 [B][H_kv][L / C][d], 16-byte aligned: the standard
+ *        normal draws, one vector per chunk, supplied by the caller.
+ * The prefill kernel takes these summaries as it takes any
+ * (eva_prefill_attention).  The decode cache builds deterministic summaries
+ * for chunks completed during decode.
+ * Errors: as eva_build_summaries; INVALID for a null or misaligned eps or a
+ * negative, NaN or infinite lambda.
+ */
+int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float lambda, void* Ksum, void* Vsum,
+                           int B, int H_kv, int L, int d, int C, int dtype, void* stream);
+
+/*
  * EVA prefill (section "FlashEVA"): O = one softmax per row over the window
  * keys and the visible chunk summaries, as described at the top of this file.
  * Builds the summaries first (into Ksum/Vsum, caller-provided, shape

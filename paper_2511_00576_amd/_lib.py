@@ -20,6 +20,7 @@ EVA_F32 = 1
 # Every entry point include/eva.h declares.
 SYMBOLS = (
     "eva_build_summaries",
+    "eva_build_summaries_rf",
     "eva_prefill",
     "eva_prefill_attention",
     "eva_cache_fill",
@@ -74,6 +75,8 @@ def load():
     cp = ctypes.POINTER(EvaCacheStruct)
     lib.eva_build_summaries.restype = i
     lib.eva_build_summaries.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
+    lib.eva_build_summaries_rf.restype = i
+    lib.eva_build_summaries_rf.argtypes = [vp, vp, vp, ctypes.c_float, vp, vp, i, i, i, i, i, i, vp]
     lib.eva_prefill.restype = i
     lib.eva_prefill.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_prefill_attention.restype = i

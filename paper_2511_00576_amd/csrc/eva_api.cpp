@@ -185,7 +185,27 @@ int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum, in
     if (!aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
-        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, s);
+        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, nullptr,
+                                                                       0.f, s);
+    }));
+}
+
+int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float lambda, void* Ksum, void* Vsum,
+                           int B, int H_kv, int L, int d, int C, int dtype, void* stream) {
+    if (B < 1 || H_kv < 1 || L < 1 || C < 1) return EVA_ERR_INVALID;
+    if (!(lambda >= 0.f) || lambda > 1e30f) return EVA_ERR_INVALID;  // rejects NaN and infinities
+    int st = supported(d, dtype);
+    if (st != EVA_OK) return st;
+    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (L / C == 0) return EVA_OK;
+    if (!K || !V || !Ksum || !Vsum || !eps) return EVA_ERR_INVALID;
+    if (!aligned16(K) || !aligned16(V) || !aligned16(eps)) return EVA_ERR_INVALID;
+    const float rf_scale = (float)(lambda * sqrt(sqrt((double)d)));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
+        return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, eps,
+                                                                       rf_scale, s);
     }));
 }
 

@@ -43,9 +43,11 @@ hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
 template <int D>
 hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream);
 
+// Chunk summaries; with eps (fp32 [BH][L / C][D]) the stochastic
+// random-feature variant with rf_scale = lambda * d^(1/4).
 template <int D, typename T>
 hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
-                            hipStream_t stream);
+                            const float* eps, float rf_scale, hipStream_t stream);
 
 struct CacheView {
     int B, H, Hkv, W, C, R, S_max;

@@ -8,10 +8,13 @@ namespace eva {
 
 namespace {
 
-template <int D, typename T>
+// eps (RF only): fp32 [BH][n_chunks][D], one noise draw per chunk;
+// rf_scale = lambda * d^(1/4).
+template <int D, typename T, bool RF>
 __global__ __launch_bounds__(kSummaryThreads) void summary_kernel(const T* __restrict__ K, const T* __restrict__ V,
                                                                   T* __restrict__ Ks, T* __restrict__ Vs, int L,
-                                                                  int C, int n_chunks) {
+                                                                  int C, int n_chunks, const float* __restrict__ eps,
+                                                                  float rf_scale) {
     extern __shared__ float smem[];
     constexpr int TPR = D / 8;
     const int chunk = blockIdx.x;
@@ -19,7 +22,8 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel(const T* __res
     const size_t row0 = bg * (size_t)L + (size_t)chunk * C;
     RowMajorChunk<D, T> src{K + row0 * D, V + row0 * D};
     float kh[8], vh[8];
-    chunk_summary<D>(src, C, smem, smem + C, kh, vh);
+    const RfNoise rf{RF ? eps + (bg * n_chunks + chunk) * D + (threadIdx.x % TPR) * 8 : nullptr, rf_scale};
+    chunk_summary<D, RF>(src, C, smem, smem + C, kh, vh, rf);
     const int t = threadIdx.x;
     if (t < TPR) {
         const size_t out = (bg * n_chunks + chunk) * D + t * 8;
@@ -35,10 +39,11 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel(const T* __res
 // thread requests all of its key and value rows up front (one memory latency
 // per chunk instead of one per pass), keeps them in registers, and the three
 // passes of the summary run on those registers.
-template <int D, typename T, int ROWS>
+template <int D, typename T, int ROWS, bool RF>
 __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* __restrict__ K, const T* __restrict__ V,
                                                                       T* __restrict__ Ks, T* __restrict__ Vs, int L,
-                                                                      int n_chunks) {
+                                                                      int n_chunks, const float* __restrict__ eps,
+                                                                      float rf_scale) {
     constexpr int TPR = D / 8;
     constexpr int RPS = kSummaryThreads / TPR;
     constexpr int C = ROWS * RPS;
@@ -52,6 +57,12 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* _
     const T* vp = V + (row0 + r0) * D + cc * 8;
 
     u32x4 kw[ROWS][VW], vw[ROWS][VW];
+    floatx4 ew[2];
+    if constexpr (RF) {
+        const float* ep = eps + (bg * n_chunks + chunk) * D + cc * 8;
+        ew[0] = *reinterpret_cast<const floatx4*>(ep);
+        ew[1] = *reinterpret_cast<const floatx4*>(ep + 4);
+    }
 #pragma unroll
     for (int i = 0; i < ROWS; ++i)
 #pragma unroll
@@ -87,8 +98,13 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* _
 #pragma unroll
     for (int e = 0; e < 8; ++e) kh[e] *= 1.0f / (float)C;
 
-    // pass 2: scores (log2 units); the TPR threads of a row hold its full score
+    // pass 2: scores (log2 units); the TPR threads of a row hold its full
+    // score.  Weight vector as in chunk_summary (RfNoise).
     const float sc = kLog2e * rsqrtf((float)D);
+    float w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        w[e] = RF ? kh[e] + rf_scale * fminf(fmaxf(ew[e >> 2][e & 3], -1.f), 1.f) : kh[e];
     float s[ROWS];
     float amax = -INFINITY;
 #pragma unroll
@@ -97,7 +113,7 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* _
         unpack(kw[i], k);
         float x = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x += kh[e] * k[e];
+        for (int e = 0; e < 8; ++e) x += (RF ? w[e] - 0.5f * k[e] : w[e]) * k[e];
 #pragma unroll
         for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
         s[i] = x * sc;
@@ -136,49 +152,61 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* _
     }
 }
 
-}  // namespace
-
-template <int D, typename T>
-hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
-                            hipStream_t stream) {
+template <int D, typename T, bool RF>
+hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
+                                 const float* eps, float rf_scale, hipStream_t stream) {
     const int n_chunks = L / C;
     if (n_chunks == 0) return hipSuccess;
     constexpr int RPS = kSummaryThreads / (D / 8);
+    const T* k = static_cast<const T*>(K);
+    const T* v = static_cast<const T*>(V);
+    T* ks = static_cast<T*>(Ks);
+    T* vs = static_cast<T*>(Vs);
     if (C % RPS == 0 && C / RPS <= 8) {
         const dim3 grid(n_chunks, BH);
-        const T* k = static_cast<const T*>(K);
-        const T* v = static_cast<const T*>(V);
         switch (C / RPS) {
             case 1:
-                hipLaunchKernelGGL((summary_kernel_reg<D, T, 1>), grid, dim3(kSummaryThreads), 0, stream, k, v,
-                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 1, RF>), grid, dim3(kSummaryThreads), 0, stream, k, v, ks,
+                                   vs, L, n_chunks, eps, rf_scale);
                 return hipGetLastError();
             case 2:
-                hipLaunchKernelGGL((summary_kernel_reg<D, T, 2>), grid, dim3(kSummaryThreads), 0, stream, k, v,
-                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 2, RF>), grid, dim3(kSummaryThreads), 0, stream, k, v, ks,
+                                   vs, L, n_chunks, eps, rf_scale);
                 return hipGetLastError();
             case 4:
-                hipLaunchKernelGGL((summary_kernel_reg<D, T, 4>), grid, dim3(kSummaryThreads), 0, stream, k, v,
-                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 4, RF>), grid, dim3(kSummaryThreads), 0, stream, k, v, ks,
+                                   vs, L, n_chunks, eps, rf_scale);
                 return hipGetLastError();
             case 8:
-                hipLaunchKernelGGL((summary_kernel_reg<D, T, 8>), grid, dim3(kSummaryThreads), 0, stream, k, v,
-                                   static_cast<T*>(Ks), static_cast<T*>(Vs), L, n_chunks);
+                hipLaunchKernelGGL((summary_kernel_reg<D, T, 8, RF>), grid, dim3(kSummaryThreads), 0, stream, k, v, ks,
+                                   vs, L, n_chunks, eps, rf_scale);
                 return hipGetLastError();
             default:
                 break;
         }
     }
     const size_t lds = (size_t)(C + summary_red_floats<D>()) * sizeof(float);
-    hipLaunchKernelGGL((summary_kernel<D, T>), dim3(n_chunks, BH), dim3(kSummaryThreads), lds, stream,
-                       static_cast<const T*>(K), static_cast<const T*>(V), static_cast<T*>(Ks),
-                       static_cast<T*>(Vs), L, C, n_chunks);
+    hipLaunchKernelGGL((summary_kernel<D, T, RF>), dim3(n_chunks, BH), dim3(kSummaryThreads), lds, stream, k, v, ks, vs,
+                       L, C, n_chunks, eps, rf_scale);
     return hipGetLastError();
 }
 
-template hipError_t launch_summaries<64, bf16>(const void*, const void*, void*, void*, int, int, int, hipStream_t);
-template hipError_t launch_summaries<128, bf16>(const void*, const void*, void*, void*, int, int, int, hipStream_t);
-template hipError_t launch_summaries<64, float>(const void*, const void*, void*, void*, int, int, int, hipStream_t);
-template hipError_t launch_summaries<128, float>(const void*, const void*, void*, void*, int, int, int, hipStream_t);
+}  // namespace
+
+template <int D, typename T>
+hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
+                            const float* eps, float rf_scale, hipStream_t stream) {
+    if (eps) return launch_summaries_impl<D, T, true>(K, V, Ks, Vs, BH, L, C, eps, rf_scale, stream);
+    return launch_summaries_impl<D, T, false>(K, V, Ks, Vs, BH, L, C, nullptr, 0.f, stream);
+}
+
+#define EVA_SUMMARIES(D, T)                                                                                       \
+    template hipError_t launch_summaries<D, T>(const void*, const void*, void*, void*, int, int, int, const float*, \
+                                               float, hipStream_t);
+EVA_SUMMARIES(64, bf16)
+EVA_SUMMARIES(128, bf16)
+EVA_SUMMARIES(64, float)
+EVA_SUMMARIES(128, float)
+#undef EVA_SUMMARIES
 
 }  // namespace eva

@@ -136,11 +136,23 @@ __device__ __forceinline__ float block_max(float x, float* red) {
     return m;
 }
 
+// Logit weight vector of one thread's 8 features.  Deterministic summaries:
+// the mean key (logit khat . k).  Stochastic random-feature summaries
+// (one sample omega = mean scaled key + lambda * clip(eps, -1, 1) per chunk,
+// feature map exp(omega . x - |x|^2 / 2) on the scaled keys x = k / d^(1/4)):
+// the logit times sqrt(d) is k . (khat + lambda d^(1/4) clip(eps) - k / 2),
+// so the weight vector is khat + rf_scale * clip(eps) and the row adds -k/2.
+struct RfNoise {
+    const float* eps;  // this thread's 8 noise values (nullptr: deterministic)
+    float scale;       // lambda * d^(1/4)
+};
+
 // Computes the summary of one chunk of C rows.  `logits` holds C floats of
 // LDS, `red` 5*TPR*8 floats of LDS.  Results: khat[8], vhat[8] for this
 // thread's feature chunk cc = threadIdx.x % TPR (valid in every thread).
-template <int D, typename Src>
-__device__ void chunk_summary(const Src& src, int C, float* logits, float* red, float khat[8], float vhat[8]) {
+template <int D, bool RF = false, typename Src>
+__device__ void chunk_summary(const Src& src, int C, float* logits, float* red, float khat[8], float vhat[8],
+                              RfNoise rf = {nullptr, 0.f}) {
     constexpr int TPR = D / 8;
     constexpr int RPS = kSummaryThreads / TPR;
     const int t = threadIdx.x;
@@ -162,13 +174,16 @@ __device__ void chunk_summary(const Src& src, int C, float* logits, float* red, 
 
     // pass 2: scores a_j (log2 units) into LDS, running max
     const float sc = kLog2e * rsqrtf((float)D);
+    float w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = RF ? khat[i] + rf.scale * fminf(fmaxf(rf.eps[i], -1.f), 1.f) : khat[i];
     float amax = -INFINITY;
     for (int r = r0; r < C; r += RPS) {
         float k[8];
         src.load_k(r, cc, k);
         float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s += khat[i] * k[i];
+        for (int i = 0; i < 8; ++i) s += (RF ? w[i] - 0.5f * k[i] : w[i]) * k[i];
 #pragma unroll
         for (int off = 1; off < TPR; off <<= 1) s += __shfl_xor(s, off, 64);
         s *= sc;

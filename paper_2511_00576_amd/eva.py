@@ -55,6 +55,25 @@ def build_summaries(K: torch.Tensor, V: torch.Tensor, C: int, out=None):
     return Ks, Vs
 
 
+def build_summaries_rf(K: torch.Tensor, V: torch.Tensor, eps: torch.Tensor, C: int, lam: float = 0.1, out=None):
+    """Stochastic random-feature summaries.  K, V: [B, Hkv, L, d]; eps: fp32
+    [B, Hkv, L // C, d] standard normal draws (one per chunk) -> (Ksum, Vsum)."""
+    _require_device(K, V, eps)
+    B, Hkv, L, d = K.shape
+    if eps.dtype != torch.float32 or tuple(eps.shape) != (B, Hkv, L // C, d):
+        raise ValueError("eps must be float32 [B, Hkv, L // C, d]")
+    if out is None:
+        Ks = torch.empty(B, Hkv, L // C, d, dtype=K.dtype, device=K.device)
+        Vs = torch.empty_like(Ks)
+    else:
+        Ks, Vs = out
+    lib = _lib.load()
+    _lib.check("eva_build_summaries_rf",
+               lib.eva_build_summaries_rf(_ptr(K), _ptr(V), _ptr(eps), float(lam), _ptr(Ks), _ptr(Vs), B, Hkv, L, d,
+                                          C, _dtype_code(K), _stream()))
+    return Ks, Vs
+
+
 class Cache:
     """Window + summary decode cache in device memory (see eva_cache in eva.h).
 

@@ -202,3 +202,24 @@ def test_rdecode_and_generate_reject(lib):
     assert g(ctypes.byref(c), FAKE, None, FAKE, FAKE, 4, None, None, 0, None) == _lib.EVA_ERR_INVALID
     assert g(ctypes.byref(c), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE, 4, None, None, 0,
              None) == _lib.EVA_ERR_INVALID
+
+
+def test_summaries_rf_rejects(lib):
+    f = lib.eva_build_summaries_rf
+    ok = dict(K=FAKE, V=FAKE, eps=FAKE, lam=0.1, Ks=FAKE, Vs=FAKE, B=1, H_kv=1, L=64, d=64, C=4, dtype=0)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["K"], a["V"], a["eps"], a["lam"], a["Ks"], a["Vs"], a["B"], a["H_kv"], a["L"], a["d"], a["C"],
+                 a["dtype"], None)
+
+    assert call(eps=None) == _lib.EVA_ERR_INVALID
+    assert call(eps=ctypes.c_void_p(0x10004)) == _lib.EVA_ERR_INVALID  # misaligned
+    assert call(lam=-0.5) == _lib.EVA_ERR_INVALID
+    assert call(lam=float("nan")) == _lib.EVA_ERR_INVALID
+    assert call(lam=float("inf")) == _lib.EVA_ERR_INVALID
+    assert call(d=96) == _lib.EVA_ERR_UNSUPPORTED
+    assert call(C=0) == _lib.EVA_ERR_INVALID
+    # fewer tokens than one chunk: nothing to do, no pointer needed
+    assert call(K=None, V=None, eps=None, Ks=None, Vs=None, L=3) == _lib.EVA_OK

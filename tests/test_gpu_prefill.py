@@ -117,6 +117,42 @@ def test_summaries(L, C, d):
                 assert_parity(to64(Vs[b, g]), rV, dtype, "Vsum")
 
 
+@pytest.mark.parametrize("L,C", [(1000, 7), (64, 64), (4096, 256), (300, 32), (600, 128), (640, 160)])
+@pytest.mark.parametrize("d", [64, 128])
+def test_summaries_rf(L, C, d):
+    # both summary kernels (register-resident and three-pass), both dtypes;
+    # lambda large enough that the noise term matters, noise beyond +-1
+    for dtype in (torch.float32, torch.bfloat16):
+        _, k, v = inputs.qkv(2, 1, 3, L, d, dtype, seed=18)
+        eps = inputs.normal((2, 3, L // C, d), 19) * 1.5
+        Ks, Vs = eva.build_summaries_rf(*cuda(k, v), eps.cuda(), C, lam=0.3)
+        torch.cuda.synchronize()
+        for b in range(2):
+            for g in range(3):
+                rK, rV = oracle.summaries_rf(k[b, g], v[b, g], eps[b, g], C, lam=0.3)
+                assert_parity(to64(Ks[b, g]), rK, dtype, "Ksum")
+                assert_parity(to64(Vs[b, g]), rV, dtype, "Vsum")
+
+
+def test_prefill_with_rf_summaries():
+    # the fused prefill with stochastic summaries against oracle rows over the
+    # oracle's stochastic summaries
+    B, H, Hkv, L, d, W, C = 2, 8, 2, 700, 128, 64, 32
+    for dtype in (torch.float32, torch.bfloat16):
+        q, k, v = inputs.qkv(B, H, Hkv, L, d, dtype, seed=20)
+        eps = inputs.normal((B, Hkv, L // C, d), 21)
+        qc, kc, vc = cuda(q, k, v)
+        Ks, Vs = eva.build_summaries_rf(kc, vc, eps.cuda(), C, lam=0.1)
+        O = eva.prefill_attention(qc, kc, vc, Ks, Vs, W, C)
+        torch.cuda.synchronize()
+        rows = edge_rows(L, W, C, extra=16, seed=3)
+        for b, h in ((0, 0), (1, 5)):
+            g = h // (H // Hkv)
+            rK, rV = oracle.summaries_rf(k[b, g], v[b, g], eps[b, g], C, lam=0.1)
+            ref = oracle.attend_rows(to64(q[b, h, torch.from_numpy(rows)]), rows, k[b, g], v[b, g], rK, rV, W, C)
+            assert_parity(to64(O[b, h, torch.from_numpy(rows)]), ref, dtype, f"rf prefill b{b} h{h}")
+
+
 FULL = [inputs.LLM_BF16, inputs.GQA_BF16, inputs.LONG_BF16]
 
 
