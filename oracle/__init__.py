@@ -39,6 +39,13 @@ def _load():
     lib.eva_ref_attend_rows.restype = None
     lib.eva_ref_attend_rows.argtypes = [_dp, _lp, ctypes.c_long, _dp, _dp, _dp, _dp, ctypes.c_int,
                                         ctypes.c_long, ctypes.c_long, _dp]
+    lib.eva_ref_attend_rows_variant.restype = None
+    lib.eva_ref_attend_rows_variant.argtypes = [_dp, _lp, ctypes.c_long, _dp, _dp, _dp, _dp, ctypes.c_long,
+                                                ctypes.c_int, ctypes.c_long, ctypes.c_long, ctypes.c_int, _dp]
+    lib.eva_ref_prefill_variant.restype = None
+    lib.eva_ref_prefill_variant.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_long, ctypes.c_int, ctypes.c_long, ctypes.c_long, ctypes.c_int,
+                                            _dp, _dp]
     lib.eva_ref_prefill.restype = None
     lib.eva_ref_prefill.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_long, ctypes.c_int, ctypes.c_long, ctypes.c_long, _dp, _dp]
@@ -122,4 +129,40 @@ def prefill(Q, K, V, W: int, C: int, return_summaries: bool = False):
                             _ptr(Ks), _ptr(Vs))
     if return_summaries:
         return O, Ks[:, :, :n_chunks], Vs[:, :, :n_chunks]
+    return O
+
+
+# Window variants (eva_ref_attend_row_variant): 0 sliding, 1 chunk-aligned,
+# 2 blocked, 3 non-causal blocked.
+SLIDING, CHUNK_ALIGNED, BLOCKED, NONCAUSAL = 0, 1, 2, 3
+
+
+def attend_rows_variant(Qrows, rows, K, V, Ksum, Vsum, W: int, C: int, variant: int):
+    """Rows of one sequence under a window variant; K, V hold the whole
+    sequence (L = K.shape[0]) and Ksum, Vsum all its L // C summaries."""
+    Qrows, K, V = _f64(Qrows), _f64(K), _f64(V)
+    Ksum, Vsum = _f64(Ksum), _f64(Vsum)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    L, d = K.shape
+    assert Ksum.shape[0] == L // C
+    if Ksum.shape[0] == 0:
+        Ksum = np.zeros((1, d))
+        Vsum = np.zeros((1, d))
+    out = np.zeros((rows.shape[0], d))
+    _load().eva_ref_attend_rows_variant(_ptr(Qrows), rows.ctypes.data_as(_lp), rows.shape[0], _ptr(K), _ptr(V),
+                                        _ptr(Ksum), _ptr(Vsum), L, d, W, C, int(variant), _ptr(out))
+    return out
+
+
+def prefill_variant(Q, K, V, W: int, C: int, variant: int):
+    """Whole prefill under a window variant: Q [B, H, L, d]; K, V [B, Hkv, L, d]."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    n_chunks = L // C
+    O = np.zeros_like(Q)
+    Ks = np.zeros((B, Hkv, max(n_chunks, 1), d))
+    Vs = np.zeros((B, Hkv, max(n_chunks, 1), d))
+    _load().eva_ref_prefill_variant(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C, int(variant),
+                                    _ptr(Ks), _ptr(Vs))
     return O

@@ -197,6 +197,94 @@ void eva_ref_attend_row(const double* q, const double* K, const double* V,
 }
 
 /* Selected rows of one sequence: rows[r] is a position, Qrows[r] its query. */
+/* Window variants (the ablation "EVA Local Window Attention Variants": the
+ * original EVA's blocked local windows besides the sliding window of section
+ * "FlashEVA"; the non-causal form of section "FlashEVA"; and a sliding window
+ * extended down to its chunk boundary).  Row n of a sequence of L tokens
+ * attends the exact keys m in [lo, hi] and the summaries of the complete
+ * chunks c < n_chunks = floor(L / C) listed below:
+ *   0 sliding        lo = max(0, n-W+1), hi = n;  chunks ending at or before lo
+ *   1 chunk-aligned  s = floor(max(0, n-W+1) / C), lo = s*C, hi = n;  c < s
+ *                    (no token between the summaries and the window)
+ *   2 blocked        lo = floor(n/W)*W, hi = n;  chunks ending at or before lo
+ *   3 non-causal     lo = floor(n/W)*W, hi = min(L, lo+W) - 1;  chunks ending
+ *                    at or before lo and chunks starting after hi
+ * Summary logits carry + ln C as in eva_ref_attend_row. */
+void eva_ref_attend_row_variant(const double* q, const double* K, const double* V,
+                                const double* Ksum, const double* Vsum,
+                                long n, long L, int d, long W, long C, int variant, double* o)
+{
+    double inv_sqrt_d = 1.0 / sqrt((double)d);
+    long n_chunks = L / C;
+    long lo, hi;
+    if (variant == 0) {
+        lo = n - W + 1 < 0 ? 0 : n - W + 1;
+        hi = n;
+    } else if (variant == 1) {
+        long start = n - W + 1 < 0 ? 0 : n - W + 1;
+        lo = (start / C) * C;
+        hi = n;
+    } else if (variant == 2) {
+        lo = (n / W) * W;
+        hi = n;
+    } else {
+        lo = (n / W) * W;
+        hi = lo + W - 1 < L - 1 ? lo + W - 1 : L - 1;
+    }
+    /* chunk c is summarized iff it lies wholly before lo, or (non-causal)
+     * wholly after hi */
+    char* take = (char*)calloc((size_t)(n_chunks > 0 ? n_chunks : 1), 1);
+    long n_take = 0;
+    for (long c = 0; c < n_chunks; ++c) {
+        int before = (c + 1) * C <= lo;
+        int after = variant == 3 && c * C > hi;
+        take[c] = (char)(before || after);
+        n_take += take[c];
+    }
+    long count = (hi - lo + 1) + n_take;
+    double* logit = (double*)malloc((size_t)count * sizeof(double));
+    const double** val = (const double**)malloc((size_t)count * sizeof(double*));
+    long i = 0;
+    for (long m = lo; m <= hi; ++m, ++i) {
+        double s = 0.0;
+        for (int e = 0; e < d; ++e) s += q[e] * K[(size_t)m * d + e];
+        logit[i] = s * inv_sqrt_d;
+        val[i] = V + (size_t)m * d;
+    }
+    for (long c = 0; c < n_chunks; ++c) {
+        if (!take[c]) continue;
+        double s = 0.0;
+        for (int e = 0; e < d; ++e) s += q[e] * Ksum[(size_t)c * d + e];
+        logit[i] = s * inv_sqrt_d + log((double)C);
+        val[i] = Vsum + (size_t)c * d;
+        ++i;
+    }
+    double lmax = -INFINITY;
+    for (i = 0; i < count; ++i)
+        if (logit[i] > lmax) lmax = logit[i];
+    double den = 0.0;
+    for (i = 0; i < count; ++i) den += exp(logit[i] - lmax);
+    for (int e = 0; e < d; ++e) {
+        double num = 0.0;
+        for (i = 0; i < count; ++i) num += exp(logit[i] - lmax) * val[i][e];
+        o[e] = num / den;
+    }
+    free(take);
+    free(logit);
+    free(val);
+}
+
+void eva_ref_attend_rows_variant(const double* Qrows, const long* rows, long n_rows,
+                                 const double* K, const double* V,
+                                 const double* Ksum, const double* Vsum,
+                                 long L, int d, long W, long C, int variant, double* Orows)
+{
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (long r = 0; r < n_rows; ++r)
+        eva_ref_attend_row_variant(Qrows + (size_t)r * d, K, V, Ksum, Vsum, rows[r], L, d, W, C, variant,
+                                   Orows + (size_t)r * d);
+}
+
 void eva_ref_attend_rows(const double* Qrows, const long* rows, long n_rows,
                          const double* K, const double* V,
                          const double* Ksum, const double* Vsum,
@@ -210,6 +298,32 @@ void eva_ref_attend_rows(const double* Qrows, const long* rows, long n_rows,
 
 /* Whole prefill: summaries of every (b, kv head), then every row of every
  * query head.  Ksum/Vsum receive [B][Hkv][floor(L/C)][d]. */
+/* Whole prefill with a window variant (see eva_ref_attend_row_variant). */
+void eva_ref_prefill_variant(const double* Q, const double* K, const double* V, double* O,
+                             int B, int H, int Hkv, long L, int d, long W, long C, int variant,
+                             double* Ksum, double* Vsum)
+{
+    int G = H / Hkv;
+    long n_chunks = L / C;
+    size_t seq = (size_t)L * d;
+    size_t sseq = (size_t)n_chunks * d;
+
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (long bg = 0; bg < (long)B * Hkv; ++bg)
+        eva_ref_summaries(K + bg * seq, V + bg * seq, L, d, C, Ksum + bg * sseq, Vsum + bg * sseq);
+
+    #pragma omp parallel for collapse(2) schedule(dynamic, 16)
+    for (long bh = 0; bh < (long)B * H; ++bh) {
+        for (long n = 0; n < L; ++n) {
+            long b = bh / H, h = bh % H;
+            long bg = b * Hkv + h / G;
+            eva_ref_attend_row_variant(Q + bh * seq + (size_t)n * d, K + bg * seq, V + bg * seq,
+                                       Ksum + bg * sseq, Vsum + bg * sseq, n, L, d, W, C, variant,
+                                       O + bh * seq + (size_t)n * d);
+        }
+    }
+}
+
 void eva_ref_prefill(const double* Q, const double* K, const double* V, double* O,
                      int B, int H, int Hkv, long L, int d, long W, long C,
                      double* Ksum, double* Vsum)

@@ -378,3 +378,93 @@ def test_rf_summary_noise_direction():
     eps[0, 0] = -3.0
     _, vs = oracle.summaries_rf(k, v, eps, C, lam=40.0)
     assert vs[0, 0] > 0.999
+
+
+# ---------------------------------------------------------------------------
+# Window variants (ablation "EVA Local Window Attention Variants"; the
+# non-causal form of section "FlashEVA")
+# ---------------------------------------------------------------------------
+
+VARIANTS = (oracle.SLIDING, oracle.CHUNK_ALIGNED, oracle.BLOCKED, oracle.NONCAUSAL)
+
+
+def test_sliding_variant_is_the_main_definition():
+    B, H, Hkv, L, d, W, C = 1, 2, 1, 90, 8, 13, 5
+    q, k, v = rand((B, H, L, d), 60), rand((B, Hkv, L, d), 61), rand((B, Hkv, L, d), 62)
+    np.testing.assert_array_equal(oracle.prefill_variant(q, k, v, W, C, oracle.SLIDING), oracle.prefill(q, k, v, W, C))
+
+
+@pytest.mark.parametrize("variant", [oracle.CHUNK_ALIGNED, oracle.BLOCKED])
+@pytest.mark.parametrize("W,C", [(7, 1), (40, 3), (50, 50)])
+def test_causal_variants_reduce_to_exact_attention(variant, W, C):
+    # C = 1 (every summary is its token) or W >= L (no summaries): causal
+    # softmax attention.
+    B, H, Hkv, L, d = 1, 2, 2, 40, 8
+    q, k, v = rand((B, H, L, d), 63), rand((B, Hkv, L, d), 64), rand((B, Hkv, L, d), 65)
+    o = oracle.prefill_variant(q, k, v, W, C, variant)
+    if C == 1 or W >= L:
+        np.testing.assert_allclose(o, sdpa(q, k, v, causal=True), rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,C", [(7, 1), (40, 3), (41, 41)])
+def test_noncausal_reduces_to_full_attention(W, C):
+    B, H, Hkv, L, d = 1, 2, 2, 40, 8
+    q, k, v = rand((B, H, L, d), 66), rand((B, Hkv, L, d), 67), rand((B, Hkv, L, d), 68)
+    o = oracle.prefill_variant(q, k, v, W, C, oracle.NONCAUSAL)
+    if C == 1 or W >= L:
+        np.testing.assert_allclose(o, sdpa(q, k, v, causal=False), rtol=1e-11, atol=1e-12)
+
+
+def equal_key_outputs(L, W, C, variant, seed):
+    # all keys equal: every attended item has logit q.k/sqrt(d) (+ ln C for a
+    # summary, whose value is its chunk's mean), so the output is the plain
+    # mean over the attended tokens
+    d = 4
+    k = np.tile(rand((1, 1, 1, d), seed), (1, 1, L, 1))
+    q = rand((1, 1, L, d), seed + 1)
+    v = rand((1, 1, L, d), seed + 2)
+    return oracle.prefill_variant(q, k, v, W, C, variant)[0, 0], v[0, 0]
+
+
+@pytest.mark.parametrize("L,W,C", [(60, 10, 4), (33, 5, 7), (50, 1, 3)])
+def test_chunk_aligned_has_no_gap(L, W, C):
+    # window + summaries cover exactly tokens 0..n
+    o, v = equal_key_outputs(L, W, C, oracle.CHUNK_ALIGNED, 69)
+    for n in range(L):
+        np.testing.assert_allclose(o[n], v[:n + 1].mean(axis=0), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("L,W,C", [(60, 12, 4), (61, 9, 3), (50, 10, 4)])
+def test_blocked_window_token_sets(L, W, C):
+    # row n: its block [floor(n/W) W, n] and the chunks ending at or before
+    # the block start
+    o, v = equal_key_outputs(L, W, C, oracle.BLOCKED, 70)
+    for n in range(L):
+        lo = (n // W) * W
+        toks = list(range((lo // C) * C)) + list(range(lo, n + 1))
+        np.testing.assert_allclose(o[n], v[toks].mean(axis=0), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("L,W,C", [(60, 12, 4), (61, 9, 3), (50, 10, 4), (23, 30, 5)])
+def test_noncausal_token_sets(L, W, C):
+    # row n: its whole block and every complete chunk wholly outside it
+    o, v = equal_key_outputs(L, W, C, oracle.NONCAUSAL, 71)
+    for n in range(L):
+        lo = (n // W) * W
+        hi = min(L, lo + W) - 1
+        toks = set(range(lo, hi + 1))
+        for c in range(L // C):
+            if (c + 1) * C <= lo or c * C > hi:
+                toks.update(range(c * C, (c + 1) * C))
+        np.testing.assert_allclose(o[n], v[sorted(toks)].mean(axis=0), rtol=1e-12, atol=1e-13)
+
+
+def test_noncausal_rows_of_a_block_share_keys():
+    # the attended set depends only on the block: equal queries inside a
+    # block give equal outputs, and changing a token of another block that
+    # lies in a summarized chunk changes them all alike
+    L, W, C, d = 48, 12, 4, 8
+    q, k, v = rand((1, 1, L, d), 72), rand((1, 1, L, d), 73), rand((1, 1, L, d), 74)
+    q[0, 0, 12:24] = q[0, 0, 12]
+    o = oracle.prefill_variant(q, k, v, W, C, oracle.NONCAUSAL)[0, 0]
+    np.testing.assert_allclose(o[12:24], np.tile(o[12], (12, 1)), rtol=1e-13, atol=1e-14)
