@@ -55,12 +55,36 @@ def attended(L, W, C):
     return int((w + s).sum())
 
 
+def attended_variant(L, W, C, variant):
+    """sum_n (exact keys + summaries) attended by row n under a window variant
+    (0 sliding, 1 chunk-aligned, 2 blocked, 3 non-causal blocks)."""
+    import numpy as np
+    n = np.arange(L, dtype=np.int64)
+    if variant == 0:
+        lo, hi = np.maximum(0, n - W + 1), n
+    elif variant == 1:
+        lo, hi = (np.maximum(0, n - W + 1) // C) * C, n
+    else:
+        lo = (n // W) * W
+        hi = np.minimum(L, lo + W) - 1 if variant == 3 else n
+    n_chunks = L // C
+    s = lo // C
+    if variant == 3:
+        s = s + np.maximum(0, n_chunks - (hi // C + 1))
+    return int((hi - lo + 1 + s).sum())
+
+
 def prefill_counts(B, H, Hkv, L, d, W, C, e):
     nc = L // C
     flops = B * H * 4 * d * attended(L, W, C)
     attn_bytes = (2 * B * H * L * d + 2 * B * Hkv * L * d + 2 * B * Hkv * nc * d) * e
     summ_bytes = (2 * B * Hkv * L * d + 2 * B * Hkv * nc * d) * e
     return flops, attn_bytes, summ_bytes
+
+
+def attn_bytes_of(B, H, Hkv, L, d, C, e):
+    """Q + K + V + Ksum + Vsum reads and O write of the fused kernel."""
+    return (2 * B * H * L * d + 2 * B * Hkv * L * d + 2 * B * Hkv * (L // C) * d) * e
 
 
 def decode_counts(B, H, Hkv, d, W, C, p, e):
@@ -202,6 +226,23 @@ def main():
 
     ms_summ, ms_attn, ms_fill_app, ms_dec = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
 
+    # window variants of the fused kernel on the same inputs (summaries as built)
+    variants = {}
+    for var, name in ((1, "chunk_aligned"), (2, "blocked"), (3, "noncausal")):
+        eva.prefill_attention(q, k, v, Ks, Vs, W, C, out=O, window=var)
+        v0 = torch.cuda.Event(enable_timing=True)
+        v1 = torch.cuda.Event(enable_timing=True)
+        n_var = max(args.steps, 1)
+        v0.record()
+        for _ in range(n_var):
+            eva.prefill_attention(q, k, v, Ks, Vs, W, C, out=O, window=var)
+        v1.record()
+        torch.cuda.synchronize()
+        ms_v = v0.elapsed_time(v1) / n_var
+        fl = B * H * 4 * d * attended_variant(L, W, C, var)
+        variants[name] = {"attention_ms": ms_v, "alg_flops": fl, "tflops": fl / (ms_v * 1e-3) / 1e12,
+                          "hbm_gbs": attn_bytes_of(B, H, Hkv, L, d, C, 2) / (ms_v * 1e-3) / 1e9}
+
     # stochastic random-feature summaries of the same K, V (one noise draw
     # per chunk, read once more: + n_chunks * d * 4 bytes per (b, kv head))
     eps = torch.randn(B, Hkv, L // C, d, device=dev)
@@ -245,6 +286,7 @@ def main():
         "prefill": {"attention_ms": ms_attn, "attention_tflops": attn_tflops,
                     "attention_mfma_frac": attn_tflops / PEAK_BF16_TFLOPS,
                     "summaries_ms": ms_summ, "summaries_gbs": summ_bytes / (ms_summ * 1e-3) / 1e9,
+                    "window_variants": variants,
                     "summaries_rf_ms": ms_summ_rf,
                     "summaries_rf_gbs": (summ_bytes + B * Hkv * (L // C) * d * 4) / (ms_summ_rf * 1e-3) / 1e9,
                     "fill_append_ms": ms_fill_app, "decode_ms": ms_dec,

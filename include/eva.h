@@ -64,6 +64,30 @@ typedef enum {
 typedef enum { EVA_BF16 = 0, EVA_F32 = 1 } eva_dtype;
 
 /*
+ * Local-window variants (the ablation "EVA Local Window Attention Variants"
+ * compares the original EVA's blocked local windows with the sliding window
+ * of section "FlashEVA"; that section also names the non-causal form).  Row n
+ * attends the exact keys [lo, hi] and the summaries of the complete chunks
+ * lying wholly outside them on the side(s) listed:
+ *   EVA_WINDOW_SLIDING        lo = max(0, n-W+1), hi = n; chunks before lo.
+ *                             The default, and what the functions without
+ *                             a window argument compute.
+ *   EVA_WINDOW_CHUNK_ALIGNED  the sliding start moved down to the start of
+ *                             its chunk: lo = s(n) C with s(n) as above, so
+ *                             no token falls between summaries and window.
+ *   EVA_WINDOW_BLOCKED        lo = floor(n/W) W, hi = n; chunks before lo.
+ *   EVA_WINDOW_NONCAUSAL      the whole block: lo = floor(n/W) W,
+ *                             hi = min(L, lo+W) - 1; chunks before lo and
+ *                             after hi.  Prefill only (no decode cache).
+ */
+typedef enum {
+    EVA_WINDOW_SLIDING = 0,
+    EVA_WINDOW_CHUNK_ALIGNED = 1,
+    EVA_WINDOW_BLOCKED = 2,
+    EVA_WINDOW_NONCAUSAL = 3
+} eva_window;
+
+/*
  * Decode cache: the state one decoded token needs — the exact keys/values of
  * the window and the chunk summaries (FlashEVA keeps a compressed cache whose
  * size grows with the number of chunks, not tokens).
@@ -80,11 +104,13 @@ typedef enum { EVA_BF16 = 0, EVA_F32 = 1 } eva_dtype;
  *   vt_sum   [B][H_kv][S_max/32][d][32] summary values, tiled the same way
  * Requirements: R >= W + C - 1 and R a multiple of 32; S_max a multiple of 32.
  * n_tok counts the tokens the cache has absorbed (the same for every
- * sequence of the batch); the library updates it.
+ * sequence of the batch); the library updates it.  `window` is the causal
+ * window variant the cache serves (any eva_window but EVA_WINDOW_NONCAUSAL).
  */
 typedef struct eva_cache {
     int B, H, H_kv, d, W, C;
     int dtype;        /* eva_dtype */
+    int window;       /* eva_window, causal */
     int R;            /* ring slots per (b, kv head) */
     int S_max;        /* summary capacity per (b, kv head) */
     long long n_tok;  /* tokens held; host-side state */
@@ -159,6 +185,19 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
                           void* stream);
 
 /*
+ * eva_prefill_attention and eva_prefill with a window variant (eva_window).
+ * A cache passed to eva_prefill_ex must carry the same window; the
+ * non-causal variant takes none.
+ * Errors: as the functions without the argument; INVALID for an unknown
+ * window or a cache with the non-causal variant or another window.
+ */
+int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                             void* O, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, int window,
+                             void* stream);
+int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d,
+                   int W, int C, int dtype, int window, void* Ksum, void* Vsum, eva_cache* cache, void* stream);
+
+/*
  * Load a decode cache from a prefilled sequence of L tokens: the last
  * min(L, R) keys/values go to ring slots p mod R and the L / C summaries
  * (as built by eva_build_summaries) to the summary arrays; n_tok becomes L.
@@ -229,6 +268,7 @@ size_t eva_decode_workspace_bytes(const eva_cache* cache);
 typedef struct eva_rcache {
     int B, H, H_kv, d, W, C;
     int dtype;        /* eva_dtype; decode needs EVA_BF16 */
+    int window;       /* eva_window, causal */
     int R;
     int S_max;
     int max_tok;

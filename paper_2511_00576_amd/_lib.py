@@ -16,6 +16,10 @@ EVA_ERR_CAPACITY = -3
 EVA_ERR_HIP = -4
 EVA_BF16 = 0
 EVA_F32 = 1
+EVA_WINDOW_SLIDING = 0
+EVA_WINDOW_CHUNK_ALIGNED = 1
+EVA_WINDOW_BLOCKED = 2
+EVA_WINDOW_NONCAUSAL = 3
 
 # Every entry point include/eva.h declares.
 SYMBOLS = (
@@ -23,6 +27,8 @@ SYMBOLS = (
     "eva_build_summaries_rf",
     "eva_prefill",
     "eva_prefill_attention",
+    "eva_prefill_attention_ex",
+    "eva_prefill_ex",
     "eva_cache_fill",
     "eva_cache_append",
     "eva_decode_step",
@@ -41,8 +47,8 @@ SYMBOLS = (
 class EvaCacheStruct(ctypes.Structure):
     _fields_ = [
         ("B", ctypes.c_int), ("H", ctypes.c_int), ("H_kv", ctypes.c_int), ("d", ctypes.c_int),
-        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("R", ctypes.c_int),
-        ("S_max", ctypes.c_int), ("n_tok", ctypes.c_longlong),
+        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("window", ctypes.c_int),
+        ("R", ctypes.c_int), ("S_max", ctypes.c_int), ("n_tok", ctypes.c_longlong),
         ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
         ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
     ]
@@ -51,8 +57,8 @@ class EvaCacheStruct(ctypes.Structure):
 class EvaRCacheStruct(ctypes.Structure):
     _fields_ = [
         ("B", ctypes.c_int), ("H", ctypes.c_int), ("H_kv", ctypes.c_int), ("d", ctypes.c_int),
-        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("R", ctypes.c_int),
-        ("S_max", ctypes.c_int), ("max_tok", ctypes.c_int),
+        ("W", ctypes.c_int), ("C", ctypes.c_int), ("dtype", ctypes.c_int), ("window", ctypes.c_int),
+        ("R", ctypes.c_int), ("S_max", ctypes.c_int), ("max_tok", ctypes.c_int),
         ("n_tok", ctypes.c_void_p), ("arrive", ctypes.c_void_p),
         ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
         ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
@@ -81,6 +87,10 @@ def load():
     lib.eva_prefill.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_prefill_attention.restype = i
     lib.eva_prefill_attention.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    lib.eva_prefill_attention_ex.restype = i
+    lib.eva_prefill_attention_ex.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp]
+    lib.eva_prefill_ex.restype = i
+    lib.eva_prefill_ex.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_cache_fill.restype = i
     lib.eva_cache_fill.argtypes = [cp, vp, vp, vp, vp, i, vp]
     lib.eva_cache_append.restype = i

@@ -191,8 +191,8 @@ __device__ inline DecodeGeom decode_geom(const DecodeParams& a, int b, bool& val
         g.fresh = APPEND && n < a.max_tok;
         g.p = g.fresh ? n : n - 1;
         valid = g.p >= 0 && !(a.active && a.active[b] == 0);
-        g.win_lo = max(0, g.p - a.c.W + 1);
-        g.n_sum = min(g.win_lo / a.c.C, a.c.S_max);  // s(p)
+        g.win_lo = win_lo_rt(a.c.window, g.p, a.c.W, a.c.C);
+        g.n_sum = min(g.win_lo / a.c.C, a.c.S_max);  // chunks wholly before the window
         g.n_sum_chunks = (g.n_sum + 31) / 32;
         g.first_win_chunk = g.win_lo / 32;
         g.n_win_chunks = g.p / 32 - g.first_win_chunk + 1;

@@ -23,10 +23,27 @@ int supported(int d, int dtype) {
     return EVA_OK;
 }
 
-int visible_summaries(long long n, long long W, long long C) {
-    long long start = n - W + 1;
-    return start > 0 ? (int)(start / C) : 0;
+// Window variants (eva_window): first exact key of row n, and the number of
+// summaries that lie wholly before it.  Non-causal rows also see chunks
+// after their block (not needed by the decode path, which is causal).
+long long window_lo(int window, long long n, long long W, long long C) {
+    switch (window) {
+        case EVA_WINDOW_CHUNK_ALIGNED: return (n - W + 1 > 0 ? (n - W + 1) / C : 0) * C;
+        case EVA_WINDOW_BLOCKED:
+        case EVA_WINDOW_NONCAUSAL: return (n / W) * W;
+        default: return n - W + 1 > 0 ? n - W + 1 : 0;
+    }
 }
+int prefix_summaries(int window, long long n, long long W, long long C) {
+    return (int)(window_lo(window, n, W, C) / C);
+}
+// Whether any row of a sequence of L tokens can see a summary (then the
+// summary pointers must be valid).
+bool any_summary(int window, long long L, long long W, long long C) {
+    if (window == EVA_WINDOW_NONCAUSAL) return L / C > 0;
+    return prefix_summaries(window, L - 1, W, C) > 0;
+}
+bool valid_window(int window) { return window >= EVA_WINDOW_SLIDING && window <= EVA_WINDOW_NONCAUSAL; }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? EVA_OK : EVA_ERR_HIP; }
 
@@ -53,6 +70,7 @@ int check_cache(const eva_cache* c) {
     if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
         return EVA_ERR_INVALID;
     if (c->n_tok < 0) return EVA_ERR_INVALID;
+    if (!valid_window(c->window) || c->window == EVA_WINDOW_NONCAUSAL) return EVA_ERR_INVALID;
     if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
     if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
     if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
@@ -69,6 +87,7 @@ eva::CacheView view_of(const eva_cache* c) {
     v.R = c->R;
     v.S_max = c->S_max;
     v.n_tok = c->n_tok;
+    v.window = c->window;
     v.k_ring = c->k_ring;
     v.vt_ring = c->vt_ring;
     v.k_sum = c->k_sum;
@@ -105,6 +124,7 @@ int check_rcache(const eva_rcache* c) {
     if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
         return EVA_ERR_INVALID;
     if (c->max_tok < 1) return EVA_ERR_INVALID;
+    if (!valid_window(c->window) || c->window == EVA_WINDOW_NONCAUSAL) return EVA_ERR_INVALID;
     if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
     if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
     // summaries are built as chunks complete: up to max_tok / C of them
@@ -123,6 +143,7 @@ eva::CacheView rview_of(const eva_rcache* c) {
     v.R = c->R;
     v.S_max = c->S_max;
     v.n_tok = 0;  // per-sequence counts live in device memory
+    v.window = c->window;
     v.k_ring = c->k_ring;
     v.vt_ring = c->vt_ring;
     v.k_sum = c->k_sum;
@@ -137,9 +158,11 @@ eva::RaggedState rstate_of(const eva_rcache* c, const int* active) {
 // Most 32-row chunks a decode row of a ragged cache can touch: the summaries
 // of a sequence at max_tok tokens plus a window starting anywhere in a tile.
 int rdecode_max_chunks(const eva_rcache* c) {
-    int n_sum = visible_summaries(c->max_tok - 1, c->W, c->C);
+    int n_sum = prefix_summaries(c->window, c->max_tok - 1, c->W, c->C);
     if (n_sum > c->S_max) n_sum = c->S_max;
-    const int win = c->W < c->max_tok ? c->W : c->max_tok;
+    // longest window: W, or W + C - 1 when extended down to its chunk
+    long long w = c->window == EVA_WINDOW_CHUNK_ALIGNED ? (long long)c->W + c->C - 1 : c->W;
+    const int win = (int)(w < c->max_tok ? w : c->max_tok);
     return (n_sum + 31) / 32 + (win + 30) / 32 + 1;
 }
 
@@ -149,8 +172,8 @@ int completed_chunk(long long p, int C) { return (p + 1) % C == 0 ? (int)((p + 1
 
 int decode_chunks(const eva_cache* c, long long p, int* n_sum_out, int* win_lo_out, int* n_sum_chunks,
                   int* n_win_chunks) {
-    const int n_sum = visible_summaries(p, c->W, c->C);
-    const long long win_lo = p - c->W + 1 > 0 ? p - c->W + 1 : 0;
+    const int n_sum = prefix_summaries(c->window, p, c->W, c->C);
+    const long long win_lo = window_lo(c->window, p, c->W, c->C);
     *n_sum_out = n_sum;
     *win_lo_out = (int)win_lo;
     *n_sum_chunks = (n_sum + 31) / 32;
@@ -211,14 +234,22 @@ int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float
 
 int eva_prefill_attention(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
                           int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream) {
+    return eva_prefill_attention_ex(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, EVA_WINDOW_SLIDING,
+                                    stream);
+}
+
+int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                             void* O, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, int window,
+                             void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (!valid_window(window)) return EVA_ERR_INVALID;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
     if (!Q || !K || !V || !O) return EVA_ERR_INVALID;
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return EVA_ERR_INVALID;
     const int n_chunks = L / C;
-    // a row sees summaries only when some chunk lies fully before its window
-    if (visible_summaries(L - 1, W, C) > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum)))
+    // a row sees summaries only when some chunk lies wholly outside its window
+    if (any_summary(window, L, W, C) && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum)))
         return EVA_ERR_INVALID;
 
     eva::PrefillParams p;
@@ -251,6 +282,7 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
     p.n_tiles = (int)tiles;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
+    p.window = window;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
         if constexpr (std::is_same<decltype(t), eva::bf16>::value)
@@ -281,7 +313,14 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
 
 int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
                 int C, int dtype, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
+    return eva_prefill_ex(Q, K, V, O, B, H, H_kv, L, d, W, C, dtype, EVA_WINDOW_SLIDING, Ksum, Vsum, cache, stream);
+}
+
+int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
+                   int C, int dtype, int window, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (!valid_window(window)) return EVA_ERR_INVALID;
+    if (cache && window == EVA_WINDOW_NONCAUSAL) return EVA_ERR_INVALID;  // no causal decode to feed
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
     if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
@@ -294,13 +333,13 @@ int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int
         st = check_cache(cache);
         if (st != EVA_OK) return st;
         if (cache->B != B || cache->H != H || cache->H_kv != H_kv || cache->d != d || cache->W != W ||
-            cache->C != C || cache->dtype != dtype)
+            cache->C != C || cache->dtype != dtype || cache->window != window)
             return EVA_ERR_INVALID;
         if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
     }
     st = eva_build_summaries(K, V, Ksum, Vsum, B, H_kv, L, d, C, dtype, stream);
     if (st != EVA_OK) return st;
-    st = eva_prefill_attention(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, stream);
+    st = eva_prefill_attention_ex(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, window, stream);
     if (st != EVA_OK) return st;
     if (cache) return eva_cache_fill(cache, K, V, Ksum, Vsum, L, stream);
     return EVA_OK;

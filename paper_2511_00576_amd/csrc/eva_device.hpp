@@ -104,4 +104,43 @@ __device__ __forceinline__ int visible_summaries(int n, int W, int C) {
     return start > 0 ? start / C : 0;
 }
 
+// Window variants (values of the ABI's eva_window).  Row n attends the exact
+// keys [win_lo(n), win_hi(n)] and the summaries of the complete chunks
+// c < sum_lo(n) (those ending at or before win_lo) and, non-causal only,
+// c >= sum_hi(n) (those starting after win_hi).  All four are non-decreasing
+// in n.
+constexpr int kWinSliding = 0;       // [n-W+1, n]
+constexpr int kWinChunkAligned = 1;  // sliding start rounded down to its chunk
+constexpr int kWinBlocked = 2;       // [floor(n/W) W, n]
+constexpr int kWinNonCausal = 3;     // the whole block [floor(n/W) W, +W)
+
+template <int VAR>
+__device__ __forceinline__ int win_lo(int n, int W, int C) {
+    if constexpr (VAR == kWinSliding) return max(0, n - W + 1);
+    if constexpr (VAR == kWinChunkAligned) return (max(0, n - W + 1) / C) * C;
+    return (n / W) * W;
+}
+template <int VAR>
+__device__ __forceinline__ int win_hi(int n, int W, int L) {
+    if constexpr (VAR == kWinNonCausal) return min(L, (n / W) * W + W) - 1;
+    return n;
+}
+template <int VAR>
+__device__ __forceinline__ int sum_lo(int n, int W, int C) {
+    return win_lo<VAR>(n, W, C) / C;
+}
+template <int VAR>
+__device__ __forceinline__ int sum_hi(int n, int W, int C, int L) {
+    return win_hi<VAR>(n, W, L) / C + 1;
+}
+
+// Runtime-variant forms (decode geometry).
+__device__ __forceinline__ int win_lo_rt(int variant, int n, int W, int C) {
+    switch (variant) {
+        case kWinChunkAligned: return win_lo<kWinChunkAligned>(n, W, C);
+        case kWinBlocked: return win_lo<kWinBlocked>(n, W, C);
+        default: return win_lo<kWinSliding>(n, W, C);
+    }
+}
+
 }  // namespace eva

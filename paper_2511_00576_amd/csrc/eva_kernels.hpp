@@ -34,6 +34,7 @@ struct PrefillParams {
     int n_tiles;      // B * Hkv * n_hg * n_pos_tiles
     float scale_log2; // log2(e) / sqrt(d)
     float log2C;      // log2(C): the ln C summary offset in log2 units
+    int window;       // window variant (kWin* in eva_device.hpp)
 };
 
 template <int D, typename T>
@@ -51,6 +52,7 @@ hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, in
 
 struct CacheView {
     int B, H, Hkv, W, C, R, S_max;
+    int window;  // causal window variant (kWinSliding / kWinChunkAligned / kWinBlocked)
     long long n_tok;
     void* k_ring;
     void* vt_ring;

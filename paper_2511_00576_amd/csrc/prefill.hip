@@ -87,7 +87,9 @@ __device__ __forceinline__ void lds_dma16(const void* base, unsigned voff, const
     asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(m0) : "memory");
 }
 
-template <int D, typename T, int NW, int NS>
+// VAR: window variant (win_lo / win_hi / sum_lo / sum_hi); masks of edge
+// blocks are per element for every variant.
+template <int D, typename T, int NW, int NS, int VAR>
 __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
     typedef PCfg<D, T, NW> Cfg;
     constexpr bool BF = Cfg::BF;
@@ -122,18 +124,26 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
     const int p0 = n0 + (wave / a.Gt) * kQW;
     const int n_hi = min(n0 + a.pos_per_wg - 1, L - 1);
 
-    // blocks the workgroup stages: summaries [0, s(n_hi)), then the window band
-    const int s_hi = visible_summaries(n_hi, W, C);
+    // blocks the workgroup stages: summaries [0, s(n_hi)) (non-causal: all),
+    // then the window band
+    constexpr bool NC = VAR == kWinNonCausal;
+    const int s_hi = NC ? a.n_chunks : sum_lo<VAR>(n_hi, W, C);
     const int nsb = (s_hi + kBN - 1) / kBN;
-    const int kb0 = max(0, n0 - W + 1) / kBN;
-    const int kb1 = n_hi / kBN;
+    const int kb0 = win_lo<VAR>(n0, W, C) / kBN;
+    const int kb1 = win_hi<VAR>(n_hi, W, L) / kBN;
     const int nb = nsb + (kb1 - kb0 + 1);
 
-    // what this wave needs
+    // what this wave needs: prefix summaries c < ws_hi (all columns: c < ws_lo),
+    // non-causal suffix summaries c >= wsx_lo (all columns: c >= wsx_hi), and
+    // window keys in [wlo_min, whi_max] (all columns: [wlo_max, whi_min])
     const bool w_active = p0 < L;
     const int wp_last = min(p0 + kQW - 1, L - 1);
-    const int ws_hi = w_active ? visible_summaries(wp_last, W, C) : 0;
-    const int ws_lo = visible_summaries(p0, W, C);
+    const int ws_hi = w_active ? sum_lo<VAR>(wp_last, W, C) : 0;
+    const int ws_lo = sum_lo<VAR>(p0, W, C);
+    const int wsx_lo = NC ? sum_hi<VAR>(p0, W, C, L) : 0;
+    const int wsx_hi = NC ? sum_hi<VAR>(wp_last, W, C, L) : 0;
+    const int wlo_min = win_lo<VAR>(p0, W, C), wlo_max = win_lo<VAR>(wp_last, W, C);
+    const int whi_min = win_hi<VAR>(p0, W, L), whi_max = win_hi<VAR>(wp_last, W, L);
 
     const size_t bg = (size_t)b * a.Hkv + kvh;
     const T* Kbg = static_cast<const T*>(a.K) + bg * (size_t)L * D;
@@ -143,11 +153,15 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
     const size_t bh = (size_t)b * a.H + h;
 
     // per-column facts (column = query position p0 + cb*16 + c16)
-    int col_n[2], col_s[2];
+    int col_n[2], col_s[2], col_sx[2], col_lo[2], col_span[2];
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
         col_n[cb] = p0 + cb * 16 + c16;
-        col_s[cb] = visible_summaries(col_n[cb], W, C);
+        const int n = min(col_n[cb], L - 1);
+        col_s[cb] = sum_lo<VAR>(n, W, C);
+        col_sx[cb] = NC ? sum_hi<VAR>(n, W, C, L) : a.n_chunks;
+        col_lo[cb] = win_lo<VAR>(n, W, C);
+        col_span[cb] = win_hi<VAR>(n, W, L) - col_lo[cb];
     }
 
     // ---- Q fragments (B operand of S^T = K Q^T) ----
@@ -257,11 +271,12 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
         is_sum = j < nsb;
         base = is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
         if (is_sum) {
-            needed = base < ws_hi;
-            full = base + kBN - 1 < ws_lo;
+            const int last = base + kBN - 1;
+            needed = base < ws_hi || (NC && w_active && last >= wsx_lo && base < a.n_chunks);
+            full = last < ws_lo || (NC && base >= wsx_hi && last < a.n_chunks);
         } else {
-            needed = w_active && base <= wp_last && base + kBN - 1 >= p0 - W + 1;
-            full = base >= wp_last - W + 1 && base + kBN - 1 <= p0;
+            needed = w_active && base <= whi_max && base + kBN - 1 >= wlo_min;
+            full = base >= wlo_max && base + kBN - 1 <= whi_min;
         }
     };
 
@@ -415,23 +430,30 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
                 if (is_sum) {
 #pragma unroll
                     for (int cb = 0; cb < 2; ++cb) {
-                        const int lim = col_s[cb] - base - g * 4;  // valid iff kb*16 + i < lim
-#pragma unroll
-                        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                s[kb][cb][i] = (kb * 16 + i < lim) ? s[kb][cb][i] : -INFINITY;
-                    }
-                } else {
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) {
-                        const int rel = col_n[cb] - base - g * 4;  // n - key = rel - (kb*16 + i)
+                        // summary x = base + 4g + kb*16 + i valid iff x < s(n), or
+                        // (non-causal) sum_hi(n) <= x < n_chunks
+                        const int lim = col_s[cb] - base - g * 4;
+                        const int lim_x = col_sx[cb] - base - g * 4;
+                        const int lim_n = a.n_chunks - base - g * 4;
 #pragma unroll
                         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                             for (int i = 0; i < 4; ++i) {
-                                const unsigned dist = (unsigned)(rel - (kb * 16 + i));  // valid iff 0 <= n-key < W
-                                s[kb][cb][i] = dist < (unsigned)W ? s[kb][cb][i] : -INFINITY;
+                                const int x = kb * 16 + i;
+                                const bool ok = x < lim || (NC && x >= lim_x && x < lim_n);
+                                s[kb][cb][i] = ok ? s[kb][cb][i] : -INFINITY;
+                            }
+                    }
+                } else {
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb) {
+                        const int rel = base + g * 4 - col_lo[cb];  // key - win_lo(n) = rel + kb*16 + i
+#pragma unroll
+                        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const unsigned dist = (unsigned)(rel + kb * 16 + i);  // valid iff lo <= key <= hi
+                                s[kb][cb][i] = dist <= (unsigned)col_span[cb] ? s[kb][cb][i] : -INFINITY;
                             }
                     }
                 }
@@ -538,14 +560,20 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
 
 }  // namespace
 
+template <int D, typename T, int VAR>
+void launch_prefill_var(const PrefillParams& p, hipStream_t stream) {
+    constexpr int NS = sizeof(T) == 2 ? 4 : 2;
+    hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, NS, VAR>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
+                       stream, p);
+}
+
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
-    if constexpr (sizeof(T) == 2) {
-        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 4>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
-                           stream, p);
-    } else {
-        hipLaunchKernelGGL((prefill_kernel<D, T, kPrefillWaves, 2>), dim3(p.n_tiles), dim3(kPrefillWaves * 64), 0,
-                           stream, p);
+    switch (p.window) {
+        case kWinChunkAligned: launch_prefill_var<D, T, kWinChunkAligned>(p, stream); break;
+        case kWinBlocked: launch_prefill_var<D, T, kWinBlocked>(p, stream); break;
+        case kWinNonCausal: launch_prefill_var<D, T, kWinNonCausal>(p, stream); break;
+        default: launch_prefill_var<D, T, kWinSliding>(p, stream); break;
     }
     return hipGetLastError();
 }

@@ -32,6 +32,13 @@
 // tile: the pattern depends only on the lane and on W mod 16, the choice per
 // tile only on wave-uniform offsets.  Summary blocks straddling s(n) are
 // masked per element.
+//
+// Window variants (template VAR, see win_lo / win_hi / sum_lo / sum_hi): the
+// block plan and the per-wave block classification follow each row's window
+// [win_lo(n), win_hi(n)] and summary ranges; the sliding window keeps the bias
+// patterns, the other variants test window blocks per element as well.  The
+// non-causal variant stages every summary block (its rows see the chunks on
+// both sides of their block).
 #include <type_traits>
 
 #include "eva_device.hpp"
@@ -95,7 +102,7 @@ __device__ __forceinline__ int lower_state(int c) { return c >= 16 ? 0 : (c < 0 
 // e = e1 (>= 0) or e = e1 - 16 (< 0), e1 = (W - 1) mod 16.
 __device__ __forceinline__ int upper_state(int e) { return e >= 15 ? 0 : (e < -15 ? 1 : (e >= 0 ? 2 : 3)); }
 
-template <int D, int NW, int NCB, int NS, int BN, int WPE>
+template <int D, int NW, int NCB, int NS, int BN, int WPE, int VAR>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void prefill_mfma_kernel(PrefillParams a) {
     typedef MCfg<D, NW, NCB, NS, BN> Cfg;
@@ -132,16 +139,24 @@ void prefill_mfma_kernel(PrefillParams a) {
     const int p0 = n0 + (wave / a.Gt) * CW;
     const int n_hi = min(n0 + a.pos_per_wg - 1, L - 1);
 
-    // blocks the workgroup stages: summaries [0, s(n_hi)), then the window band
-    const int nsb = (visible_summaries(n_hi, W, C) + kBN - 1) / kBN;
-    const int kb0 = max(0, n0 - W + 1) / kBN;
-    const int nb = nsb + (n_hi / kBN - kb0 + 1);
+    // blocks the workgroup stages: summaries [0, s(n_hi)) (non-causal: all),
+    // then the window band
+    constexpr bool NC = VAR == kWinNonCausal;
+    const int nsb = ((NC ? a.n_chunks : sum_lo<VAR>(n_hi, W, C)) + kBN - 1) / kBN;
+    const int kb0 = win_lo<VAR>(n0, W, C) / kBN;
+    const int nb = nsb + (win_hi<VAR>(n_hi, W, L) / kBN - kb0 + 1);
 
-    // what this wave needs
+    // what this wave needs: prefix summaries c < ws_hi (all columns: c < ws_lo),
+    // non-causal suffix summaries c >= wsx_lo (all columns: c >= wsx_hi), and
+    // window keys in [wlo_min, whi_max] (all columns: [wlo_max, whi_min])
     const bool w_active = p0 < L;
     const int wp_last = min(p0 + CW - 1, L - 1);
-    const int ws_hi = w_active ? visible_summaries(wp_last, W, C) : 0;
-    const int ws_lo = visible_summaries(p0, W, C);
+    const int ws_hi = w_active ? sum_lo<VAR>(wp_last, W, C) : 0;
+    const int ws_lo = sum_lo<VAR>(p0, W, C);
+    const int wsx_lo = NC ? sum_hi<VAR>(p0, W, C, L) : 0;
+    const int wsx_hi = NC ? sum_hi<VAR>(wp_last, W, C, L) : 0;
+    const int wlo_min = win_lo<VAR>(p0, W, C), wlo_max = win_lo<VAR>(wp_last, W, C);
+    const int whi_min = win_hi<VAR>(p0, W, L), whi_max = win_hi<VAR>(wp_last, W, L);
 
     // ---- request plan.  Block j's rows come from the summaries (j < nsb) or
     // from the window band; with the band's base pointer shifted back by nsb
@@ -207,7 +222,7 @@ void prefill_mfma_kernel(PrefillParams a) {
 
     // ---- bias patterns: pattern (lo, up) at lane (g, c16), element i is the
     //      mask of query c16 vs key 4g + i of a tile with the given edge states
-    if (wave == 0) {
+    if (VAR == kWinSliding && wave == 0) {
         const int e1 = (W - 1) & 15;
 #pragma unroll
         for (int p = 0; p < kNPat; ++p) {
@@ -292,11 +307,12 @@ void prefill_mfma_kernel(PrefillParams a) {
         k.is_sum = j < nsb;
         k.base = k.is_sum ? j * kBN : (kb0 + j - nsb) * kBN;
         if (k.is_sum) {
-            k.needed = k.base < ws_hi;
-            k.full = k.base + kBN - 1 < ws_lo;
+            const int last = k.base + kBN - 1;
+            k.needed = k.base < ws_hi || (NC && w_active && last >= wsx_lo && k.base < a.n_chunks);
+            k.full = last < ws_lo || (NC && k.base >= wsx_hi && last < a.n_chunks);
         } else {
-            k.needed = w_active && k.base <= wp_last && k.base + kBN - 1 >= p0 - W + 1;
-            k.full = k.base >= wp_last - W + 1 && k.base + kBN - 1 <= p0;
+            k.needed = w_active && k.base <= whi_max && k.base + kBN - 1 >= wlo_min;
+            k.full = k.base >= wlo_max && k.base + kBN - 1 <= whi_min;
         }
         return k;
     };
@@ -324,15 +340,45 @@ void prefill_mfma_kernel(PrefillParams a) {
         }
     };
     // summary block straddling s(n): key base + kb*16 + 4g + i valid iff < s(n)
+    // (non-causal: or in [sum_hi(n), n_chunks))
     auto mask_sum = [&](floatx4 (&sc)[NKB][NCB], int base) {
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
-            const int lim = visible_summaries(col_n(cb), W, C) - base - g * 4;
+            const int n = min(col_n(cb), L - 1);
+            const int lim = sum_lo<VAR>(n, W, C) - base - g * 4;
+            const int lim_x = (NC ? sum_hi<VAR>(n, W, C, L) : 0) - base - g * 4;
+            const int lim_n = a.n_chunks - base - g * 4;
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sc[kb][cb][i] = (kb * 16 + i < lim) ? sc[kb][cb][i] : -INFINITY;
+                for (int i = 0; i < 4; ++i) {
+                    const int x = kb * 16 + i;
+                    const bool ok = x < lim || (NC && x >= lim_x && x < lim_n);
+                    sc[kb][cb][i] = ok ? sc[kb][cb][i] : -INFINITY;
+                }
         }
+    };
+    // window block crossing an edge, variants other than sliding: key
+    // base + kb*16 + 4g + i valid iff win_lo(n) <= key <= win_hi(n)
+    auto mask_win = [&](floatx4 (&sc)[NKB][NCB], int base) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            const int n = min(col_n(cb), L - 1);
+            const int lo = win_lo<VAR>(n, W, C);
+            const unsigned span = (unsigned)(win_hi<VAR>(n, W, L) - lo);
+            const int rel0 = base + g * 4 - lo;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    sc[kb][cb][i] = (unsigned)(rel0 + kb * 16 + i) <= span ? sc[kb][cb][i] : -INFINITY;
+        }
+    };
+    auto mask_window = [&](floatx4 (&sc)[NKB][NCB], int base) {
+        if constexpr (VAR == kWinSliding)
+            add_bias(sc, base);
+        else
+            mask_win(sc, base);
     };
     // lazy maximum update once the scores of a block are known; returns
     // whether the accumulators must be rescaled by alpha
@@ -402,7 +448,7 @@ void prefill_mfma_kernel(PrefillParams a) {
         }
         if (kc.needed) {
             if (kc.is_sum && !kc.full) mask_sum(s0, kc.base);
-            if (!kc.is_sum && !kc.full) add_bias(s0, kc.base);
+            if (!kc.is_sum && !kc.full) mask_window(s0, kc.base);
             lane_max(s0);
             update_max(kc.is_sum ? a.log2C : 0.f);  // acc is zero: no rescale owed
         }
@@ -538,7 +584,7 @@ void prefill_mfma_kernel(PrefillParams a) {
                 if (kn.is_sum)
                     mask_sum(sn, kn.base);
                 else
-                    add_bias(sn, kn.base);
+                    mask_window(sn, kn.base);
                 lane_max(sn);
             }
             pending = update_max(kn.is_sum ? a.log2C : 0.f);
@@ -576,16 +622,26 @@ void prefill_mfma_kernel(PrefillParams a) {
 
 }  // namespace
 
-template <int D>
-hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
+template <int D, int VAR>
+void launch_prefill_mfma_var(const PrefillParams& p, hipStream_t stream) {
     if (prefill_mfma_narrow(p.G)) {
         // 4 waves x 32 columns, 32-key blocks: 77 KB of LDS, two workgroups per CU
-        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2>), dim3(p.n_tiles),
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2, VAR>), dim3(p.n_tiles),
                            dim3(kMfmaWavesNarrow * 64), 0, stream, p);
     } else {
         // 8 waves x 32 columns, 64-key blocks: 141 KB of LDS, one workgroup per CU
-        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesWide, kMfmaColBlocks, 4, 64, 2>), dim3(p.n_tiles),
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesWide, kMfmaColBlocks, 4, 64, 2, VAR>), dim3(p.n_tiles),
                            dim3(kMfmaWavesWide * 64), 0, stream, p);
+    }
+}
+
+template <int D>
+hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
+    switch (p.window) {
+        case kWinChunkAligned: launch_prefill_mfma_var<D, kWinChunkAligned>(p, stream); break;
+        case kWinBlocked: launch_prefill_mfma_var<D, kWinBlocked>(p, stream); break;
+        case kWinNonCausal: launch_prefill_mfma_var<D, kWinNonCausal>(p, stream); break;
+        default: launch_prefill_mfma_var<D, kWinSliding>(p, stream); break;
     }
     return hipGetLastError();
 }

@@ -85,7 +85,7 @@ class Cache:
     """
 
     def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None,
-                 fill=None):
+                 fill=None, window=_lib.EVA_WINDOW_SLIDING):
         if R is None:
             R = -(-(W + C - 1) // 32) * 32
         S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
@@ -96,9 +96,10 @@ class Cache:
         self.k_sum = mk(B, Hkv, S_max, d)
         self.vt_sum = mk(B, Hkv, S_max // 32, d, 32)
         self.dtype = dtype
-        self.struct = _lib.EvaCacheStruct(B, H, Hkv, d, W, C, _DTYPES[dtype], R, S_max, 0,
-                                          self.k_ring.data_ptr(), self.vt_ring.data_ptr(),
-                                          self.k_sum.data_ptr(), self.vt_sum.data_ptr())
+        self.struct = _lib.EvaCacheStruct(B=B, H=H, H_kv=Hkv, d=d, W=W, C=C, dtype=_DTYPES[dtype], window=window,
+                                          R=R, S_max=S_max, n_tok=0, k_ring=self.k_ring.data_ptr(),
+                                          vt_ring=self.vt_ring.data_ptr(), k_sum=self.k_sum.data_ptr(),
+                                          vt_sum=self.vt_sum.data_ptr())
         self._ws = None
 
     @property
@@ -123,8 +124,10 @@ class Cache:
         return self._ws
 
 
-def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool = False):
-    """EVA prefill. Q [B, H, L, d]; K, V [B, Hkv, L, d] -> O [B, H, L, d]."""
+def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool = False,
+            window: int = _lib.EVA_WINDOW_SLIDING):
+    """EVA prefill. Q [B, H, L, d]; K, V [B, Hkv, L, d] -> O [B, H, L, d].
+    `window`: one of the EVA_WINDOW_* variants."""
     _require_device(Q, K, V)
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
@@ -136,15 +139,15 @@ def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool
     Vs = torch.empty_like(Ks)
     lib = _lib.load()
     cref = ctypes.byref(cache.struct) if cache is not None else None
-    _lib.check("eva_prefill",
-               lib.eva_prefill(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C, _dtype_code(Q),
-                               _ptr(Ks) if n_chunks else None, _ptr(Vs) if n_chunks else None, cref, _stream()))
+    _lib.check("eva_prefill_ex",
+               lib.eva_prefill_ex(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C, _dtype_code(Q), window,
+                                  _ptr(Ks) if n_chunks else None, _ptr(Vs) if n_chunks else None, cref, _stream()))
     if return_summaries:
         return O, Ks, Vs
     return O
 
 
-def prefill_attention(Q, K, V, Ks, Vs, W: int, C: int, out=None):
+def prefill_attention(Q, K, V, Ks, Vs, W: int, C: int, out=None, window: int = _lib.EVA_WINDOW_SLIDING):
     """The fused window + summary attention alone, given summaries from
     build_summaries(K, V, C). Q [B, H, L, d] -> O [B, H, L, d]."""
     _require_device(Q, K, V)
@@ -156,9 +159,9 @@ def prefill_attention(Q, K, V, Ks, Vs, W: int, C: int, out=None):
         raise ValueError("summaries must be [B, Hkv, L // C, d]")
     O = torch.empty_like(Q) if out is None else out
     _require_device(O)
-    _lib.check("eva_prefill_attention",
-               _lib.load().eva_prefill_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), _ptr(O), B, H, Hkv,
-                                                 L, d, W, C, _dtype_code(Q), _stream()))
+    _lib.check("eva_prefill_attention_ex",
+               _lib.load().eva_prefill_attention_ex(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks), _ptr(Vs), _ptr(O), B, H,
+                                                    Hkv, L, d, W, C, _dtype_code(Q), window, _stream()))
     return O
 
 
@@ -221,7 +224,8 @@ class RaggedCache:
     `n_tok` [B] (int32) and the library's arrival counters live on the device,
     so steps need no host-side state.  `max_tokens` bounds every sequence."""
 
-    def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None, fill=None):
+    def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None, fill=None,
+                 window=_lib.EVA_WINDOW_SLIDING):
         if R is None:
             R = -(-(W + C - 1) // 32) * 32
         S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
@@ -234,10 +238,11 @@ class RaggedCache:
         self.n_tok = torch.zeros(B, dtype=torch.int32, device=device)
         self.arrive = torch.zeros(B, dtype=torch.int32, device=device)
         self.dtype = dtype
-        self.struct = _lib.EvaRCacheStruct(B, H, Hkv, d, W, C, _DTYPES[dtype], R, S_max, max_tokens,
-                                           self.n_tok.data_ptr(), self.arrive.data_ptr(),
-                                           self.k_ring.data_ptr(), self.vt_ring.data_ptr(),
-                                           self.k_sum.data_ptr(), self.vt_sum.data_ptr())
+        self.struct = _lib.EvaRCacheStruct(B=B, H=H, H_kv=Hkv, d=d, W=W, C=C, dtype=_DTYPES[dtype], window=window,
+                                           R=R, S_max=S_max, max_tok=max_tokens, n_tok=self.n_tok.data_ptr(),
+                                           arrive=self.arrive.data_ptr(), k_ring=self.k_ring.data_ptr(),
+                                           vt_ring=self.vt_ring.data_ptr(), k_sum=self.k_sum.data_ptr(),
+                                           vt_sum=self.vt_sum.data_ptr())
         n = _lib.load().eva_rdecode_workspace_bytes(ctypes.byref(self.struct))
         self.ws = torch.empty((n + 3) // 4, dtype=torch.float32, device=device) if n else None
 

@@ -73,11 +73,10 @@ def test_prefill_rejects(lib, kw, code):
 
 
 def make_cache(**kw):
-    a = dict(B=1, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, R=32, S_max=32, n_tok=0,
+    a = dict(B=1, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, window=0, R=32, S_max=32, n_tok=0,
              k_ring=0x10000, vt_ring=0x20000, k_sum=0x30000, vt_sum=0x40000)
     a.update(kw)
-    return _lib.EvaCacheStruct(a["B"], a["H"], a["H_kv"], a["d"], a["W"], a["C"], a["dtype"], a["R"], a["S_max"],
-                               a["n_tok"], a["k_ring"], a["vt_ring"], a["k_sum"], a["vt_sum"])
+    return _lib.EvaCacheStruct(**a)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -147,12 +146,10 @@ def test_summaries_rejects(lib):
 
 
 def make_rcache(**kw):
-    a = dict(B=2, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, R=32, S_max=32, max_tok=100,
+    a = dict(B=2, H=4, H_kv=2, d=64, W=8, C=4, dtype=_lib.EVA_BF16, window=0, R=32, S_max=32, max_tok=100,
              n_tok=0x50000, arrive=0x60000, k_ring=0x10000, vt_ring=0x20000, k_sum=0x30000, vt_sum=0x40000)
     a.update(kw)
-    return _lib.EvaRCacheStruct(a["B"], a["H"], a["H_kv"], a["d"], a["W"], a["C"], a["dtype"], a["R"], a["S_max"],
-                                a["max_tok"], a["n_tok"], a["arrive"], a["k_ring"], a["vt_ring"], a["k_sum"],
-                                a["vt_sum"])
+    return _lib.EvaRCacheStruct(**a)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -223,3 +220,23 @@ def test_summaries_rf_rejects(lib):
     assert call(C=0) == _lib.EVA_ERR_INVALID
     # fewer tokens than one chunk: nothing to do, no pointer needed
     assert call(K=None, V=None, eps=None, Ks=None, Vs=None, L=3) == _lib.EVA_OK
+
+
+@pytest.mark.parametrize("window,code", [(4, _lib.EVA_ERR_INVALID), (-1, _lib.EVA_ERR_INVALID)])
+def test_prefill_rejects_unknown_window(lib, window, code):
+    f = lib.eva_prefill_attention_ex
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 64, 64, 8, 4, 0, window, None) == code
+
+
+def test_noncausal_takes_no_cache(lib):
+    c = make_cache(window=_lib.EVA_WINDOW_NONCAUSAL)
+    assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_INVALID
+    c = make_cache()
+    assert lib.eva_prefill_ex(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 64, 64, 8, 4, 0, _lib.EVA_WINDOW_NONCAUSAL, FAKE, FAKE,
+                              ctypes.byref(c), None) == _lib.EVA_ERR_INVALID
+    # a cache of another window variant
+    c = make_cache(window=_lib.EVA_WINDOW_BLOCKED)
+    assert lib.eva_prefill_ex(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 64, 64, 8, 4, 0, _lib.EVA_WINDOW_SLIDING, FAKE, FAKE,
+                              ctypes.byref(c), None) == _lib.EVA_ERR_INVALID
+    r = make_rcache(window=_lib.EVA_WINDOW_NONCAUSAL)
+    assert lib.eva_rcache_append(ctypes.byref(r), FAKE, FAKE, None, None) == _lib.EVA_ERR_INVALID

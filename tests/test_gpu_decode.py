@@ -24,13 +24,16 @@ def _gpu():
     eva._lib.load()
 
 
-def oracle_row(qrow, K, V, p, W, C):
+def oracle_row(qrow, K, V, p, W, C, window=oracle.SLIDING):
     """Oracle output of the query at position p; K, V hold positions 0..p."""
     Ks, Vs = oracle.summaries(K[: p + 1], V[: p + 1], C)
-    return oracle.attend_rows(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C)[0]
+    if window == oracle.SLIDING:
+        return oracle.attend_rows(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C)[0]
+    return oracle.attend_rows_variant(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C, window)[0]
 
 
-def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1, fused=False):
+def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1, fused=False,
+                 window=oracle.SLIDING):
     """Prefill L0 tokens (if L0 > 0) into a cache, then append + decode `steps`
     tokens (two calls, or the fused call); compare every `check_every`-th
     decode output with the oracle."""
@@ -39,10 +42,10 @@ def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, ch
     dtype = torch.bfloat16
     total = L0 + steps
     q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
-    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=total, dtype=dtype, fill=fill)
+    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=total, dtype=dtype, fill=fill, window=window)
     if L0 > 0:
         eva.prefill(q[:, :, :L0].contiguous().cuda(), k[:, :, :L0].contiguous().cuda(),
-                    v[:, :, :L0].contiguous().cuda(), W, C, cache=cache)
+                    v[:, :, :L0].contiguous().cuda(), W, C, cache=cache, window=window)
         assert cache.n_tok == L0
     k64, v64 = to64(k), to64(v)
     worst = 0.0
@@ -62,7 +65,7 @@ def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, ch
         for b in range(B):
             for h in range(H):
                 g = h // (H // Hkv)
-                ref = oracle_row(to64(q[b, h, p]), k64[b, g], v64[b, g], p, W, C)
+                ref = oracle_row(to64(q[b, h, p]), k64[b, g], v64[b, g], p, W, C, window)
                 worst = max(worst, assert_parity(got[b, h][None], ref[None], dtype, f"p={p} b{b} h{h}"))
     return cache
 
@@ -106,6 +109,14 @@ def test_decode_head_groupings(H, Hkv):
 def test_decode_split_and_unsplit(use_ws, fused):
     # B * Hkv = 2 units: with a workspace the rows are split over many workgroups
     run_sequence(1, 8, 2, 128, 512, 64, L0=3000, steps=3, seed=26, use_ws=use_ws, fused=fused)
+
+
+@pytest.mark.parametrize("window", [oracle.CHUNK_ALIGNED, oracle.BLOCKED])
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_window_variants(window, fused):
+    # window / summary sets of the causal variants across chunk completions,
+    # block starts and ring wraps (R = 96 for W = 64, C = 16)
+    run_sequence(1, 8, 2, 128, 64, 16, L0=150, steps=140, seed=32, check_every=3, fused=fused, window=window)
 
 
 def test_fused_step_equals_two_calls():

@@ -43,12 +43,12 @@ def padded_prefill_inputs(q, k, v, lens, seed):
     return q[:, :, :L].contiguous(), K.contiguous(), V.contiguous()
 
 
-def load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=None):
+def load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=None, window=oracle.SLIDING):
     B, H, _, d = q.shape
     Hkv = k.shape[1]
     Qp, Kp, Vp = (t.cuda() for t in padded_prefill_inputs(q, k, v, lens, seed))
-    cache = eva.RaggedCache(B, H, Hkv, d, W, C, max_tokens=max_tokens, dtype=q.dtype, fill=fill)
-    _, Ks, Vs = eva.prefill(Qp, Kp, Vp, W, C, return_summaries=True)
+    cache = eva.RaggedCache(B, H, Hkv, d, W, C, max_tokens=max_tokens, dtype=q.dtype, fill=fill, window=window)
+    _, Ks, Vs = eva.prefill(Qp, Kp, Vp, W, C, return_summaries=True, window=window)
     eva.rcache_fill(cache, Kp, Vp, Ks, Vs, torch.tensor(lens, dtype=torch.int32, device="cuda"))
     return cache
 
@@ -56,8 +56,8 @@ def load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=None):
 class SequenceOracle:
     """Oracle rows of sequence b over its own tokens k[b], v[b] (by position)."""
 
-    def __init__(self, q, k, v, W, C):
-        self.q, self.W, self.C = q, W, C
+    def __init__(self, q, k, v, W, C, window=oracle.SLIDING):
+        self.q, self.W, self.C, self.window = q, W, C, window
         self.G = q.shape[1] // k.shape[1]
         self.kv = {}
         self.k, self.v = k, v
@@ -73,7 +73,16 @@ class SequenceOracle:
         pos = np.asarray(positions, dtype=np.int64)
         if qrows is None:
             qrows = self.q[b, h, torch.from_numpy(pos)]
-        return oracle.attend_rows(to64(qrows), pos, *self.kv_of(b, h // self.G), self.W, self.C)
+        if self.window == oracle.SLIDING:
+            return oracle.attend_rows(to64(qrows), pos, *self.kv_of(b, h // self.G), self.W, self.C)
+        # causal variants: the summaries of the tokens up to the row suffice
+        K64, V64, _, _ = self.kv_of(b, h // self.G)
+        out = []
+        for r, p in enumerate(pos):
+            Ks, Vs = oracle.summaries(K64[: p + 1], V64[: p + 1], self.C)
+            out.append(oracle.attend_rows_variant(to64(qrows[r:r + 1]), pos[r:r + 1], K64[: p + 1], V64[: p + 1],
+                                                  Ks, Vs, self.W, self.C, self.window)[0])
+        return np.stack(out)
 
 
 def step_inputs(q, k, v, pos):
@@ -84,16 +93,16 @@ def step_inputs(q, k, v, pos):
 
 
 def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, use_ws=True, max_tokens=None,
-              check_every=1, fused=False):
+              check_every=1, fused=False, window=oracle.SLIDING):
     print(f"ragged B{B} H{H}/{Hkv} d{d} W{W} C{C} lens={lens} steps={steps} fill={fill} ws={use_ws} "
           f"fused={fused}", flush=True)
     total = max(lens) + steps
     q, k, v = inputs.qkv(B, H, Hkv, total, d, torch.bfloat16, seed=seed)
     if max_tokens is None:
         max_tokens = total
-    cache = load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=fill)
+    cache = load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=fill, window=window)
     assert cache.n_tok.cpu().tolist() == [min(n, max_tokens) for n in lens]
-    orc = SequenceOracle(q, k, v, W, C)
+    orc = SequenceOracle(q, k, v, W, C, window)
     n = [min(x, max_tokens) for x in lens]
     sentinel = torch.full((B, H, d), 7.0, dtype=torch.bfloat16, device="cuda")
     for t in range(steps):
@@ -151,6 +160,11 @@ def test_ragged_generation_split_and_unsplit(use_ws, fused):
     # B * Hkv = 2 units: with the workspace the rows split over many workgroups
     run_steps(2, 8, 1, 128, 256, 32, lens=[1500, 700], steps=40, seed=44, use_ws=use_ws, check_every=13,
               fused=fused)
+
+
+@pytest.mark.parametrize("window", [oracle.CHUNK_ALIGNED, oracle.BLOCKED])
+def test_ragged_window_variants(window):
+    run_steps(3, 8, 2, 128, 48, 16, lens=[60, 130, 7], steps=70, seed=50, check_every=3, fused=True, window=window)
 
 
 def test_ragged_window_of_one():

@@ -153,6 +153,60 @@ def test_prefill_with_rf_summaries():
             assert_parity(to64(O[b, h, torch.from_numpy(rows)]), ref, dtype, f"rf prefill b{b} h{h}")
 
 
+# ---- window variants ----
+VARIANTS = [oracle.CHUNK_ALIGNED, oracle.BLOCKED, oracle.NONCAUSAL]
+VARIANT_SHAPES = [
+    # B, H, Hkv, L, d, W, C
+    (1, 2, 2, 300, 64, 40, 16),     # G = 1: 4-wave configuration
+    (2, 8, 2, 517, 128, 64, 24),    # G = 4: 8-wave configuration, ragged tail
+    (1, 4, 4, 700, 128, 100, 7),    # odd chunk, window not a multiple of 16
+    (1, 2, 1, 250, 128, 1, 5),      # W = 1
+    (1, 2, 2, 120, 64, 200, 16),    # W >= L
+    (1, 16, 2, 400, 128, 96, 32),   # G = 8: two head groups per kv head
+]
+
+
+def check_variant(B, H, Hkv, L, d, W, C, dtype, variant, seed, maker=inputs.qkv):
+    print(f"variant {variant} B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C} {dtype} {maker.__name__}", flush=True)
+    q, k, v = maker(B, H, Hkv, L, d, dtype=dtype, seed=seed)
+    O = eva.prefill(*cuda(q, k, v), W, C, window=variant)
+    torch.cuda.synchronize()
+    ref = oracle.prefill_variant(q, k, v, W, C, variant)
+    assert_parity(to64(O), ref, dtype, f"variant {variant}")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", VARIANT_SHAPES)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_prefill_variants(variant, shape, dtype):
+    check_variant(*shape, dtype, variant, seed=30)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_prefill_variant_mask_probe(variant, dtype):
+    # one-hot values make a token wrongly in or out cost far more than the
+    # bf16 tolerance
+    check_variant(1, 4, 2, 1500, 128, 96, 16, dtype, variant, seed=31, maker=inputs.needle_qkv)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("w", [inputs.LLM_BF16, inputs.GQA_BF16], ids=lambda w: w.name.split()[0])
+def test_prefill_variant_full_size_sampled(variant, w):
+    print(f"full-size {w.name} variant {variant}", flush=True)
+    q, k, v = inputs.workload_qkv(w)
+    O = eva.prefill(*cuda(q, k, v), w.W, w.C, window=variant)
+    torch.cuda.synchronize()
+    rows = edge_rows(w.L, w.W, w.C, extra=24, seed=variant)
+    rows = np.unique(np.concatenate([rows, np.arange(0, w.L, w.W), np.arange(w.W - 1, w.L, w.W)]))
+    for b, h in ((0, 0), (w.B - 1, w.H - 1)):
+        g = h // (w.H // w.Hkv)
+        Ks, Vs = oracle.summaries(k[b, g], v[b, g], w.C)
+        ref = oracle.attend_rows_variant(to64(q[b, h, torch.from_numpy(rows)]), rows, k[b, g], v[b, g], Ks, Vs,
+                                         w.W, w.C, variant)
+        assert_parity(to64(O[b, h, torch.from_numpy(rows)]), ref, w.dtype, f"{w.name} variant {variant} b{b} h{h}")
+
+
 FULL = [inputs.LLM_BF16, inputs.GQA_BF16, inputs.LONG_BF16]
 
 
