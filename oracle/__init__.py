@@ -49,6 +49,9 @@ def _load():
     lib.eva_ref_prefill.restype = None
     lib.eva_ref_prefill.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_long, ctypes.c_int, ctypes.c_long, ctypes.c_long, _dp, _dp]
+    lib.eva_ref_backward_group.restype = None
+    lib.eva_ref_backward_group.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
+                                           ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
     lib.eva_ref_num_threads.restype = ctypes.c_int
     lib.eva_ref_num_threads.argtypes = []
     _lib = lib
@@ -166,3 +169,30 @@ def prefill_variant(Q, K, V, W: int, C: int, variant: int):
     _load().eva_ref_prefill_variant(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, H, Hkv, L, d, W, C, int(variant),
                                     _ptr(Ks), _ptr(Vs))
     return O
+
+
+def backward(Q, K, V, dO, W: int, C: int):
+    """Gradients of the EVA prefill (sliding window): Q, dO [B, H, L, d];
+    K, V [B, Hkv, L, d] -> (dQ, dK, dV) in fp64, for the loss whose gradient
+    with respect to O is dO."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    G = H // Hkv
+    dQ = np.zeros_like(Q)
+    dK = np.zeros_like(K)
+    dV = np.zeros_like(V)
+    lib = _load()
+    for b in range(B):
+        for g in range(Hkv):
+            q = np.ascontiguousarray(Q[b, g * G:(g + 1) * G])
+            go = np.ascontiguousarray(dO[b, g * G:(g + 1) * G])
+            dq = np.zeros_like(q)
+            dk = np.zeros((L, d))
+            dv = np.zeros((L, d))
+            lib.eva_ref_backward_group(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])), _ptr(np.ascontiguousarray(V[b, g])),
+                                       _ptr(go), G, L, d, W, C, _ptr(dq), _ptr(dk), _ptr(dv))
+            dQ[b, g * G:(g + 1) * G] = dq
+            dK[b, g] = dk
+            dV[b, g] = dv
+    return dQ, dK, dV

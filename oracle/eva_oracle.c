@@ -350,6 +350,144 @@ void eva_ref_prefill(const double* Q, const double* K, const double* V, double* 
 }
 
 /* Threads the OpenMP runtime will use (1 when built without OpenMP). */
+/* Backward pass of the EVA prefill for one kv group: G query heads sharing
+ * K, V.  Given dO (the gradient of a loss with respect to O), returns dQ,
+ * dK, dV of that loss, through the window keys and values, the summary keys
+ * and values, and the summaries' own dependence on K and V (the mean key and
+ * the softmax(mean . k / sqrt(d))-weighted value).
+ *   Q, dO, dQ: [G][L][d];  K, V, dK, dV: [L][d]  (dK, dV are overwritten).
+ * Plain chain rule, row by row: with p the row's softmax over its items
+ * (keys key_i, values val_i), o = sum_i p_i val_i and D = dO . o,
+ *   dlogit_i = p_i (dO . val_i - D),  dq = sum_i dlogit_i key_i / sqrt(d),
+ *   dkey_i += dlogit_i q / sqrt(d),   dval_i += p_i dO;
+ * then for each chunk (a_j = khat . k_j / sqrt(d), b = softmax(a)):
+ *   dv_j += b_j dvhat,  da_j = b_j (dvhat . v_j - dvhat . vhat),
+ *   dkhat = dkey_c + sum_j da_j k_j / sqrt(d),
+ *   dk_j += da_j khat / sqrt(d) + dkhat / C.
+ * The + ln C logit offset is a constant. */
+void eva_ref_backward_group(const double* Q, const double* K, const double* V, const double* dO,
+                            int G, long L, int d, long W, long C,
+                            double* dQ, double* dK, double* dV)
+{
+    double inv_sqrt_d = 1.0 / sqrt((double)d);
+    long n_chunks = L / C;
+    size_t nc1 = (size_t)(n_chunks > 0 ? n_chunks : 1);
+    double* Ks = (double*)calloc(nc1 * d, sizeof(double));
+    double* Vs = (double*)calloc(nc1 * d, sizeof(double));
+    double* dKs = (double*)calloc(nc1 * d, sizeof(double));
+    double* dVs = (double*)calloc(nc1 * d, sizeof(double));
+    eva_ref_summaries(K, V, L, d, C, Ks, Vs);
+    memset(dK, 0, (size_t)L * d * sizeof(double));
+    memset(dV, 0, (size_t)L * d * sizeof(double));
+
+    double* logit = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    double* p = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    double* o = (double*)malloc((size_t)d * sizeof(double));
+    for (int h = 0; h < G; ++h) {
+        for (long n = 0; n < L; ++n) {
+            const double* q = Q + ((size_t)h * L + n) * d;
+            const double* g = dO + ((size_t)h * L + n) * d;
+            double* dq = dQ + ((size_t)h * L + n) * d;
+            long lo = n - W + 1 < 0 ? 0 : n - W + 1;
+            long n_win = n - lo + 1;
+            long n_sum = eva_ref_visible_summaries(n, W, C);
+            long count = n_win + n_sum;
+            /* forward of the row: items 0..n_win-1 are keys lo..n, then summaries */
+            double lmax = -INFINITY;
+            for (long i = 0; i < count; ++i) {
+                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                double s = 0.0;
+                for (int e = 0; e < d; ++e) s += q[e] * key[e];
+                logit[i] = s * inv_sqrt_d + (i < n_win ? 0.0 : log((double)C));
+                if (logit[i] > lmax) lmax = logit[i];
+            }
+            double den = 0.0;
+            for (long i = 0; i < count; ++i) {
+                p[i] = exp(logit[i] - lmax);
+                den += p[i];
+            }
+            for (long i = 0; i < count; ++i) p[i] /= den;
+            for (int e = 0; e < d; ++e) {
+                double acc = 0.0;
+                for (long i = 0; i < count; ++i) {
+                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                    acc += p[i] * val[e];
+                }
+                o[e] = acc;
+            }
+            double D = 0.0;
+            for (int e = 0; e < d; ++e) D += g[e] * o[e];
+            /* backward of the row */
+            for (int e = 0; e < d; ++e) dq[e] = 0.0;
+            for (long i = 0; i < count; ++i) {
+                const int win = i < n_win;
+                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                double* dkey = win ? dK + (size_t)(lo + i) * d : dKs + (size_t)(i - n_win) * d;
+                double* dval = win ? dV + (size_t)(lo + i) * d : dVs + (size_t)(i - n_win) * d;
+                double gv = 0.0;
+                for (int e = 0; e < d; ++e) gv += g[e] * val[e];
+                const double dl = p[i] * (gv - D);
+                for (int e = 0; e < d; ++e) {
+                    dq[e] += dl * key[e] * inv_sqrt_d;
+                    dkey[e] += dl * q[e] * inv_sqrt_d;
+                    dval[e] += p[i] * g[e];
+                }
+            }
+        }
+    }
+    /* through the summaries */
+    double* a = (double*)malloc((size_t)C * sizeof(double));
+    double* b = (double*)malloc((size_t)C * sizeof(double));
+    double* dkh = (double*)malloc((size_t)d * sizeof(double));
+    for (long c = 0; c < n_chunks; ++c) {
+        const double* Kc = K + (size_t)c * C * d;
+        const double* Vc = V + (size_t)c * C * d;
+        const double* kh = Ks + (size_t)c * d;
+        const double* vh = Vs + (size_t)c * d;
+        const double* gk = dKs + (size_t)c * d;
+        const double* gvh = dVs + (size_t)c * d;
+        double amax = -INFINITY;
+        for (long j = 0; j < C; ++j) {
+            double s = 0.0;
+            for (int e = 0; e < d; ++e) s += kh[e] * Kc[(size_t)j * d + e];
+            a[j] = s * inv_sqrt_d;
+            if (a[j] > amax) amax = a[j];
+        }
+        double den = 0.0;
+        for (long j = 0; j < C; ++j) {
+            b[j] = exp(a[j] - amax);
+            den += b[j];
+        }
+        for (long j = 0; j < C; ++j) b[j] /= den;
+        double gvh_vh = 0.0;
+        for (int e = 0; e < d; ++e) gvh_vh += gvh[e] * vh[e];
+        for (int e = 0; e < d; ++e) dkh[e] = gk[e];
+        for (long j = 0; j < C; ++j) {
+            double gv = 0.0;
+            for (int e = 0; e < d; ++e) gv += gvh[e] * Vc[(size_t)j * d + e];
+            const double da = b[j] * (gv - gvh_vh);
+            for (int e = 0; e < d; ++e) {
+                dV[((size_t)c * C + j) * d + e] += b[j] * gvh[e];
+                dkh[e] += da * Kc[(size_t)j * d + e] * inv_sqrt_d;
+                dK[((size_t)c * C + j) * d + e] += da * kh[e] * inv_sqrt_d;
+            }
+        }
+        for (long j = 0; j < C; ++j)
+            for (int e = 0; e < d; ++e) dK[((size_t)c * C + j) * d + e] += dkh[e] / (double)C;
+    }
+    free(a);
+    free(b);
+    free(dkh);
+    free(logit);
+    free(p);
+    free(o);
+    free(Ks);
+    free(Vs);
+    free(dKs);
+    free(dVs);
+}
+
 int eva_ref_num_threads(void)
 {
 #ifdef _OPENMP

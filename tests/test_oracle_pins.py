@@ -468,3 +468,53 @@ def test_noncausal_rows_of_a_block_share_keys():
     q[0, 0, 12:24] = q[0, 0, 12]
     o = oracle.prefill_variant(q, k, v, W, C, oracle.NONCAUSAL)[0, 0]
     np.testing.assert_allclose(o[12:24], np.tile(o[12], (12, 1)), rtol=1e-13, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Backward pass (the paper benchmarks forward + backward, section "FlashEVA
+# Attention speedup"; training runs the kernels both ways)
+# ---------------------------------------------------------------------------
+
+def numeric_grad(f, x, h=1e-5):
+    g = np.zeros_like(x)
+    it = np.nditer(x, flags=["multi_index"])
+    for _ in it:
+        i = it.multi_index
+        old = x[i]
+        x[i] = old + h
+        up = f()
+        x[i] = old - h
+        dn = f()
+        x[i] = old
+        g[i] = (up - dn) / (2 * h)
+    return g
+
+
+@pytest.mark.parametrize("L,W,C", [(11, 4, 2), (13, 3, 4), (9, 20, 3), (12, 1, 2)])
+def test_backward_matches_finite_differences(L, W, C):
+    # loss = sum(O * R) for a fixed R: dO = R; every gradient of Q, K, V
+    # (through window, summary keys/values and the summaries' own K, V
+    # dependence) against central differences of the forward
+    B, H, Hkv, d = 1, 2, 1, 3
+    q, k, v = rand((B, H, L, d), 80), rand((B, Hkv, L, d), 81), rand((B, Hkv, L, d), 82)
+    R = rand((B, H, L, d), 83)
+    loss = lambda: float((oracle.prefill(q, k, v, W, C) * R).sum())
+    dq, dk, dv = oracle.backward(q, k, v, R, W, C)
+    for x, g in ((q, dq), (k, dk), (v, dv)):
+        np.testing.assert_allclose(g, numeric_grad(loss, x), rtol=1e-6, atol=1e-8)
+
+
+def test_backward_chunk_of_one_is_exact_attention_autograd():
+    # C = 1: the forward is exact causal attention, so its gradients are the
+    # library's (torch autograd through scaled_dot_product_attention, fp64)
+    B, H, Hkv, L, d, W = 1, 4, 2, 24, 8, 5
+    q, k, v = rand((B, H, L, d), 84), rand((B, Hkv, L, d), 85), rand((B, Hkv, L, d), 86)
+    R = rand((B, H, L, d), 87)
+    tq, tk, tv = (torch.from_numpy(x.copy()).requires_grad_() for x in (q, k, v))
+    o = torch.nn.functional.scaled_dot_product_attention(tq, tk.repeat_interleave(H // Hkv, 1),
+                                                         tv.repeat_interleave(H // Hkv, 1), is_causal=True)
+    (o * torch.from_numpy(R)).sum().backward()
+    dq, dk, dv = oracle.backward(q, k, v, R, W, 1)
+    np.testing.assert_allclose(dq, tq.grad.numpy(), rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(dk, tk.grad.numpy(), rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(dv, tv.grad.numpy(), rtol=1e-10, atol=1e-11)
