@@ -226,6 +226,42 @@ def main():
 
     ms_summ, ms_attn, ms_fill_app, ms_dec = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
 
+    # training step of the same layer: forward with log-sum-exp, then the
+    # backward for a random output gradient (algorithmic FLOPs: five products
+    # per attended (row, key) pair, S recomputed once: 10 d)
+    dO_t = torch.randn(B, H, L, d, device=dev).to(w.dtype)
+    lse_t = torch.empty(B, H, L, dtype=torch.float32, device=dev)
+    lib = eva._lib.load()
+    ws_b = torch.empty((lib.eva_prefill_backward_workspace_bytes(B, H, Hkv, L, d, C) + 3) // 4, dtype=torch.float32,
+                       device=dev)
+    dQ_t, dK_t, dV_t = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+
+    def fwd_bwd(ev=None):
+        if ev: ev[0].record()
+        eva._lib.check("eva_prefill_forward", lib.eva_prefill_forward(
+            eva._ptr(q), eva._ptr(k), eva._ptr(v), eva._ptr(Ks), eva._ptr(Vs), eva._ptr(O), eva._ptr(lse_t),
+            B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
+        if ev: ev[1].record()
+        eva._lib.check("eva_prefill_backward", lib.eva_prefill_backward(
+            eva._ptr(q), eva._ptr(k), eva._ptr(v), eva._ptr(Ks), eva._ptr(Vs), eva._ptr(O), eva._ptr(dO_t),
+            eva._ptr(lse_t), eva._ptr(dQ_t), eva._ptr(dK_t), eva._ptr(dV_t), eva._ptr(ws_b), ws_b.numel() * 4,
+            B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
+        if ev: ev[2].record()
+
+    fwd_bwd()
+    n_tr = max(args.steps // 2, 1)
+    tev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_tr)]
+    for i in range(n_tr):
+        fwd_bwd(tev[i])
+    torch.cuda.synchronize()
+    ms_fwd_t = sum(e[0].elapsed_time(e[1]) for e in tev) / n_tr
+    ms_bwd_t = sum(e[1].elapsed_time(e[2]) for e in tev) / n_tr
+    bwd_flops = B * H * 10 * d * attended(L, W, C)
+    training = {"forward_lse_ms": ms_fwd_t, "backward_ms": ms_bwd_t, "backward_alg_flops": bwd_flops,
+                "backward_tflops": bwd_flops / (ms_bwd_t * 1e-3) / 1e12,
+                "backward_mfma_frac": bwd_flops / (ms_bwd_t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+    del dO_t, dQ_t, dK_t, dV_t, ws_b
+
     # window variants of the fused kernel on the same inputs (summaries as built)
     variants = {}
     for var, name in ((1, "chunk_aligned"), (2, "blocked"), (3, "noncausal")):
@@ -287,6 +323,7 @@ def main():
                     "attention_mfma_frac": attn_tflops / PEAK_BF16_TFLOPS,
                     "summaries_ms": ms_summ, "summaries_gbs": summ_bytes / (ms_summ * 1e-3) / 1e9,
                     "window_variants": variants,
+                    "training": training,
                     "summaries_rf_ms": ms_summ_rf,
                     "summaries_rf_gbs": (summ_bytes + B * Hkv * (L // C) * d * 4) / (ms_summ_rf * 1e-3) / 1e9,
                     "fill_append_ms": ms_fill_app, "decode_ms": ms_dec,

@@ -198,6 +198,40 @@ int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, 
                    int W, int C, int dtype, int window, void* Ksum, void* Vsum, eva_cache* cache, void* stream);
 
 /*
+ * Training forward: eva_prefill_attention (sliding window) that also stores,
+ * for every row, lse[b][h][n] = natural log of the sum of exp(logits) over
+ * the row's window keys and summaries (logits q.k / sqrt(d), + ln C for a
+ * summary), fp32 [B][H][L], as eva_prefill_backward needs it.
+ * Errors: as eva_prefill_attention; INVALID for a null lse.
+ */
+int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                        float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream);
+
+/*
+ * Backward of the EVA prefill (sliding window, bf16): given dO [B][H][L][d],
+ * the gradient of a loss with respect to O, writes dQ [B][H][L][d] and
+ * dK, dV [B][H_kv][L][d] of that loss — through the window keys and values,
+ * the summary keys and values, and the summaries' own dependence on K and V
+ * (the mean key, and the softmax(mean . k / sqrt(d))-weighted value; the
+ * ln C offset is a constant).  Inputs: the forward's Q, K, V, its summaries
+ * Ksum, Vsum [B][H_kv][L / C][d] (eva_build_summaries), its output O and lse
+ * (eva_prefill_forward).  The softmax is recomputed from lse, so nothing of
+ * size L x L is stored (FlashAttention-style, section "FlashAttention").
+ * ws: caller-owned device scratch of eva_prefill_backward_workspace_bytes()
+ * bytes (fp32 row dots and window / summary gradients before they are
+ * combined); every byte the call reads it writes first.
+ * Errors: INVALID (shapes, null or misaligned pointers), UNSUPPORTED (dtype
+ * other than EVA_BF16, d not 64 or 128), CAPACITY (workspace too small).
+ */
+int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                         const void* O, const void* dO, const float* lse, void* dQ, void* dK, void* dV, void* ws,
+                         size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                         void* stream);
+
+/* Workspace eva_prefill_backward needs (0 for invalid sizes). */
+size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d, int C);
+
+/*
  * Load a decode cache from a prefilled sequence of L tokens: the last
  * min(L, R) keys/values go to ring slots p mod R and the L / C summaries
  * (as built by eva_build_summaries) to the summary arrays; n_tok becomes L.

@@ -16,7 +16,7 @@ OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libeva.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["summary.hip", "prefill.hip", "prefill_mfma.hip", "decode.hip", "eva_api.cpp"]
+SOURCES = ["summary.hip", "prefill.hip", "prefill_mfma.hip", "decode.hip", "backward.hip", "eva_api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -1,0 +1,600 @@
+// Backward pass of the fused EVA prefill (bf16, sliding window): dQ, dK, dV
+// of a loss given dO, through the window keys/values, the summary keys and
+// values, and the summaries' own dependence on K and V.
+//
+// Notation: logits l = q.k / sqrt(d) (+ ln C for a summary), the row's
+// softmax P = exp(l - lse) with lse saved by the forward, D = dO . O per row,
+// dS = P (dP - D) with dP = dO . v.  Then dq = sum dS k / sqrt(d),
+// dk += dS q / sqrt(d), dv += P dO (FlashAttention-style recomputation: no
+// attention matrix is stored).
+//
+// Kernels (all bf16 storage, fp32 arithmetic, v_mfma_f32_16x16x32_bf16):
+//   bwd_dot_kernel     D = rowwise dO . O
+//   bwd_dq_kernel      per query tile (4 waves x 32 columns of one head), key
+//                      blocks of 32 rows (summaries then window band) streamed
+//                      through LDS: S^T = K Q^T, dP^T = V dO^T, dS^T, and
+//                      dQ^T += K^T dS^T (K^T by the transposing LDS read)
+//   bwd_dkdv_kernel    per key tile (4 waves x 16 keys, window keys or
+//                      summaries of one kv head), query blocks of 32 rows of
+//                      every head of the group streamed through LDS:
+//                      S = Q K^T, dP = dO V^T, dS, dV^T += dO^T P,
+//                      dK^T += Q^T dS; fp32 results to a workspace
+//   bwd_summary_kernel per chunk: through khat = mean and the chunk softmax
+//                      (vhat = sum_j b_j v_j, b = softmax(khat . k / sqrt(d))),
+//                      added to the window gradients and stored as bf16
+// The fragment layouts are those of the forward kernel: streamed rows are the
+// A operand (16-B row reads, or transposing reads for the transposed
+// products), the stationary rows are B-operand fragments in registers, and
+// the 16x16 score tiles of two key (or query) halves form the next product's
+// B operand in place.
+#include "eva_device.hpp"
+#include "eva_kernels.hpp"
+#include "summary.hpp"
+
+namespace eva {
+
+namespace {
+
+constexpr int kBwdWaves = 4;
+constexpr int kBwdBN = 32;  // rows per streamed block
+
+template <int D>
+struct BCfg {
+    static constexpr int ROWB = 2 * D;            // bytes per row
+    static constexpr int CPR = ROWB / 16;         // 16-B chunks per row
+    static constexpr int BLK = kBwdBN * ROWB;     // bytes per block
+    static constexpr int NI = BLK / 1024 / kBwdWaves;  // DMA instructions per wave per array
+    static constexpr int NDC = D / 32;            // contraction steps over features
+    static constexpr int NDB = D / 16;            // 16-feature output blocks
+};
+
+// stored 16-B chunk = logical chunk ^ bswz(row): conflict-free 16-B row reads
+template <int CPR>
+__device__ __forceinline__ int bswz(int r) {
+    return CPR >= 16 ? (r & 15) : ((r >> 1) & 7);
+}
+
+__device__ __forceinline__ void bdma16(const void* base, unsigned voff, unsigned lds_addr) {
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
+
+template <int D>
+struct Stager {
+    typedef BCfg<D> Cfg;
+    int row[Cfg::NI], off[Cfg::NI];  // per DMA instruction: source row and chunk byte offset
+    __device__ Stager(int wave, int lane) {
+#pragma unroll
+        for (int i = 0; i < Cfg::NI; ++i) {
+            const int byte = (i * kBwdWaves + wave) * 1024 + lane * 16;
+            const int r = byte / Cfg::ROWB;
+            const int pos = (byte % Cfg::ROWB) / 16;
+            row[i] = r;
+            off[i] = (pos ^ bswz<Cfg::CPR>(r)) << 4;
+        }
+    }
+    // rows [0, n_valid) of `src` (row-major, D bf16 each) into the LDS block at
+    // lds_addr; rows past n_valid repeat the last valid row (finite, masked)
+    __device__ void issue(const bf16* src, int n_valid, unsigned lds_addr, int wave) const {
+#pragma unroll
+        for (int i = 0; i < Cfg::NI; ++i) {
+            const int r = min(row[i], n_valid - 1);
+            bdma16(src, (unsigned)(r * Cfg::ROWB + off[i]), lds_addr + (i * kBwdWaves + wave) * 1024);
+        }
+    }
+};
+
+template <int D>
+__device__ __forceinline__ unsigned lds_addr_of(const void* p) {
+    return (unsigned)(size_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// 16-B row fragment: row kb*16 + c16, features dc*32 + 8g .. +7
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag(const unsigned char* blk, int kb, int dc, int c16, int g) {
+    typedef BCfg<D> Cfg;
+    const int r = kb * 16 + c16;
+    const int chunk = (dc * 4 + g) ^ bswz<Cfg::CPR>(r);
+    return *reinterpret_cast<const bf16x8*>(blk + r * Cfg::ROWB + chunk * 16);
+}
+
+// transposing fragment (A operand of a transposed product): lane (g, c16)
+// receives feature db*16 + c16 of rows 4g .. 4g+3 and 16+4g .. 16+4g+3
+template <int D>
+__device__ __forceinline__ bf16x8 tr_frag(const unsigned char* blk, int db, int c16, int g) {
+    typedef BCfg<D> Cfg;
+    const int r = g * 4 + (c16 >> 2);
+    const int t = c16 & 3;
+    const int chunk = (2 * db + (t >> 1)) ^ bswz<Cfg::CPR>(r);
+    const unsigned char* p = blk + r * Cfg::ROWB + chunk * 16 + (t & 1) * 8;
+    const shortx4 lo = lds_read_tr16(reinterpret_cast<const bf16*>(p));
+    // row r + 16 has the same swizzle (bswz depends on r mod 16)
+    const shortx4 hi = lds_read_tr16(reinterpret_cast<const bf16*>(p + 16 * Cfg::ROWB));
+    return __builtin_bit_cast(
+        bf16x8, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+}
+
+// B-operand fragment in the contraction order of tr_frag: element e is tile
+// kb = e / 4, row 4g + e % 4 of a pair of 16x16 output tiles
+__device__ __forceinline__ bf16x8 pair_to_b(const floatx4& t0, const floatx4& t1) {
+    bf16x8 f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[i] = to_bf16(t0[i]);
+        f[4 + i] = to_bf16(t1[i]);
+    }
+    return f;
+}
+
+// ---------------------------------------------------------------------------
+// D = rowwise dO . O
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dot_kernel(const bf16* __restrict__ dO, const bf16* __restrict__ O,
+                                                      float* __restrict__ Dv, long long rows) {
+    constexpr int TPR = D / 8;
+    const long long r = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+    const int cc = threadIdx.x % TPR;
+    float s = 0.f;
+    if (r < rows) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(dO + r * D + cc * 8);
+        const u32x4 b = *reinterpret_cast<const u32x4*>(O + r * D + cc * 8);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s += bf16_lo(a[i]) * bf16_lo(b[i]) + bf16_hi(a[i]) * bf16_hi(b[i]);
+    }
+#pragma unroll
+    for (int off = 1; off < TPR; off <<= 1) s += __shfl_xor(s, off, 64);
+    if (r < rows && cc == 0) Dv[r] = s;
+}
+
+// ---------------------------------------------------------------------------
+// dQ
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
+    typedef BCfg<D> Cfg;
+    constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2][BLK];  // [stage][K, V]
+
+    const int L = a.L, W = a.W, C = a.C;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    constexpr int POS = kBwdWaves * 32;  // positions per workgroup
+    const int n_pt = (L + POS - 1) / POS;
+    const int pt = n_pt - 1 - (int)blockIdx.x % n_pt;  // late (heavy) tiles first
+    const int bh = (int)blockIdx.x / n_pt;
+    const int b = bh / a.H, h = bh % a.H;
+    const int kvh = h / (a.H / a.Hkv);
+    const size_t bg = (size_t)b * a.Hkv + kvh;
+    const int n0 = pt * POS;
+    const int n_hi = min(n0 + POS - 1, L - 1);
+    const int p0 = n0 + wave * 32;
+    const bool w_active = p0 < L;
+    const int wp_last = min(p0 + 31, L - 1);
+
+    // block plan as in the forward: summaries [0, s(n_hi)), then the window band
+    const int nsb = (visible_summaries(n_hi, W, C) + kBwdBN - 1) / kBwdBN;
+    const int kb0 = max(0, n0 - W + 1) / kBwdBN;
+    const int nb = nsb + (n_hi / kBwdBN - kb0 + 1);
+    const int ws_hi = w_active ? visible_summaries(wp_last, W, C) : 0;
+
+    const bf16* Kbg = static_cast<const bf16*>(a.K) + bg * (size_t)L * D;
+    const bf16* Vbg = static_cast<const bf16*>(a.V) + bg * (size_t)L * D;
+    const bf16* Ksbg = static_cast<const bf16*>(a.Ks) + bg * (size_t)a.n_chunks * D;
+    const bf16* Vsbg = static_cast<const bf16*>(a.Vs) + bg * (size_t)a.n_chunks * D;
+
+    // stationary columns: q and dO fragments (B operands), lse and D
+    const size_t row0 = (size_t)bh * L;
+    bf16x8 qf[2][NDC], gf[2][NDC];
+    float lse2[2], dcol[2];
+    int col_n[2], col_s[2];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+        col_n[cb] = p0 + cb * 16 + c16;
+        const int n = min(col_n[cb], L - 1);
+        col_s[cb] = visible_summaries(n, W, C);
+        const bf16* qrow = static_cast<const bf16*>(a.Q) + (row0 + n) * D;
+        const bf16* grow = static_cast<const bf16*>(a.dO) + (row0 + n) * D;
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc) {
+            qf[cb][dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
+            gf[cb][dc] = *reinterpret_cast<const bf16x8*>(grow + dc * 32 + g * 8);
+        }
+        lse2[cb] = a.lse[row0 + n] * kLog2e;
+        dcol[cb] = a.Dv[row0 + n];
+    }
+
+    floatx4 acc[NDB][2];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) acc[db][0] = acc[db][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    const Stager<D> st(wave, lane);
+    auto stage = [&](int j) {
+        const bool sum = j < nsb;
+        const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
+        const int lim = sum ? a.n_chunks : L;
+        const int nv = min(kBwdBN, lim - base);
+        st.issue((sum ? Ksbg : Kbg) + (size_t)base * D, nv, lds_addr_of<D>(lds[j & 1][0]), wave);
+        st.issue((sum ? Vsbg : Vbg) + (size_t)base * D, nv, lds_addr_of<D>(lds[j & 1][1]), wave);
+    };
+    if (nb > 0) stage(0);
+    for (int j = 0; j < nb; ++j) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();  // block j landed; every wave is done with block j-1's stage
+        if (j + 1 < nb) stage(j + 1);
+        const bool sum = j < nsb;
+        const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
+        const bool needed =
+            w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
+        if (!needed) continue;
+        const unsigned char* ks = lds[j & 1][0];
+        const unsigned char* vs = lds[j & 1][1];
+        // S^T and dP^T: rows = keys base + kb*16 + 4g + i, column = query c16
+        floatx4 s[2][2], dp[2][2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) s[kb][cb] = dp[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const bf16x8 kf = row_frag<D>(ks, kb, dc, c16, g);
+                const bf16x8 vf = row_frag<D>(vs, kb, dc, c16, g);
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    s[kb][cb] = mfma_bf16(kf, qf[cb][dc], s[kb][cb]);
+                    dp[kb][cb] = mfma_bf16(vf, gf[cb][dc], dp[kb][cb]);
+                }
+            }
+        // P^T and dS^T (masked entries: 0)
+        const float bias = sum ? a.log2C : 0.f;
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            const int n = col_n[cb];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = base + kb * 16 + g * 4 + i;
+                    const bool ok = n < L && (sum ? key < col_s[cb] : (unsigned)(n - key) < (unsigned)W);
+                    const float p = ok ? fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, bias - lse2[cb])) : 0.f;
+                    s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
+                }
+        }
+        bf16x8 dsf[2];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) dsf[cb] = pair_to_b(s[0][cb], s[1][cb]);
+        // dQ^T += K^T dS^T
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const bf16x8 kt = tr_frag<D>(ks, db, c16, g);
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_bf16(kt, dsf[cb], acc[db][cb]);
+        }
+    }
+
+    // dQ = acc / sqrt(d): lane (g, c16) holds features db*16 + 4g .. +3 of column c16
+    const float inv_sqrt_d = a.scale_log2 / kLog2e;
+    bf16* dQ = static_cast<bf16*>(a.dQ);
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+        const int n = col_n[cb];
+        if (n >= L) continue;
+        bf16* orow = dQ + (row0 + n) * D;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const floatx4 v = acc[db][cb] * inv_sqrt_d;
+            u32x2 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+            *reinterpret_cast<u32x2*>(orow + db * 16 + g * 4) = w;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV of window keys and of summaries
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
+    typedef BCfg<D> Cfg;
+    constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
+    constexpr int KT = kBwdWaves * 16;  // keys per workgroup
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2][BLK];  // [stage][Q, dO]
+
+    const int L = a.L, W = a.W, C = a.C;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const int n_wt = (L + KT - 1) / KT;           // window key tiles per (b, kv head)
+    const int n_st = (a.n_chunks + KT - 1) / KT;  // summary tiles
+    const int per_bg = n_wt + n_st;
+    const int bgi = (int)blockIdx.x / per_bg;
+    const int t = (int)blockIdx.x % per_bg;
+    const size_t bg = (size_t)bgi;
+    const int b = bgi / a.Hkv, kvh = bgi % a.Hkv;
+    const int G = a.H / a.Hkv;
+    const bool sum = t >= n_wt;
+    const int k0 = (sum ? t - n_wt : t) * KT;     // first key (or summary) of the tile
+    const int lim = sum ? a.n_chunks : L;
+    const int key = k0 + wave * 16 + c16;         // this lane's key column
+    const int key_c = min(key, lim - 1);
+
+    // stationary key/value rows (B operands): features dc*32 + 8g .. +7 of key_c
+    const bf16* Kr = static_cast<const bf16*>(sum ? a.Ks : a.K) + (bg * (size_t)lim + key_c) * D;
+    const bf16* Vr = static_cast<const bf16*>(sum ? a.Vs : a.V) + (bg * (size_t)lim + key_c) * D;
+    bf16x8 kf[NDC], vf[NDC];
+#pragma unroll
+    for (int dc = 0; dc < NDC; ++dc) {
+        kf[dc] = *reinterpret_cast<const bf16x8*>(Kr + dc * 32 + g * 8);
+        vf[dc] = *reinterpret_cast<const bf16x8*>(Vr + dc * 32 + g * 8);
+    }
+
+    // query rows that can see some key of the tile: window keys k are seen by
+    // rows [k, k + W - 1]; summary c by rows n with s(n) > c, i.e.
+    // n >= (c + 1) C + W - 1
+    const int k_last = min(k0 + KT, lim) - 1;
+    const int r_lo = sum ? (int)min((long long)L, (long long)(k0 + 1) * C + W - 1) : k0;
+    const int r_hi = sum ? L - 1 : min(L - 1, k_last + W - 1);
+    const int qb0 = r_lo / kBwdBN;
+    const int nqb = r_lo <= r_hi ? r_hi / kBwdBN - qb0 + 1 : 0;
+    // this wave's keys [wk0, wk1]
+    const int wk0 = k0 + wave * 16, wk1 = min(wk0 + 15, lim - 1);
+    const bool w_active = wk0 < lim;
+    const int wr_lo = sum ? (int)min((long long)L, (long long)(wk0 + 1) * C + W - 1) : wk0;
+    const int wr_hi = sum ? L - 1 : min(L - 1, wk1 + W - 1);
+
+    floatx4 dk[NDB], dv[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dk[db] = dv[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float bias = sum ? a.log2C : 0.f;
+
+    const Stager<D> stg(wave, lane);
+    const int steps = nqb * G;  // (head, query block) pairs
+    auto stage = [&](int j) {
+        const int hh = j / nqb, qb = qb0 + j % nqb;
+        const size_t rowb = ((size_t)b * a.H + kvh * G + hh) * L + (size_t)qb * kBwdBN;
+        const int nv = min(kBwdBN, L - qb * kBwdBN);
+        stg.issue(static_cast<const bf16*>(a.Q) + rowb * D, nv, lds_addr_of<D>(lds[j & 1][0]), wave);
+        stg.issue(static_cast<const bf16*>(a.dO) + rowb * D, nv, lds_addr_of<D>(lds[j & 1][1]), wave);
+    };
+    if (steps > 0) stage(0);
+    for (int j = 0; j < steps; ++j) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (j + 1 < steps) stage(j + 1);
+        const int hh = j / nqb, qb = qb0 + j % nqb;
+        const int r0 = qb * kBwdBN;
+        if (!w_active || r0 > wr_hi || r0 + kBwdBN - 1 < wr_lo) continue;
+        const size_t rowh = ((size_t)b * a.H + kvh * G + hh) * L;
+        // lse and D of this lane's 8 query rows r0 + 16 kb + 4g + i
+        float lse2[2][4], dq[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = min(r0 + kb * 16 + g * 4 + i, L - 1);
+                lse2[kb][i] = a.lse[rowh + n] * kLog2e;
+                dq[kb][i] = a.Dv[rowh + n];
+            }
+        const unsigned char* qs = lds[j & 1][0];
+        const unsigned char* gs = lds[j & 1][1];
+        // S and dP: rows = queries r0 + kb*16 + 4g + i, column = key c16
+        floatx4 s[2], dp[2];
+        s[0] = s[1] = dp[0] = dp[1] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int dc = 0; dc < NDC; ++dc)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                s[kb] = mfma_bf16(row_frag<D>(qs, kb, dc, c16, g), kf[dc], s[kb]);
+                dp[kb] = mfma_bf16(row_frag<D>(gs, kb, dc, c16, g), vf[dc], dp[kb]);
+            }
+        floatx4 p[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = r0 + kb * 16 + g * 4 + i;
+                const bool ok = key < lim && n < L &&
+                                (sum ? key < visible_summaries(n, W, C) : (unsigned)(n - key) < (unsigned)W);
+                p[kb][i] = ok ? fast_exp2(fmaf(s[kb][i], a.scale_log2, bias - lse2[kb][i])) : 0.f;
+                s[kb][i] = p[kb][i] * (dp[kb][i] - dq[kb][i]);  // dS
+            }
+        const bf16x8 pf = pair_to_b(p[0], p[1]);
+        const bf16x8 dsf = pair_to_b(s[0], s[1]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            dv[db] = mfma_bf16(tr_frag<D>(gs, db, c16, g), pf, dv[db]);
+            dk[db] = mfma_bf16(tr_frag<D>(qs, db, c16, g), dsf, dk[db]);
+        }
+    }
+
+    // fp32 results: window gradients (per key row) or summary gradients
+    if (key >= lim) return;
+    const float inv_sqrt_d = a.scale_log2 / kLog2e;
+    float* dKo = (sum ? a.dKs_w : a.dK_w) + (bg * (size_t)lim + key) * D;
+    float* dVo = (sum ? a.dVs_w : a.dV_w) + (bg * (size_t)lim + key) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+        *reinterpret_cast<floatx4*>(dKo + db * 16 + g * 4) = dk[db] * inv_sqrt_d;
+        *reinterpret_cast<floatx4*>(dVo + db * 16 + g * 4) = dv[db];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// through the summaries, plus the window gradients, to dK and dV
+// ---------------------------------------------------------------------------
+// One 256-thread workgroup per chunk (blockIdx.x < n_chunks), or for the
+// rows after the last complete chunk (blockIdx.x == n_chunks: window part
+// only).  Thread t holds features cc*8 .. cc*8+7 (cc = t % TPR) of rows
+// r0, r0 + RPS, ... (r0 = t / TPR).  LDS: a_j (log2 units) and da_j, C floats
+// each, then the reduction scratch.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
+    constexpr int TPR = D / 8;
+    constexpr int RPS = 256 / TPR;
+    extern __shared__ float smem[];
+    float* logit = smem;
+    float* dal = smem + a.C;
+    float* red = smem + 2 * a.C;
+    const int chunk = blockIdx.x;
+    const size_t bg = blockIdx.y;
+    const int L = a.L, C = a.C;
+    const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
+    const bool tail = chunk == a.n_chunks;
+    const int first = chunk * C;
+    const int rows = tail ? L - first : C;
+    const bf16* K = static_cast<const bf16*>(a.K) + (bg * (size_t)L + first) * D;
+    const bf16* V = static_cast<const bf16*>(a.V) + (bg * (size_t)L + first) * D;
+    const float* dKw = a.dK_w + (bg * (size_t)L + first) * D;
+    const float* dVw = a.dV_w + (bg * (size_t)L + first) * D;
+    bf16* dK = static_cast<bf16*>(a.dK) + (bg * (size_t)L + first) * D;
+    bf16* dV = static_cast<bf16*>(a.dV) + (bg * (size_t)L + first) * D;
+    auto load8 = [&](const bf16* base, int r, float out[8]) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)r * D + cc * 8);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            out[2 * i] = bf16_lo(w[i]);
+            out[2 * i + 1] = bf16_hi(w[i]);
+        }
+    };
+    auto row_sum = [&](float x) {
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
+        return x;
+    };
+    const float sc = a.scale_log2;  // log2(e) / sqrt(d): logits in log2 units
+    const float inv_sqrt_d = sc / kLog2e;
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, gvh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float amax = 0.f, inv_den = 0.f;
+    if (!tail) {
+        float gkh[8];
+        const float* gk = a.dKs_w + (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+        const float* gv = a.dVs_w + (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            gkh[i] = gk[i];
+            gvh[i] = gv[i];
+        }
+        // khat = mean key
+        for (int r = r0; r < C; r += RPS) {
+            float k[8];
+            load8(K, r, k);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) kh[i] += k[i];
+        }
+        reduce_rows8<TPR>(kh, red);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) kh[i] *= 1.f / (float)C;
+        // a_j and their max
+        float mx = -INFINITY;
+        for (int r = r0; r < C; r += RPS) {
+            float k[8];
+            load8(K, r, k);
+            float x = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x += kh[i] * k[i];
+            x = row_sum(x) * sc;
+            if (cc == 0) logit[r] = x;
+            mx = fmaxf(mx, x);
+        }
+        amax = block_max(mx, red);  // also orders the logit writes before the reads
+        // vhat = sum_j b_j v_j (unnormalized) and the denominator
+        float vh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        float psum = 0.f;
+        for (int r = r0; r < C; r += RPS) {
+            float v[8];
+            load8(V, r, v);
+            const float p = fast_exp2(logit[r] - amax);
+            psum += p;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) vh[i] += p * v[i];
+        }
+#pragma unroll
+        for (int off = TPR; off < 64; off <<= 1) psum += __shfl_xor(psum, off, 64);
+        if ((t & 63) == 0) red[5 * TPR * 8 + (t >> 6)] = psum;
+        __syncthreads();
+        inv_den = 1.f / (red[5 * TPR * 8] + red[5 * TPR * 8 + 1] + red[5 * TPR * 8 + 2] + red[5 * TPR * 8 + 3]);
+        __syncthreads();
+        reduce_rows8<TPR>(vh, red);
+        // dvhat . vhat
+        float x = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x += gvh[i] * vh[i] * inv_den;
+        const float gvv = row_sum(x);
+        // da_j = b_j (dvhat . v_j - dvhat . vhat); dkhat = dK^_c + sum_j da_j k_j / sqrt(d)
+        for (int r = r0; r < C; r += RPS) {
+            float v[8], k[8];
+            load8(V, r, v);
+            load8(K, r, k);
+            float y = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y += gvh[i] * v[i];
+            y = row_sum(y);
+            const float da = fast_exp2(logit[r] - amax) * inv_den * (y - gvv);
+            if (cc == 0) dal[r] = da;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dkh[i] += da * k[i];
+        }
+        reduce_rows8<TPR>(dkh, red);  // its barriers also order the dal writes before the reads below
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dkh[i] = gkh[i] + dkh[i] * inv_sqrt_d;
+    }
+    // dK_j = window part + da_j khat / sqrt(d) + dkhat / C;  dV_j = window part + b_j dvhat
+    for (int r = r0; r < rows; r += RPS) {
+        const floatx4 wk0 = *reinterpret_cast<const floatx4*>(dKw + (size_t)r * D + cc * 8);
+        const floatx4 wk1 = *reinterpret_cast<const floatx4*>(dKw + (size_t)r * D + cc * 8 + 4);
+        const floatx4 wv0 = *reinterpret_cast<const floatx4*>(dVw + (size_t)r * D + cc * 8);
+        const floatx4 wv1 = *reinterpret_cast<const floatx4*>(dVw + (size_t)r * D + cc * 8 + 4);
+        float gk[8] = {wk0[0], wk0[1], wk0[2], wk0[3], wk1[0], wk1[1], wk1[2], wk1[3]};
+        float gv[8] = {wv0[0], wv0[1], wv0[2], wv0[3], wv1[0], wv1[1], wv1[2], wv1[3]};
+        if (!tail) {
+            const float da = dal[r];
+            const float bj = fast_exp2(logit[r] - amax) * inv_den;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                gk[i] += da * kh[i] * inv_sqrt_d + dkh[i] * (1.f / (float)C);
+                gv[i] += bj * gvh[i];
+            }
+        }
+        u32x4 ok, ov;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            ok[i] = pack_bf16x2(gk[2 * i], gk[2 * i + 1]);
+            ov[i] = pack_bf16x2(gv[2 * i], gv[2 * i + 1]);
+        }
+        *reinterpret_cast<u32x4*>(dK + (size_t)r * D + cc * 8) = ok;
+        *reinterpret_cast<u32x4*>(dV + (size_t)r * D + cc * 8) = ov;
+    }
+}
+
+}  // namespace
+
+template <int D>
+hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
+    // D = rowwise dO . O
+    const long long rows = (long long)p.B * p.H * p.L;
+    constexpr int RPB = 256 / (D / 8);
+    hipLaunchKernelGGL((bwd_dot_kernel<D>), dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), 0, stream,
+                       static_cast<const bf16*>(p.dO), static_cast<const bf16*>(p.O), p.Dv, rows);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int n_pt = (p.L + kBwdWaves * 32 - 1) / (kBwdWaves * 32);
+    hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    constexpr int KT = kBwdWaves * 16;
+    const int tiles = (p.L + KT - 1) / KT + (p.n_chunks + KT - 1) / KT;
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3(p.B * p.Hkv * tiles), dim3(kBwdWaves * 64), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const bool has_tail = p.L % p.C != 0;
+    const size_t lds = (size_t)(2 * p.C + summary_red_floats<D>()) * sizeof(float);
+    const int nx = p.n_chunks + (has_tail ? 1 : 0);
+    if (nx > 0)
+        hipLaunchKernelGGL((bwd_summary_kernel<D>), dim3(nx, p.B * p.Hkv), dim3(256), lds, stream, p);
+    return hipGetLastError();
+}
+
+template hipError_t launch_backward<64>(const BwdParams&, hipStream_t);
+template hipError_t launch_backward<128>(const BwdParams&, hipStream_t);
+
+}  // namespace eva

@@ -238,9 +238,26 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
                                     stream);
 }
 
+static int prefill_attention_impl(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                                  void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                                  int window, void* stream);
+
 int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
                              void* O, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, int window,
                              void* stream) {
+    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, nullptr, B, H, H_kv, L, d, W, C, dtype, window, stream);
+}
+
+int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                        float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream) {
+    if (!lse) return EVA_ERR_INVALID;
+    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, lse, B, H, H_kv, L, d, W, C, dtype, EVA_WINDOW_SLIDING,
+                                  stream);
+}
+
+static int prefill_attention_impl(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                                  void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                                  int window, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
     if (!valid_window(window)) return EVA_ERR_INVALID;
     int st = supported(d, dtype);
@@ -283,6 +300,7 @@ int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const 
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
     p.window = window;
+    p.lse = lse;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
         if constexpr (std::is_same<decltype(t), eva::bf16>::value)
@@ -425,6 +443,82 @@ int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const 
     if (st != EVA_OK) return st;
     cache->n_tok = p + 1;
     return EVA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// backward
+// ---------------------------------------------------------------------------
+
+namespace {
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+struct BwdLayout {
+    size_t dv, dkw, dvw, dksw, dvsw, total;
+};
+BwdLayout bwd_layout(long long B, long long H, long long H_kv, long long L, long long d, long long C) {
+    BwdLayout l;
+    const long long nc = L / C;
+    l.dv = 0;
+    l.dkw = align256(l.dv + (size_t)(B * H * L) * 4);
+    l.dvw = align256(l.dkw + (size_t)(B * H_kv * L * d) * 4);
+    l.dksw = align256(l.dvw + (size_t)(B * H_kv * L * d) * 4);
+    l.dvsw = align256(l.dksw + (size_t)(B * H_kv * nc * d) * 4);
+    l.total = align256(l.dvsw + (size_t)(B * H_kv * nc * d) * 4);
+    return l;
+}
+}  // namespace
+
+size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d, int C) {
+    if (B < 1 || H < 1 || H_kv < 1 || L < 1 || C < 1 || d < 1) return 0;
+    return bwd_layout(B, H, H_kv, L, d, C).total;
+}
+
+int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                         const void* O, const void* dO, const float* lse, void* dQ, void* dK, void* dV, void* ws,
+                         size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                         void* stream) {
+    if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    int st = supported(d, dtype);
+    if (st != EVA_OK) return st;
+    if (dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
+    if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H * ((L + 127) / 128) > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
+    const void* must[] = {Q, K, V, O, dO, lse, dQ, dK, dV, ws};
+    for (const void* ptr : must)
+        if (!ptr || !aligned16(ptr)) return EVA_ERR_INVALID;
+    const int n_chunks = L / C;
+    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
+    const BwdLayout lay = bwd_layout(B, H, H_kv, L, d, C);
+    if (ws_bytes < lay.total) return EVA_ERR_CAPACITY;
+    char* w = static_cast<char*>(ws);
+    eva::BwdParams p;
+    p.Q = Q;
+    p.K = K;
+    p.V = V;
+    p.Ks = Ksum;
+    p.Vs = Vsum;
+    p.O = O;
+    p.dO = dO;
+    p.lse = lse;
+    p.dQ = dQ;
+    p.dK = dK;
+    p.dV = dV;
+    p.Dv = reinterpret_cast<float*>(w + lay.dv);
+    p.dK_w = reinterpret_cast<float*>(w + lay.dkw);
+    p.dV_w = reinterpret_cast<float*>(w + lay.dvw);
+    p.dKs_w = reinterpret_cast<float*>(w + lay.dksw);
+    p.dVs_w = reinterpret_cast<float*>(w + lay.dvsw);
+    p.B = B;
+    p.H = H;
+    p.Hkv = H_kv;
+    p.L = L;
+    p.W = W;
+    p.C = C;
+    p.n_chunks = n_chunks;
+    p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
+    p.log2C = (float)log2((double)C);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = d == 64 ? eva::launch_backward<64>(p, s) : eva::launch_backward<128>(p, s);
+    return hip_status(e);
 }
 
 // ---------------------------------------------------------------------------

@@ -35,10 +35,38 @@ struct PrefillParams {
     float scale_log2; // log2(e) / sqrt(d)
     float log2C;      // log2(C): the ln C summary offset in log2 units
     int window;       // window variant (kWin* in eva_device.hpp)
+    float* lse;       // optional [B][H][L]: natural log of each row's softmax denominator
 };
 
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
+
+// Backward of the bf16 prefill (sliding window).  Device pointers; the fp32
+// scratch (Dv, dK_w, dV_w, dKs_w, dVs_w) comes from the caller's workspace.
+struct BwdParams {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* Ks;  // [B][Hkv][n_chunks][d], the forward's summaries
+    const void* Vs;
+    const void* O;
+    const void* dO;
+    const float* lse;  // [B][H][L], natural log of each row's softmax denominator
+    void* dQ;
+    void* dK;
+    void* dV;
+    float* Dv;     // [B][H][L]   dO . O
+    float* dK_w;   // [B][Hkv][L][d]   window parts
+    float* dV_w;
+    float* dKs_w;  // [B][Hkv][n_chunks][d]   gradients of the summary keys / values
+    float* dVs_w;
+    int B, H, Hkv, L, W, C, n_chunks;
+    float scale_log2;  // log2(e) / sqrt(d)
+    float log2C;
+};
+
+template <int D>
+hipError_t launch_backward(const BwdParams& p, hipStream_t stream);
 
 // bf16 only; tile geometry for the configuration prefill_mfma_narrow(G) picks.
 template <int D>

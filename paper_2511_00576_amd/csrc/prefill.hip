@@ -544,6 +544,8 @@ __global__ __launch_bounds__(NW * 64) void prefill_kernel(PrefillParams a) {
         const int n = col_n[cb];
         if (n >= L) continue;
         const float inv = 1.f / lt;
+        // natural log of the softmax denominator: sum 2^(x - m_run) = lt
+        if (a.lse && g == 0) a.lse[bh * L + n] = (m_run[cb] + __builtin_amdgcn_logf(lt)) * kLn2;
         T* orow = O + (bh * L + (size_t)n) * D;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {

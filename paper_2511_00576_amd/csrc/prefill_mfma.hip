@@ -610,6 +610,8 @@ void prefill_mfma_kernel(PrefillParams a) {
         const int n = col_n(cb);
         if (n >= L) continue;
         const float inv = 1.f / l_acc[cb][0];
+        // natural log of the softmax denominator: sum 2^(x - m_run) = l
+        if (a.lse && g == 0) a.lse[bh * L + n] = (m_run[cb] + __builtin_amdgcn_logf(l_acc[cb][0])) * kLn2;
         bf16* orow = O + (bh * L + (size_t)n) * D;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {

@@ -342,3 +342,45 @@ def generate(cache: RaggedCache, q, k, v, active=None, out=None, use_workspace=T
                _lib.load().eva_generate(ctypes.byref(s), _ptr(q), _ptr(k), _ptr(v), _ptr(o), T, _active_ptr(active),
                                         ws, nbytes, _stream()))
     return o
+
+
+def prefill_forward(Q, K, V, W: int, C: int):
+    """Training forward (sliding window): summaries, O and the per-row
+    log-sum-exp.  Returns (O, lse, Ks, Vs); lse is fp32 [B, H, L]."""
+    _require_device(Q, K, V)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    Ks, Vs = build_summaries(K, V, C)
+    O = torch.empty_like(Q)
+    lse = torch.empty(B, H, L, dtype=torch.float32, device=Q.device)
+    n_chunks = L // C
+    _lib.check("eva_prefill_forward",
+               _lib.load().eva_prefill_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
+                                               _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(lse), B, H, Hkv, L, d, W,
+                                               C, _dtype_code(Q), _stream()))
+    return O, lse, Ks, Vs
+
+
+def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None):
+    """Gradients (dQ, dK, dV) of the EVA prefill for the output gradient dO
+    (bf16, sliding window), from the training forward's O, lse and summaries."""
+    _require_device(Q, K, V, O, lse, dO)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    if dO.shape != Q.shape or O.shape != Q.shape or tuple(lse.shape) != (B, H, L) or lse.dtype != torch.float32:
+        raise ValueError("O, dO [B, H, L, d] and fp32 lse [B, H, L] expected")
+    lib = _lib.load()
+    need = lib.eva_prefill_backward_workspace_bytes(B, H, Hkv, L, d, C)
+    ws = workspace
+    if ws is None or ws.numel() * ws.element_size() < need:
+        ws = torch.empty((need + 3) // 4, dtype=torch.float32, device=Q.device)
+    dQ = torch.empty_like(Q)
+    dK = torch.empty_like(K)
+    dV = torch.empty_like(V)
+    n_chunks = L // C
+    _lib.check("eva_prefill_backward",
+               lib.eva_prefill_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
+                                        _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(dO), _ptr(lse), _ptr(dQ),
+                                        _ptr(dK), _ptr(dV), _ptr(ws), ws.numel() * ws.element_size(), B, H, Hkv, L, d,
+                                        W, C, _dtype_code(Q), _stream()))
+    return dQ, dK, dV

@@ -72,3 +72,19 @@ def oracle_sampled(Q, K, V, W, C, heads, rows):
         Kb, Vb, Ks, Vs = summ[(b, g)]
         out[(b, h)] = oracle.attend_rows(to64(Q[b, h, torch.from_numpy(rows)]), rows, Kb, Vb, Ks, Vs, W, C)
     return out
+
+
+GRAD_NORM_REL = 2e-2
+
+
+def assert_grad_parity(got, ref, what=""):
+    """bf16 gradients: max |got - ref| <= 2e-2 * max |ref| over the tensor
+    (normwise: the gradient entries span orders of magnitude, so an absolute
+    bound would be meaningless at one scale and loose at another)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite gradient"
+    scale = float(np.abs(ref).max()) if ref.size else 0.0
+    err = float(np.abs(got - ref).max()) if ref.size else 0.0
+    assert err <= GRAD_NORM_REL * max(scale, 1e-30), f"{what}: max abs error {err:.3e} > 2e-2 * {scale:.3e}"
+    return err / max(scale, 1e-30)
