@@ -142,7 +142,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # the GPU reaches its steady clocks only after ~0.1 s of load: 200 warmup
+    # steps (about 0.1 s) before the timed ones
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--decode-iters", type=int, default=64, help="graph-captured decode tokens (x4 caches)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
