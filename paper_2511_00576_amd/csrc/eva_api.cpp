@@ -287,7 +287,7 @@ static int prefill_attention_impl(const void* Q, const void* K, const void* V, c
     // workgroup geometry of the kernel that runs: bf16 -> pipelined kernel,
     // fp32 -> two-phase kernel
     const int waves = dtype != EVA_BF16              ? eva::kPrefillWaves
-                      : eva::prefill_mfma_narrow(p.G) ? eva::kMfmaWavesNarrow
+                      : eva::prefill_mfma_narrow(p.G, W) ? eva::kMfmaWavesNarrow
                                                       : eva::kMfmaWavesWide;
     const int cols = dtype == EVA_BF16 ? 16 * eva::kMfmaColBlocks : 32;
     p.Gt = gcd(p.G, waves);

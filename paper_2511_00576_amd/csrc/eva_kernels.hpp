@@ -12,11 +12,14 @@ constexpr int kPrefillWaves = 8;
 // Pipelined bf16 prefill: 16-column blocks per wave (32 query columns), and
 // waves per workgroup of its two configurations: 8 waves on 64-key blocks
 // (one workgroup per CU), or 4 waves on 32-key blocks (two workgroups per CU,
-// half the positions per tile: used when every kv head has one query head).
+// whose prologues and barriers overlap; half the positions per tile).  The
+// narrow one is used when every kv head has one query head, and for windows
+// of up to 512 keys, where a workgroup's prologue is a large part of its time
+// (measured on MI355X: 429 vs 452 us at W 512, 704 vs 694 us at W 1024).
 constexpr int kMfmaColBlocks = 2;
 constexpr int kMfmaWavesWide = 8;
 constexpr int kMfmaWavesNarrow = 4;
-inline bool prefill_mfma_narrow(int G) { return G == 1; }
+inline bool prefill_mfma_narrow(int G, int W) { return G == 1 || W <= 512; }
 
 struct PrefillParams {
     const void* Q;

@@ -626,7 +626,7 @@ void prefill_mfma_kernel(PrefillParams a) {
 
 template <int D, int VAR>
 void launch_prefill_mfma_var(const PrefillParams& p, hipStream_t stream) {
-    if (prefill_mfma_narrow(p.G)) {
+    if (prefill_mfma_narrow(p.G, p.W)) {
         // 4 waves x 32 columns, 32-key blocks: 77 KB of LDS, two workgroups per CU
         hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2, VAR>), dim3(p.n_tiles),
                            dim3(kMfmaWavesNarrow * 64), 0, stream, p);
