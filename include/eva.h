@@ -218,8 +218,8 @@ int eva_prefill_forward(const void* Q, const void* K, const void* V, const void*
  * (eva_prefill_forward).  The softmax is recomputed from lse, so nothing of
  * size L x L is stored (FlashAttention-style, section "FlashAttention").
  * ws: caller-owned device scratch of eva_prefill_backward_workspace_bytes()
- * bytes (fp32 row dots and window / summary gradients before they are
- * combined); every byte the call reads it writes first.
+ * bytes (fp32 row dots, summary gradients, and per-chunk and per-key factors
+ * of the summaries' own gradient); every byte the call reads it writes first.
  * Errors: INVALID (shapes, null or misaligned pointers), UNSUPPORTED (dtype
  * other than EVA_BF16, d not 64 or 128), CAPACITY (workspace too small).
  */

@@ -18,10 +18,17 @@
 //                      summaries of one kv head), query blocks of 32 rows of
 //                      every head of the group streamed through LDS:
 //                      S = Q K^T, dP = dO V^T, dS, dV^T += dO^T P,
-//                      dK^T += Q^T dS; fp32 results to a workspace
-//   bwd_summary_kernel per chunk: through khat = mean and the chunk softmax
-//                      (vhat = sum_j b_j v_j, b = softmax(khat . k / sqrt(d))),
-//                      added to the window gradients and stored as bf16
+//                      dK^T += Q^T dS.  Summary tiles run first and leave
+//                      fp32 summary gradients; window tiles run last and add
+//                      each key's share of its chunk's summary gradient
+//                      before storing dK, dV as bf16
+//   bwd_summary_kernel per chunk, between the two: through khat = mean and
+//                      the chunk softmax (vhat = sum_j b_j v_j,
+//                      b = softmax(khat . k / sqrt(d))); leaves khat, the
+//                      total gradient of khat, and each key's b_j and
+//                      logit gradient da_j, from which
+//                        dk_j += da_j khat / sqrt(d) + dkhat / C,
+//                        dv_j += b_j dvhat
 // The fragment layouts are those of the forward kernel: streamed rows are the
 // A operand (16-B row reads, or transposing reads for the transposed
 // products), the stationary rows are B-operand fragments in registers, and
@@ -295,7 +302,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
 // ---------------------------------------------------------------------------
 // dK, dV of window keys and of summaries
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool SUM>
 __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
@@ -306,16 +313,15 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
-    const int n_wt = (L + KT - 1) / KT;           // window key tiles per (b, kv head)
-    const int n_st = (a.n_chunks + KT - 1) / KT;  // summary tiles
-    const int per_bg = n_wt + n_st;
+    // key tiles per (b, kv head): summaries, or window keys
+    constexpr bool sum = SUM;
+    const int per_bg = SUM ? (a.n_chunks + KT - 1) / KT : (L + KT - 1) / KT;
     const int bgi = (int)blockIdx.x / per_bg;
     const int t = (int)blockIdx.x % per_bg;
     const size_t bg = (size_t)bgi;
     const int b = bgi / a.Hkv, kvh = bgi % a.Hkv;
     const int G = a.H / a.Hkv;
-    const bool sum = t >= n_wt;
-    const int k0 = (sum ? t - n_wt : t) * KT;     // first key (or summary) of the tile
+    const int k0 = t * KT;                        // first key (or summary) of the tile
     const int lim = sum ? a.n_chunks : L;
     const int key = k0 + wave * 16 + c16;         // this lane's key column
     const int key_c = min(key, lim - 1);
@@ -409,47 +415,70 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
         }
     }
 
-    // fp32 results: window gradients (per key row) or summary gradients
     if (key >= lim) return;
     const float inv_sqrt_d = a.scale_log2 / kLog2e;
-    float* dKo = (sum ? a.dKs_w : a.dK_w) + (bg * (size_t)lim + key) * D;
-    float* dVo = (sum ? a.dVs_w : a.dV_w) + (bg * (size_t)lim + key) * D;
+    if constexpr (SUM) {
+        // fp32 summary gradients, for the per-chunk pass
+        float* dKo = a.dKs_w + (bg * (size_t)lim + key) * D;
+        float* dVo = a.dVs_w + (bg * (size_t)lim + key) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-        *reinterpret_cast<floatx4*>(dKo + db * 16 + g * 4) = dk[db] * inv_sqrt_d;
-        *reinterpret_cast<floatx4*>(dVo + db * 16 + g * 4) = dv[db];
+        for (int db = 0; db < NDB; ++db) {
+            *reinterpret_cast<floatx4*>(dKo + db * 16 + g * 4) = dk[db] * inv_sqrt_d;
+            *reinterpret_cast<floatx4*>(dVo + db * 16 + g * 4) = dv[db];
+        }
+    } else {
+        // window gradient plus the key's share of its chunk's summary gradient
+        // (keys after the last complete chunk have none)
+        const int c = key / C;
+        const bool in_chunk = c < a.n_chunks;
+        float da = 0.f, bj = 0.f;
+        const size_t cv = (bg * (size_t)a.n_chunks + (in_chunk ? c : 0)) * D;
+        if (in_chunk) {
+            da = a.da_w[bg * (size_t)a.n_chunks * C + key] * inv_sqrt_d;
+            bj = a.bw_w[bg * (size_t)a.n_chunks * C + key];
+        }
+        bf16* dKo = static_cast<bf16*>(a.dK) + (bg * (size_t)L + key) * D;
+        bf16* dVo = static_cast<bf16*>(a.dV) + (bg * (size_t)L + key) * D;
+        const float inv_c = 1.f / (float)C;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            floatx4 gk = dk[db] * inv_sqrt_d, gv = dv[db];
+            if (in_chunk) {
+                const int f = db * 16 + g * 4;
+                const floatx4 kh = *reinterpret_cast<const floatx4*>(a.khat_w + cv + f);
+                const floatx4 dkh = *reinterpret_cast<const floatx4*>(a.dkhat_w + cv + f);
+                const floatx4 dvh = *reinterpret_cast<const floatx4*>(a.dVs_w + cv + f);
+                gk += da * kh + dkh * inv_c;
+                gv += bj * dvh;
+            }
+            const u32x2 wk = {pack_bf16x2(gk[0], gk[1]), pack_bf16x2(gk[2], gk[3])};
+            const u32x2 wv = {pack_bf16x2(gv[0], gv[1]), pack_bf16x2(gv[2], gv[3])};
+            *reinterpret_cast<u32x2*>(dKo + db * 16 + g * 4) = wk;
+            *reinterpret_cast<u32x2*>(dVo + db * 16 + g * 4) = wv;
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
 // through the summaries, plus the window gradients, to dK and dV
 // ---------------------------------------------------------------------------
-// One 256-thread workgroup per chunk (blockIdx.x < n_chunks), or for the
-// rows after the last complete chunk (blockIdx.x == n_chunks: window part
-// only).  Thread t holds features cc*8 .. cc*8+7 (cc = t % TPR) of rows
-// r0, r0 + RPS, ... (r0 = t / TPR).  LDS: a_j (log2 units) and da_j, C floats
-// each, then the reduction scratch.
+// One 256-thread workgroup per chunk.  Thread t holds features cc*8 ..
+// cc*8+7 (cc = t % TPR) of rows r0, r0 + RPS, ... (r0 = t / TPR).  LDS: a_j
+// (log2 units), C floats, then the reduction scratch.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
     constexpr int TPR = D / 8;
     constexpr int RPS = 256 / TPR;
     extern __shared__ float smem[];
     float* logit = smem;
-    float* dal = smem + a.C;
-    float* red = smem + 2 * a.C;
+    float* red = smem + a.C;
     const int chunk = blockIdx.x;
     const size_t bg = blockIdx.y;
     const int L = a.L, C = a.C;
     const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
-    const bool tail = chunk == a.n_chunks;
     const int first = chunk * C;
-    const int rows = tail ? L - first : C;
     const bf16* K = static_cast<const bf16*>(a.K) + (bg * (size_t)L + first) * D;
     const bf16* V = static_cast<const bf16*>(a.V) + (bg * (size_t)L + first) * D;
-    const float* dKw = a.dK_w + (bg * (size_t)L + first) * D;
-    const float* dVw = a.dV_w + (bg * (size_t)L + first) * D;
-    bf16* dK = static_cast<bf16*>(a.dK) + (bg * (size_t)L + first) * D;
-    bf16* dV = static_cast<bf16*>(a.dV) + (bg * (size_t)L + first) * D;
     auto load8 = [&](const bf16* base, int r, float out[8]) {
         const u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)r * D + cc * 8);
 #pragma unroll
@@ -465,106 +494,86 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
     };
     const float sc = a.scale_log2;  // log2(e) / sqrt(d): logits in log2 units
     const float inv_sqrt_d = sc / kLog2e;
-    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, gvh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    float amax = 0.f, inv_den = 0.f;
-    if (!tail) {
-        float gkh[8];
-        const float* gk = a.dKs_w + (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
-        const float* gv = a.dVs_w + (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+    const size_t cv = (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;  // this thread's features of the chunk
+    const size_t kv = bg * (size_t)a.n_chunks * C + first;             // the chunk's first key
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, gvh[8], dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float gkh[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            gkh[i] = gk[i];
-            gvh[i] = gv[i];
-        }
-        // khat = mean key
-        for (int r = r0; r < C; r += RPS) {
-            float k[8];
-            load8(K, r, k);
+    for (int i = 0; i < 8; ++i) {
+        gkh[i] = a.dKs_w[cv + i];
+        gvh[i] = a.dVs_w[cv + i];
+    }
+    // khat = mean key
+    for (int r = r0; r < C; r += RPS) {
+        float k[8];
+        load8(K, r, k);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) kh[i] += k[i];
-        }
-        reduce_rows8<TPR>(kh, red);
+        for (int i = 0; i < 8; ++i) kh[i] += k[i];
+    }
+    reduce_rows8<TPR>(kh, red);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) kh[i] *= 1.f / (float)C;
-        // a_j and their max
-        float mx = -INFINITY;
-        for (int r = r0; r < C; r += RPS) {
-            float k[8];
-            load8(K, r, k);
-            float x = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) x += kh[i] * k[i];
-            x = row_sum(x) * sc;
-            if (cc == 0) logit[r] = x;
-            mx = fmaxf(mx, x);
-        }
-        amax = block_max(mx, red);  // also orders the logit writes before the reads
-        // vhat = sum_j b_j v_j (unnormalized) and the denominator
-        float vh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        float psum = 0.f;
-        for (int r = r0; r < C; r += RPS) {
-            float v[8];
-            load8(V, r, v);
-            const float p = fast_exp2(logit[r] - amax);
-            psum += p;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) vh[i] += p * v[i];
-        }
-#pragma unroll
-        for (int off = TPR; off < 64; off <<= 1) psum += __shfl_xor(psum, off, 64);
-        if ((t & 63) == 0) red[5 * TPR * 8 + (t >> 6)] = psum;
-        __syncthreads();
-        inv_den = 1.f / (red[5 * TPR * 8] + red[5 * TPR * 8 + 1] + red[5 * TPR * 8 + 2] + red[5 * TPR * 8 + 3]);
-        __syncthreads();
-        reduce_rows8<TPR>(vh, red);
-        // dvhat . vhat
+    for (int i = 0; i < 8; ++i) kh[i] *= 1.f / (float)C;
+    // a_j and their max
+    float mx = -INFINITY;
+    for (int r = r0; r < C; r += RPS) {
+        float k[8];
+        load8(K, r, k);
         float x = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) x += gvh[i] * vh[i] * inv_den;
-        const float gvv = row_sum(x);
-        // da_j = b_j (dvhat . v_j - dvhat . vhat); dkhat = dK^_c + sum_j da_j k_j / sqrt(d)
-        for (int r = r0; r < C; r += RPS) {
-            float v[8], k[8];
-            load8(V, r, v);
-            load8(K, r, k);
-            float y = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) y += gvh[i] * v[i];
-            y = row_sum(y);
-            const float da = fast_exp2(logit[r] - amax) * inv_den * (y - gvv);
-            if (cc == 0) dal[r] = da;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) dkh[i] += da * k[i];
-        }
-        reduce_rows8<TPR>(dkh, red);  // its barriers also order the dal writes before the reads below
-#pragma unroll
-        for (int i = 0; i < 8; ++i) dkh[i] = gkh[i] + dkh[i] * inv_sqrt_d;
+        for (int i = 0; i < 8; ++i) x += kh[i] * k[i];
+        x = row_sum(x) * sc;
+        if (cc == 0) logit[r] = x;
+        mx = fmaxf(mx, x);
     }
-    // dK_j = window part + da_j khat / sqrt(d) + dkhat / C;  dV_j = window part + b_j dvhat
-    for (int r = r0; r < rows; r += RPS) {
-        const floatx4 wk0 = *reinterpret_cast<const floatx4*>(dKw + (size_t)r * D + cc * 8);
-        const floatx4 wk1 = *reinterpret_cast<const floatx4*>(dKw + (size_t)r * D + cc * 8 + 4);
-        const floatx4 wv0 = *reinterpret_cast<const floatx4*>(dVw + (size_t)r * D + cc * 8);
-        const floatx4 wv1 = *reinterpret_cast<const floatx4*>(dVw + (size_t)r * D + cc * 8 + 4);
-        float gk[8] = {wk0[0], wk0[1], wk0[2], wk0[3], wk1[0], wk1[1], wk1[2], wk1[3]};
-        float gv[8] = {wv0[0], wv0[1], wv0[2], wv0[3], wv1[0], wv1[1], wv1[2], wv1[3]};
-        if (!tail) {
-            const float da = dal[r];
-            const float bj = fast_exp2(logit[r] - amax) * inv_den;
+    const float amax = block_max(mx, red);  // also orders the logit writes before the reads
+    // vhat = sum_j b_j v_j (unnormalized) and the denominator
+    float vh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float psum = 0.f;
+    for (int r = r0; r < C; r += RPS) {
+        float v[8];
+        load8(V, r, v);
+        const float p = fast_exp2(logit[r] - amax);
+        psum += p;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                gk[i] += da * kh[i] * inv_sqrt_d + dkh[i] * (1.f / (float)C);
-                gv[i] += bj * gvh[i];
-            }
-        }
-        u32x4 ok, ov;
+        for (int i = 0; i < 8; ++i) vh[i] += p * v[i];
+    }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ok[i] = pack_bf16x2(gk[2 * i], gk[2 * i + 1]);
-            ov[i] = pack_bf16x2(gv[2 * i], gv[2 * i + 1]);
+    for (int off = TPR; off < 64; off <<= 1) psum += __shfl_xor(psum, off, 64);
+    if ((t & 63) == 0) red[5 * TPR * 8 + (t >> 6)] = psum;
+    __syncthreads();
+    const float inv_den = 1.f / (red[5 * TPR * 8] + red[5 * TPR * 8 + 1] + red[5 * TPR * 8 + 2] + red[5 * TPR * 8 + 3]);
+    __syncthreads();
+    reduce_rows8<TPR>(vh, red);
+    // dvhat . vhat
+    float x = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x += gvh[i] * vh[i] * inv_den;
+    const float gvv = row_sum(x);
+    // b_j and da_j = b_j (dvhat . v_j - dvhat . vhat); dkhat = dK^_c + sum_j da_j k_j / sqrt(d)
+    for (int r = r0; r < C; r += RPS) {
+        float v[8], k[8];
+        load8(V, r, v);
+        load8(K, r, k);
+        float y = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) y += gvh[i] * v[i];
+        y = row_sum(y);
+        const float bj = fast_exp2(logit[r] - amax) * inv_den;
+        const float da = bj * (y - gvv);
+        if (cc == 0) {
+            a.da_w[kv + r] = da;
+            a.bw_w[kv + r] = bj;
         }
-        *reinterpret_cast<u32x4*>(dK + (size_t)r * D + cc * 8) = ok;
-        *reinterpret_cast<u32x4*>(dV + (size_t)r * D + cc * 8) = ov;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dkh[i] += da * k[i];
+    }
+    reduce_rows8<TPR>(dkh, red);
+    if (t < TPR) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            a.khat_w[cv + i] = kh[i];
+            a.dkhat_w[cv + i] = gkh[i] + dkh[i] * inv_sqrt_d;
+        }
     }
 }
 
@@ -583,14 +592,17 @@ hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
     hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     constexpr int KT = kBwdWaves * 16;
-    const int tiles = (p.L + KT - 1) / KT + (p.n_chunks + KT - 1) / KT;
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3(p.B * p.Hkv * tiles), dim3(kBwdWaves * 64), 0, stream, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const bool has_tail = p.L % p.C != 0;
-    const size_t lds = (size_t)(2 * p.C + summary_red_floats<D>()) * sizeof(float);
-    const int nx = p.n_chunks + (has_tail ? 1 : 0);
-    if (nx > 0)
-        hipLaunchKernelGGL((bwd_summary_kernel<D>), dim3(nx, p.B * p.Hkv), dim3(256), lds, stream, p);
+    if (p.n_chunks > 0) {
+        // summary gradients, then their per-chunk and per-key factors
+        const int st = (p.n_chunks + KT - 1) / KT;
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(p.B * p.Hkv * st), dim3(kBwdWaves * 64), 0, stream, p);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        const size_t lds = (size_t)(p.C + summary_red_floats<D>()) * sizeof(float);
+        hipLaunchKernelGGL((bwd_summary_kernel<D>), dim3(p.n_chunks, p.B * p.Hkv), dim3(256), lds, stream, p);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const int wt = (p.L + KT - 1) / KT;
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(p.B * p.Hkv * wt), dim3(kBwdWaves * 64), 0, stream, p);
     return hipGetLastError();
 }
 

@@ -451,18 +451,24 @@ int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const 
 
 namespace {
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+// fp32 scratch of the backward: row dots, summary gradients, and the
+// per-chunk / per-key factors through which the summaries reach dK and dV
 struct BwdLayout {
-    size_t dv, dkw, dvw, dksw, dvsw, total;
+    size_t dv, dksw, dvsw, khat, dkhat, da, bw, total;
 };
 BwdLayout bwd_layout(long long B, long long H, long long H_kv, long long L, long long d, long long C) {
     BwdLayout l;
     const long long nc = L / C;
+    const size_t vec = (size_t)(B * H_kv * nc * d) * 4;
+    const size_t key = (size_t)(B * H_kv * nc * C) * 4;
     l.dv = 0;
-    l.dkw = align256(l.dv + (size_t)(B * H * L) * 4);
-    l.dvw = align256(l.dkw + (size_t)(B * H_kv * L * d) * 4);
-    l.dksw = align256(l.dvw + (size_t)(B * H_kv * L * d) * 4);
-    l.dvsw = align256(l.dksw + (size_t)(B * H_kv * nc * d) * 4);
-    l.total = align256(l.dvsw + (size_t)(B * H_kv * nc * d) * 4);
+    l.dksw = align256(l.dv + (size_t)(B * H * L) * 4);
+    l.dvsw = align256(l.dksw + vec);
+    l.khat = align256(l.dvsw + vec);
+    l.dkhat = align256(l.khat + vec);
+    l.da = align256(l.dkhat + vec);
+    l.bw = align256(l.da + key);
+    l.total = align256(l.bw + key);
     return l;
 }
 }  // namespace
@@ -503,10 +509,12 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
     p.dK = dK;
     p.dV = dV;
     p.Dv = reinterpret_cast<float*>(w + lay.dv);
-    p.dK_w = reinterpret_cast<float*>(w + lay.dkw);
-    p.dV_w = reinterpret_cast<float*>(w + lay.dvw);
     p.dKs_w = reinterpret_cast<float*>(w + lay.dksw);
     p.dVs_w = reinterpret_cast<float*>(w + lay.dvsw);
+    p.khat_w = reinterpret_cast<float*>(w + lay.khat);
+    p.dkhat_w = reinterpret_cast<float*>(w + lay.dkhat);
+    p.da_w = reinterpret_cast<float*>(w + lay.da);
+    p.bw_w = reinterpret_cast<float*>(w + lay.bw);
     p.B = B;
     p.H = H;
     p.Hkv = H_kv;

@@ -58,11 +58,13 @@ struct BwdParams {
     void* dQ;
     void* dK;
     void* dV;
-    float* Dv;     // [B][H][L]   dO . O
-    float* dK_w;   // [B][Hkv][L][d]   window parts
-    float* dV_w;
-    float* dKs_w;  // [B][Hkv][n_chunks][d]   gradients of the summary keys / values
+    float* Dv;       // [B][H][L]   dO . O
+    float* dKs_w;    // [B][Hkv][n_chunks][d]   gradients of the summary keys / values
     float* dVs_w;
+    float* khat_w;   // [B][Hkv][n_chunks][d]   mean key of each chunk
+    float* dkhat_w;  // [B][Hkv][n_chunks][d]   total gradient of that mean key
+    float* da_w;     // [B][Hkv][n_chunks * C]  gradient of each key's chunk-softmax logit
+    float* bw_w;     // [B][Hkv][n_chunks * C]  each key's chunk-softmax weight
     int B, H, Hkv, L, W, C, n_chunks;
     float scale_log2;  // log2(e) / sqrt(d)
     float log2C;
