@@ -43,7 +43,27 @@ namespace eva {
 namespace {
 
 constexpr int kBwdWaves = 4;
-constexpr int kBwdBN = 32;  // rows per streamed block
+constexpr int kBwdBN = 32;     // rows per streamed block
+constexpr int kBwdNS = 4;      // LDS ring stages
+constexpr int kBwdAhead = 3;   // blocks requested ahead of the one computed
+
+// s_waitcnt vmcnt(N) lgkmcnt(0): the kernel's own DMA requests are invisible
+// to the compiler, so every wait for them is explicit
+template <int N>
+__device__ __forceinline__ void bwait_vm() {
+    static_assert(N < 64, "vmcnt field is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+// wait for a block (LATER DMA instructions issued after it may stay in
+// flight), then a workgroup barrier: the block is visible to every wave, and
+// every wave is done with the stage the next request refills
+template <int LATER>
+__device__ __forceinline__ void bsync() {
+    asm volatile("" ::: "memory");
+    bwait_vm<LATER>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 template <int D>
 struct BCfg {
@@ -81,12 +101,14 @@ struct Stager {
         }
     }
     // rows [0, n_valid) of `src` (row-major, D bf16 each) into the LDS block at
-    // lds_addr; rows past n_valid repeat the last valid row (finite, masked)
-    __device__ void issue(const bf16* src, int n_valid, unsigned lds_addr, int wave) const {
+    // lds_addr; rows past n_valid repeat the last valid row (finite, masked).
+    // With real false the same number of instructions read row 0 of src into
+    // the 1-KB area at lds_addr (requests past the last block).
+    __device__ void issue(const bf16* src, int n_valid, unsigned lds_addr, int wave, bool real = true) const {
 #pragma unroll
         for (int i = 0; i < Cfg::NI; ++i) {
-            const int r = min(row[i], n_valid - 1);
-            bdma16(src, (unsigned)(r * Cfg::ROWB + off[i]), lds_addr + (i * kBwdWaves + wave) * 1024);
+            const int r = real ? min(row[i], n_valid - 1) : 0;
+            bdma16(src, (unsigned)(r * Cfg::ROWB + off[i]), real ? lds_addr + (i * kBwdWaves + wave) * 1024 : lds_addr);
         }
     }
 };
@@ -161,7 +183,8 @@ template <int D>
 __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2][BLK];  // [stage][K, V]
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[kBwdNS][2][BLK];  // [stage][K, V]
+    __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
     const int L = a.L, W = a.W, C = a.C;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -216,27 +239,39 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db) acc[db][0] = acc[db][1] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+    // block j of the plan into stage j % NS; past the last block the same
+    // number of DMA instructions go to the dummy area
     const Stager<D> st(wave, lane);
+    constexpr int REQ = 2 * Cfg::NI;  // DMA instructions per request and wave
     auto stage = [&](int j) {
+        const bool real = j < nb;
         const bool sum = j < nsb;
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
         const int lim = sum ? a.n_chunks : L;
         const int nv = min(kBwdBN, lim - base);
-        st.issue((sum ? Ksbg : Kbg) + (size_t)base * D, nv, lds_addr_of<D>(lds[j & 1][0]), wave);
-        st.issue((sum ? Vsbg : Vbg) + (size_t)base * D, nv, lds_addr_of<D>(lds[j & 1][1]), wave);
+        const bf16* ksrc = real ? (sum ? Ksbg : Kbg) + (size_t)base * D : Kbg;
+        const bf16* vsrc = real ? (sum ? Vsbg : Vbg) + (size_t)base * D : Vbg;
+        st.issue(ksrc, nv, lds_addr_of<D>(real ? lds[j & (kBwdNS - 1)][0] : dummy), wave, real);
+        st.issue(vsrc, nv, lds_addr_of<D>(real ? lds[j & (kBwdNS - 1)][1] : dummy), wave, real);
     };
-    if (nb > 0) stage(0);
+#pragma unroll
+    for (int k = 0; k < kBwdAhead; ++k) stage(k);
+    // the stationary fragments (plain loads) and the first blocks: the
+    // compiler does not count the DMA requests, so its own wait for the
+    // fragments would otherwise sit inside the loop and drain every request
+    bwait_vm<0>();
     for (int j = 0; j < nb; ++j) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();  // block j landed; every wave is done with block j-1's stage
-        if (j + 1 < nb) stage(j + 1);
+        // block j landed (the two requested after it may be in flight); the
+        // request below refills the stage of block j-1
+        bsync<(kBwdAhead - 1) * REQ>();
+        stage(j + kBwdAhead);
         const bool sum = j < nsb;
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
         const bool needed =
             w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
         if (!needed) continue;
-        const unsigned char* ks = lds[j & 1][0];
-        const unsigned char* vs = lds[j & 1][1];
+        const unsigned char* ks = lds[j & (kBwdNS - 1)][0];
+        const unsigned char* vs = lds[j & (kBwdNS - 1)][1];
         // S^T and dP^T: rows = keys base + kb*16 + 4g + i, column = query c16
         floatx4 s[2][2], dp[2][2];
 #pragma unroll
@@ -282,6 +317,8 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         }
     }
 
+    bwait_vm<0>();  // no request may still be writing LDS when the workgroup ends
+
     // dQ = acc / sqrt(d): lane (g, c16) holds features db*16 + 4g .. +3 of column c16
     const float inv_sqrt_d = a.scale_log2 / kLog2e;
     bf16* dQ = static_cast<bf16*>(a.dQ);
@@ -307,7 +344,9 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
     constexpr int KT = kBwdWaves * 16;  // keys per workgroup
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2][BLK];  // [stage][Q, dO]
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[kBwdNS][2][BLK];  // [stage][Q, dO]
+    __shared__ __attribute__((aligned(256))) float rowf[kBwdNS][2][64];            // [stage][lse, D] of its rows
+    __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
     const int L = a.L, W = a.W, C = a.C;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -315,9 +354,13 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
     const int g = lane >> 4, c16 = lane & 15;
     // key tiles per (b, kv head): summaries, or window keys
     constexpr bool sum = SUM;
-    const int per_bg = SUM ? (a.n_chunks + KT - 1) / KT : (L + KT - 1) / KT;
+    // summary tiles: n_split workgroups per tile, each over a part of the
+    // query range, leaving partial sums
+    const int n_split = SUM ? a.n_split : 1;
+    const int per_bg = (SUM ? (a.n_chunks + KT - 1) / KT : (L + KT - 1) / KT) * n_split;
     const int bgi = (int)blockIdx.x / per_bg;
-    const int t = (int)blockIdx.x % per_bg;
+    const int t = (int)blockIdx.x % per_bg / n_split;
+    const int sp = (int)blockIdx.x % n_split;
     const size_t bg = (size_t)bgi;
     const int b = bgi / a.Hkv, kvh = bgi % a.Hkv;
     const int G = a.H / a.Hkv;
@@ -356,35 +399,60 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
     const float bias = sum ? a.log2C : 0.f;
 
     const Stager<D> stg(wave, lane);
-    const int steps = nqb * G;  // (head, query block) pairs
+    // (head, query block) pairs [j0, j0 + steps) of the nqb * G the tile sees
+    const int all_steps = nqb * G;
+    const int j0 = (int)((long long)all_steps * sp / n_split);
+    const int steps = (int)((long long)all_steps * (sp + 1) / n_split) - j0;
+    // request of step j: its Q and dO rows (stage j % NS), and their lse and D
+    // (one 4-B DMA instruction each, by waves 0 and 1; waves 2 and 3 issue one
+    // into the dummy area so that every wave counts the same instructions)
+    constexpr int REQ = 2 * Cfg::NI + 1;
     auto stage = [&](int j) {
-        const int hh = j / nqb, qb = qb0 + j % nqb;
-        const size_t rowb = ((size_t)b * a.H + kvh * G + hh) * L + (size_t)qb * kBwdBN;
+        const bool real = j < steps;
+        // past the last step: row 0 of the group's first head (always valid)
+        const int hh = real ? (j0 + j) / nqb : 0, qb = real ? qb0 + (j0 + j) % nqb : 0;
+        const size_t rowh = ((size_t)b * a.H + kvh * G + hh) * L;
+        const size_t rowb = rowh + (size_t)qb * kBwdBN;
         const int nv = min(kBwdBN, L - qb * kBwdBN);
-        stg.issue(static_cast<const bf16*>(a.Q) + rowb * D, nv, lds_addr_of<D>(lds[j & 1][0]), wave);
-        stg.issue(static_cast<const bf16*>(a.dO) + rowb * D, nv, lds_addr_of<D>(lds[j & 1][1]), wave);
+        const int st_i = j & (kBwdNS - 1);
+        stg.issue(static_cast<const bf16*>(a.Q) + rowb * D, nv, lds_addr_of<D>(real ? lds[st_i][0] : dummy), wave, real);
+        stg.issue(static_cast<const bf16*>(a.dO) + rowb * D, nv, lds_addr_of<D>(real ? lds[st_i][1] : dummy), wave,
+                  real);
+        const bool mine = real && wave < 2;
+        const float* src = wave == 1 ? a.Dv : a.lse;
+        const unsigned voff = (unsigned)(mine ? min(lane, nv - 1) : 0) * 4u;
+        const unsigned dst = mine ? lds_addr_of<D>(rowf[st_i][wave]) : lds_addr_of<D>(dummy);
+        asm volatile("global_load_lds_dword %0, %1" ::"v"(voff), "s"(src + rowb),
+                     "{m0}"(__builtin_amdgcn_readfirstlane(dst))
+                     : "memory");
     };
-    if (steps > 0) stage(0);
+#pragma unroll
+    for (int k = 0; k < kBwdAhead; ++k) stage(k);
+    // see bwd_dq_kernel: the stationary fragments are waited for here
+    bwait_vm<0>();
     for (int j = 0; j < steps; ++j) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (j + 1 < steps) stage(j + 1);
-        const int hh = j / nqb, qb = qb0 + j % nqb;
+        // step j's rows landed (the two requests after it may be in flight);
+        // the request below refills the stage of step j-1
+        bsync<(kBwdAhead - 1) * REQ>();
+        stage(j + kBwdAhead);
+        const int qb = qb0 + (j0 + j) % nqb;
         const int r0 = qb * kBwdBN;
         if (!w_active || r0 > wr_hi || r0 + kBwdBN - 1 < wr_lo) continue;
-        const size_t rowh = ((size_t)b * a.H + kvh * G + hh) * L;
+        const int st_i = j & (kBwdNS - 1);
         // lse and D of this lane's 8 query rows r0 + 16 kb + 4g + i
         float lse2[2][4], dq[2][4];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) {
+            const floatx4 l4 = *reinterpret_cast<const floatx4*>(&rowf[st_i][0][kb * 16 + g * 4]);
+            const floatx4 d4 = *reinterpret_cast<const floatx4*>(&rowf[st_i][1][kb * 16 + g * 4]);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int n = min(r0 + kb * 16 + g * 4 + i, L - 1);
-                lse2[kb][i] = a.lse[rowh + n] * kLog2e;
-                dq[kb][i] = a.Dv[rowh + n];
+                lse2[kb][i] = l4[i] * kLog2e;
+                dq[kb][i] = d4[i];
             }
-        const unsigned char* qs = lds[j & 1][0];
-        const unsigned char* gs = lds[j & 1][1];
+        }
+        const unsigned char* qs = lds[st_i][0];
+        const unsigned char* gs = lds[st_i][1];
         // S and dP: rows = queries r0 + kb*16 + 4g + i, column = key c16
         floatx4 s[2], dp[2];
         s[0] = s[1] = dp[0] = dp[1] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -415,12 +483,14 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
         }
     }
 
+    bwait_vm<0>();  // no request may still be writing LDS when the workgroup ends
     if (key >= lim) return;
     const float inv_sqrt_d = a.scale_log2 / kLog2e;
     if constexpr (SUM) {
-        // fp32 summary gradients, for the per-chunk pass
-        float* dKo = a.dKs_w + (bg * (size_t)lim + key) * D;
-        float* dVo = a.dVs_w + (bg * (size_t)lim + key) * D;
+        // fp32 partial summary gradients, for the per-chunk pass
+        const size_t slot = (size_t)sp * a.B * a.Hkv * lim;
+        float* dKo = a.dKs_w + (slot + bg * (size_t)lim + key) * D;
+        float* dVo = a.dVs_w + (slot + bg * (size_t)lim + key) * D;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
             *reinterpret_cast<floatx4*>(dKo + db * 16 + g * 4) = dk[db] * inv_sqrt_d;
@@ -464,7 +534,8 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
 // ---------------------------------------------------------------------------
 // One 256-thread workgroup per chunk.  Thread t holds features cc*8 ..
 // cc*8+7 (cc = t % TPR) of rows r0, r0 + RPS, ... (r0 = t / TPR).  LDS: a_j
-// (log2 units), C floats, then the reduction scratch.
+// (log2 units), C floats, the reduction scratch, then the chunk's summary
+// gradients (2 D floats).
 template <int D>
 __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
     constexpr int TPR = D / 8;
@@ -497,11 +568,23 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
     const size_t cv = (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;  // this thread's features of the chunk
     const size_t kv = bg * (size_t)a.n_chunks * C + first;             // the chunk's first key
     float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, gvh[8], dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    // summary gradients: sums of the partials of the query-range splits,
+    // formed once per feature (threads t < 2 D / 4: four features of dK^ or
+    // dV^ each) and shared through LDS
+    float* gsh = smem + ((a.C + summary_red_floats<D>() + 3) & ~3);  // [dK^ | dV^], 2 D floats, 16-B aligned
+    if (t < 2 * D / 4) {
+        const float* src = (t < D / 4 ? a.dKs_w : a.dVs_w) + (bg * (size_t)a.n_chunks + chunk) * D + (t % (D / 4)) * 4;
+        const size_t slot = (size_t)a.B * a.Hkv * a.n_chunks * D;
+        floatx4 acc4 = *reinterpret_cast<const floatx4*>(src);
+        for (int sp = 1; sp < a.n_split; ++sp) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
+        *reinterpret_cast<floatx4*>(gsh + t * 4) = acc4;
+    }
+    __syncthreads();
     float gkh[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        gkh[i] = a.dKs_w[cv + i];
-        gvh[i] = a.dVs_w[cv + i];
+        gkh[i] = gsh[cc * 8 + i];
+        gvh[i] = gsh[D + cc * 8 + i];
     }
     // khat = mean key
     for (int r = r0; r < C; r += RPS) {
@@ -567,12 +650,147 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) dkh[i] += da * k[i];
     }
-    reduce_rows8<TPR>(dkh, red);
+    reduce_rows8<TPR>(dkh, red);  // its barriers also order every thread's reads of slot 0 before the write
     if (t < TPR) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             a.khat_w[cv + i] = kh[i];
             a.dkhat_w[cv + i] = gkh[i] + dkh[i] * inv_sqrt_d;
+            a.dVs_w[cv + i] = gvh[i];  // the total dvhat, for the window tiles
+        }
+    }
+}
+
+// Register-resident variant for chunks of exactly ROWS * RPS rows: every
+// thread loads its key and value rows once, and the passes over the chunk
+// run on registers (one memory latency per chunk instead of one per pass).
+template <int D, int ROWS>
+__global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
+    constexpr int TPR = D / 8;
+    constexpr int RPS = 256 / TPR;
+    constexpr int C = ROWS * RPS;
+    __shared__ float red[summary_red_floats<D>()];
+    __shared__ __attribute__((aligned(16))) float gsh[2 * D];  // [dK^ | dV^] of the chunk
+    const int chunk = blockIdx.x;
+    const size_t bg = blockIdx.y;
+    const int L = a.L;
+    const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
+    const int first = chunk * C;
+    const bf16* K = static_cast<const bf16*>(a.K) + (bg * (size_t)L + first + r0) * D + cc * 8;
+    const bf16* V = static_cast<const bf16*>(a.V) + (bg * (size_t)L + first + r0) * D + cc * 8;
+    u32x4 kw[ROWS], vw[ROWS];
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        kw[i] = *reinterpret_cast<const u32x4*>(K + (size_t)i * RPS * D);
+        vw[i] = *reinterpret_cast<const u32x4*>(V + (size_t)i * RPS * D);
+    }
+    auto unpack = [&](const u32x4& w, float out[8]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            out[2 * e] = bf16_lo(w[e]);
+            out[2 * e + 1] = bf16_hi(w[e]);
+        }
+    };
+    auto row_sum = [&](float x) {
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
+        return x;
+    };
+    const float sc = a.scale_log2;  // log2(e) / sqrt(d): logits in log2 units
+    const float inv_sqrt_d = sc / kLog2e;
+    // summary gradients: sums of the partials of the query-range splits
+    if (t < 2 * D / 4) {
+        const float* src = (t < D / 4 ? a.dKs_w : a.dVs_w) + (bg * (size_t)a.n_chunks + chunk) * D + (t % (D / 4)) * 4;
+        const size_t slot = (size_t)a.B * a.Hkv * a.n_chunks * D;
+        floatx4 acc4 = *reinterpret_cast<const floatx4*>(src);
+        for (int sp = 1; sp < a.n_split; ++sp) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
+        *reinterpret_cast<floatx4*>(gsh + t * 4) = acc4;
+    }
+    // khat = mean key
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] += k[e];
+    }
+    reduce_rows8<TPR>(kh, red);  // its barriers also publish gsh
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kh[e] *= 1.f / (float)C;
+    float gkh[8], gvh[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        gkh[e] = gsh[cc * 8 + e];
+        gvh[e] = gsh[D + cc * 8 + e];
+    }
+    // logits (log2 units) and their max
+    float sl[ROWS];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x += kh[e] * k[e];
+        sl[i] = row_sum(x) * sc;
+        mx = fmaxf(mx, sl[i]);
+    }
+    const float amax = block_max(mx, red);
+    // vhat = sum_j b_j v_j (unnormalized) and the denominator
+    float vh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float v[8];
+        unpack(vw[i], v);
+        sl[i] = fast_exp2(sl[i] - amax);
+        psum += sl[i];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vh[e] += sl[i] * v[e];
+    }
+#pragma unroll
+    for (int off = TPR; off < 64; off <<= 1) psum += __shfl_xor(psum, off, 64);
+    if ((t & 63) == 0) red[5 * TPR * 8 + (t >> 6)] = psum;
+    __syncthreads();
+    const float inv_den = 1.f / (red[5 * TPR * 8] + red[5 * TPR * 8 + 1] + red[5 * TPR * 8 + 2] + red[5 * TPR * 8 + 3]);
+    __syncthreads();
+    reduce_rows8<TPR>(vh, red);
+    // dvhat . vhat
+    float x = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x += gvh[e] * vh[e] * inv_den;
+    const float gvv = row_sum(x);
+    // b_j, da_j = b_j (dvhat . v_j - dvhat . vhat); dkhat = dK^_c + sum_j da_j k_j / sqrt(d)
+    const size_t kv = bg * (size_t)a.n_chunks * C + first + r0;
+    float dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float v[8], k[8];
+        unpack(vw[i], v);
+        unpack(kw[i], k);
+        float y = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y += gvh[e] * v[e];
+        y = row_sum(y);
+        const float bj = sl[i] * inv_den;
+        const float da = bj * (y - gvv);
+        if (cc == 0) {
+            a.da_w[kv + (size_t)i * RPS] = da;
+            a.bw_w[kv + (size_t)i * RPS] = bj;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dkh[e] += da * k[e];
+    }
+    reduce_rows8<TPR>(dkh, red);
+    if (t < TPR) {
+        const size_t cv = (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            a.khat_w[cv + e] = kh[e];
+            a.dkhat_w[cv + e] = gkh[e] + dkh[e] * inv_sqrt_d;
+            a.dVs_w[cv + e] = gvh[e];  // the total dvhat, for the window tiles
         }
     }
 }
@@ -594,11 +812,21 @@ hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
     constexpr int KT = kBwdWaves * 16;
     if (p.n_chunks > 0) {
         // summary gradients, then their per-chunk and per-key factors
-        const int st = (p.n_chunks + KT - 1) / KT;
+        const int st = (p.n_chunks + KT - 1) / KT * p.n_split;
         hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(p.B * p.Hkv * st), dim3(kBwdWaves * 64), 0, stream, p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        const size_t lds = (size_t)(p.C + summary_red_floats<D>()) * sizeof(float);
-        hipLaunchKernelGGL((bwd_summary_kernel<D>), dim3(p.n_chunks, p.B * p.Hkv), dim3(256), lds, stream, p);
+        constexpr int RPS = 256 / (D / 8);
+        const dim3 grid(p.n_chunks, p.B * p.Hkv);
+        switch (p.C % RPS == 0 ? p.C / RPS : 0) {
+            case 1: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 1>), grid, dim3(256), 0, stream, p); break;
+            case 2: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 2>), grid, dim3(256), 0, stream, p); break;
+            case 4: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 4>), grid, dim3(256), 0, stream, p); break;
+            case 8: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 8>), grid, dim3(256), 0, stream, p); break;
+            default: {
+                const size_t lds = (size_t)(((p.C + summary_red_floats<D>() + 3) & ~3) + 2 * D) * sizeof(float);
+                hipLaunchKernelGGL((bwd_summary_kernel<D>), grid, dim3(256), lds, stream, p);
+            }
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const int wt = (p.L + KT - 1) / KT;

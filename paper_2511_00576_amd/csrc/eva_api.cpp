@@ -461,10 +461,11 @@ BwdLayout bwd_layout(long long B, long long H, long long H_kv, long long L, long
     const long long nc = L / C;
     const size_t vec = (size_t)(B * H_kv * nc * d) * 4;
     const size_t key = (size_t)(B * H_kv * nc * C) * 4;
+    const size_t split = (size_t)eva::bwd_summary_splits(B, H_kv, L, C, H / H_kv);
     l.dv = 0;
     l.dksw = align256(l.dv + (size_t)(B * H * L) * 4);
-    l.dvsw = align256(l.dksw + vec);
-    l.khat = align256(l.dvsw + vec);
+    l.dvsw = align256(l.dksw + split * vec);
+    l.khat = align256(l.dvsw + split * vec);
     l.dkhat = align256(l.khat + vec);
     l.da = align256(l.dkhat + vec);
     l.bw = align256(l.da + key);
@@ -522,6 +523,7 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
     p.W = W;
     p.C = C;
     p.n_chunks = n_chunks;
+    p.n_split = eva::bwd_summary_splits(B, H_kv, L, C, H / H_kv);
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
     hipStream_t s = static_cast<hipStream_t>(stream);

@@ -59,16 +59,29 @@ struct BwdParams {
     void* dK;
     void* dV;
     float* Dv;       // [B][H][L]   dO . O
-    float* dKs_w;    // [B][Hkv][n_chunks][d]   gradients of the summary keys / values
-    float* dVs_w;
+    float* dKs_w;    // [n_split][B][Hkv][n_chunks][d]   partial gradients of the summary keys / values
+    float* dVs_w;    //   (slot 0 of dVs_w holds their sum once the per-chunk pass ran)
     float* khat_w;   // [B][Hkv][n_chunks][d]   mean key of each chunk
     float* dkhat_w;  // [B][Hkv][n_chunks][d]   total gradient of that mean key
     float* da_w;     // [B][Hkv][n_chunks * C]  gradient of each key's chunk-softmax logit
     float* bw_w;     // [B][Hkv][n_chunks * C]  each key's chunk-softmax weight
     int B, H, Hkv, L, W, C, n_chunks;
+    int n_split;       // query-range splits of each summary-key tile
     float scale_log2;  // log2(e) / sqrt(d)
     float log2C;
 };
+
+// Splits of the query range of each summary-key tile of the backward (a
+// function of the shapes only, so that the workspace size can use it).
+inline int bwd_summary_splits(long long B, long long Hkv, long long L, long long C, long long G) {
+    const long long tiles = B * Hkv * ((L / C + 63) / 64);
+    if (tiles <= 0) return 1;
+    long long s = (2048 + tiles - 1) / tiles;              // about 2048 workgroups
+    const long long by_len = ((L + 31) / 32) * G / 8;      // at least ~8 query blocks each
+    if (s > by_len) s = by_len;
+    if (s > 16) s = 16;
+    return s < 1 ? 1 : (int)s;
+}
 
 template <int D>
 hipError_t launch_backward(const BwdParams& p, hipStream_t stream);

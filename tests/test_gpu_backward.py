@@ -43,6 +43,9 @@ SHAPES = [
     (1, 2, 2, 100, 128, 10, 128),   # C > L: no chunk
     (2, 2, 1, 17, 128, 5, 3),       # shorter than one block
     (1, 16, 2, 300, 128, 48, 32),   # G = 8
+    (1, 4, 2, 400, 128, 96, 64),    # chunk of 4 rows per thread in the per-chunk pass
+    (1, 2, 1, 333, 64, 50, 32),     # d = 64, one row per thread in the per-chunk pass
+    (1, 2, 2, 260, 128, 32, 16),    # d = 128, one row per thread in the per-chunk pass
 ]
 
 
