@@ -44,8 +44,12 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdBN = 32;     // rows per streamed block
-constexpr int kBwdNS = 4;      // LDS ring stages
-constexpr int kBwdAhead = 3;   // blocks requested ahead of the one computed
+// LDS ring stages and blocks requested ahead of the one computed: dQ keeps
+// four stages at two waves per SIMD (its fragments need ~256 VGPRs); dK/dV
+// fits 168 VGPRs, so three stages (50 KB) let three workgroups share a CU
+// (measured on MI355X: 631 vs 767 us for the window tiles of the LLM workload)
+constexpr int kDqNS = 4, kDqAhead = 3;
+constexpr int kKvNS = 3, kKvAhead = 2;
 
 // s_waitcnt vmcnt(N) lgkmcnt(0): the kernel's own DMA requests are invisible
 // to the compiler, so every wait for them is explicit
@@ -183,7 +187,7 @@ template <int D>
 __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[kBwdNS][2][BLK];  // [stage][K, V]
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[kDqNS][2][BLK];  // [stage][K, V]
     __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
     const int L = a.L, W = a.W, C = a.C;
@@ -251,11 +255,11 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         const int nv = min(kBwdBN, lim - base);
         const bf16* ksrc = real ? (sum ? Ksbg : Kbg) + (size_t)base * D : Kbg;
         const bf16* vsrc = real ? (sum ? Vsbg : Vbg) + (size_t)base * D : Vbg;
-        st.issue(ksrc, nv, lds_addr_of<D>(real ? lds[j & (kBwdNS - 1)][0] : dummy), wave, real);
-        st.issue(vsrc, nv, lds_addr_of<D>(real ? lds[j & (kBwdNS - 1)][1] : dummy), wave, real);
+        st.issue(ksrc, nv, lds_addr_of<D>(real ? lds[j & (kDqNS - 1)][0] : dummy), wave, real);
+        st.issue(vsrc, nv, lds_addr_of<D>(real ? lds[j & (kDqNS - 1)][1] : dummy), wave, real);
     };
 #pragma unroll
-    for (int k = 0; k < kBwdAhead; ++k) stage(k);
+    for (int k = 0; k < kDqAhead; ++k) stage(k);
     // the stationary fragments (plain loads) and the first blocks: the
     // compiler does not count the DMA requests, so its own wait for the
     // fragments would otherwise sit inside the loop and drain every request
@@ -263,15 +267,15 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
     for (int j = 0; j < nb; ++j) {
         // block j landed (the two requested after it may be in flight); the
         // request below refills the stage of block j-1
-        bsync<(kBwdAhead - 1) * REQ>();
-        stage(j + kBwdAhead);
+        bsync<(kDqAhead - 1) * REQ>();
+        stage(j + kDqAhead);
         const bool sum = j < nsb;
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
         const bool needed =
             w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
         if (!needed) continue;
-        const unsigned char* ks = lds[j & (kBwdNS - 1)][0];
-        const unsigned char* vs = lds[j & (kBwdNS - 1)][1];
+        const unsigned char* ks = lds[j & (kDqNS - 1)][0];
+        const unsigned char* vs = lds[j & (kDqNS - 1)][1];
         // S^T and dP^T: rows = keys base + kb*16 + 4g + i, column = query c16
         floatx4 s[2][2], dp[2][2];
 #pragma unroll
@@ -340,12 +344,12 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
 // dK, dV of window keys and of summaries
 // ---------------------------------------------------------------------------
 template <int D, bool SUM>
-__global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
+__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(3, 3))) void bwd_dkdv_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
     constexpr int KT = kBwdWaves * 16;  // keys per workgroup
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[kBwdNS][2][BLK];  // [stage][Q, dO]
-    __shared__ __attribute__((aligned(256))) float rowf[kBwdNS][2][64];            // [stage][lse, D] of its rows
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[kKvNS][2][BLK];  // [stage][Q, dO]
+    __shared__ __attribute__((aligned(256))) float rowf[kKvNS][2][64];            // [stage][lse, D] of its rows
     __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
     const int L = a.L, W = a.W, C = a.C;
@@ -414,7 +418,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
         const size_t rowh = ((size_t)b * a.H + kvh * G + hh) * L;
         const size_t rowb = rowh + (size_t)qb * kBwdBN;
         const int nv = min(kBwdBN, L - qb * kBwdBN);
-        const int st_i = j & (kBwdNS - 1);
+        const int st_i = j % kKvNS;
         stg.issue(static_cast<const bf16*>(a.Q) + rowb * D, nv, lds_addr_of<D>(real ? lds[st_i][0] : dummy), wave, real);
         stg.issue(static_cast<const bf16*>(a.dO) + rowb * D, nv, lds_addr_of<D>(real ? lds[st_i][1] : dummy), wave,
                   real);
@@ -427,18 +431,18 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dkdv_kernel(BwdParams a) {
                      : "memory");
     };
 #pragma unroll
-    for (int k = 0; k < kBwdAhead; ++k) stage(k);
+    for (int k = 0; k < kKvAhead; ++k) stage(k);
     // see bwd_dq_kernel: the stationary fragments are waited for here
     bwait_vm<0>();
     for (int j = 0; j < steps; ++j) {
-        // step j's rows landed (the two requests after it may be in flight);
-        // the request below refills the stage of step j-1
-        bsync<(kBwdAhead - 1) * REQ>();
-        stage(j + kBwdAhead);
+        // step j's rows landed (the request after it may be in flight); the
+        // request below refills the stage of step j-1
+        bsync<(kKvAhead - 1) * REQ>();
+        stage(j + kKvAhead);
         const int qb = qb0 + (j0 + j) % nqb;
         const int r0 = qb * kBwdBN;
         if (!w_active || r0 > wr_hi || r0 + kBwdBN - 1 < wr_lo) continue;
-        const int st_i = j & (kBwdNS - 1);
+        const int st_i = j % kKvNS;
         // lse and D of this lane's 8 query rows r0 + 16 kb + 4g + i
         float lse2[2][4], dq[2][4];
 #pragma unroll
