@@ -9,8 +9,8 @@
 // attention matrix is stored).
 //
 // Kernels (all bf16 storage, fp32 arithmetic, v_mfma_f32_16x16x32_bf16):
-//   bwd_dot_kernel     D = rowwise dO . O
-//   bwd_dq_kernel      per query tile (4 waves x 32 columns of one head), key
+//   bwd_dq_kernel      per query tile (4 waves x 32 columns of one head): the
+//                      columns' D = dO . O (stored for the dK/dV kernels), then key
 //                      blocks of 32 rows (summaries then window band) streamed
 //                      through LDS: S^T = K Q^T, dP^T = V dO^T, dS^T, and
 //                      dQ^T += K^T dS^T (K^T by the transposing LDS read)
@@ -160,27 +160,6 @@ __device__ __forceinline__ bf16x8 pair_to_b(const floatx4& t0, const floatx4& t1
 }
 
 // ---------------------------------------------------------------------------
-// D = rowwise dO . O
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(256) void bwd_dot_kernel(const bf16* __restrict__ dO, const bf16* __restrict__ O,
-                                                      float* __restrict__ Dv, long long rows) {
-    constexpr int TPR = D / 8;
-    const long long r = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-    const int cc = threadIdx.x % TPR;
-    float s = 0.f;
-    if (r < rows) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(dO + r * D + cc * 8);
-        const u32x4 b = *reinterpret_cast<const u32x4*>(O + r * D + cc * 8);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s += bf16_lo(a[i]) * bf16_lo(b[i]) + bf16_hi(a[i]) * bf16_hi(b[i]);
-    }
-#pragma unroll
-    for (int off = 1; off < TPR; off <<= 1) s += __shfl_xor(s, off, 64);
-    if (r < rows && cc == 0) Dv[r] = s;
-}
-
-// ---------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------
 template <int D>
@@ -230,13 +209,21 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         col_s[cb] = visible_summaries(n, W, C);
         const bf16* qrow = static_cast<const bf16*>(a.Q) + (row0 + n) * D;
         const bf16* grow = static_cast<const bf16*>(a.dO) + (row0 + n) * D;
+        const bf16* orow = static_cast<const bf16*>(a.O) + (row0 + n) * D;
+        // D = dO . O of the column: this lane's 8 NDC features, then the four
+        // lanes (g) of the column; stored for the dK/dV kernels
+        float dot = 0.f;
 #pragma unroll
         for (int dc = 0; dc < NDC; ++dc) {
             qf[cb][dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
             gf[cb][dc] = *reinterpret_cast<const bf16x8*>(grow + dc * 32 + g * 8);
+            const bf16x8 of = *reinterpret_cast<const bf16x8*>(orow + dc * 32 + g * 8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dot += (float)gf[cb][dc][e] * (float)of[e];
         }
+        dcol[cb] = xgroup_sum(dot);
+        if (g == 0 && col_n[cb] < L) a.Dv[row0 + n] = dcol[cb];
         lse2[cb] = a.lse[row0 + n] * kLog2e;
-        dcol[cb] = a.Dv[row0 + n];
     }
 
     floatx4 acc[NDB][2];
@@ -803,16 +790,11 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
 
 template <int D>
 hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
-    // D = rowwise dO . O
-    const long long rows = (long long)p.B * p.H * p.L;
-    constexpr int RPB = 256 / (D / 8);
-    hipLaunchKernelGGL((bwd_dot_kernel<D>), dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), 0, stream,
-                       static_cast<const bf16*>(p.dO), static_cast<const bf16*>(p.O), p.Dv, rows);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // dQ, and the row dots D = dO . O the dK/dV kernels read
     const int n_pt = (p.L + kBwdWaves * 32 - 1) / (kBwdWaves * 32);
     hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64), 0, stream, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     constexpr int KT = kBwdWaves * 16;
     if (p.n_chunks > 0) {
         // summary gradients, then their per-chunk and per-key factors
