@@ -235,7 +235,10 @@ size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d
  * Load a decode cache from a prefilled sequence of L tokens: the last
  * min(L, R) keys/values go to ring slots p mod R and the L / C summaries
  * (as built by eva_build_summaries) to the summary arrays; n_tok becomes L.
- * Errors: INVALID (malformed cache, null pointers), CAPACITY (S_max < L / C).
+ * K, V [H_kv][L][d] per batch row as in eva_prefill; all four device
+ * pointers 16-byte aligned.
+ * Errors: INVALID (malformed cache, null or misaligned pointers), CAPACITY
+ * (S_max < L / C).
  */
 int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum,
                    int L, void* stream);
@@ -322,8 +325,9 @@ typedef struct eva_rcache {
  * [B], the valid length of each sequence; a length is clamped to
  * [0, min(L, max_tok)].  For each b the last min(len, R) positions go to the
  * ring, summaries c < len / C to the summary arrays, and n_tok[b] = len.
- * Errors: INVALID (malformed cache, null pointers, L < 1), CAPACITY
- * (S_max < min(L, max_tok) / C).
+ * K, V, Ksum, Vsum 16-byte aligned.
+ * Errors: INVALID (malformed cache, null or misaligned pointers, L < 1),
+ * CAPACITY (S_max < min(L, max_tok) / C).
  */
 int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const void* Ksum, const void* Vsum,
                     int L, const int* lens, void* stream);

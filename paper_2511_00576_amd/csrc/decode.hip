@@ -74,6 +74,33 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
         dst_vt = static_cast<T*>(c.vt_sum) + bg * (size_t)c.S_max * D;
     }
     const int rows = max(r1 - r0, 0);
+    if (rows == 32 && dst0 % 32 == 0) {
+        // whole 32-row tile of the destination: 16-B row copies of K, and the
+        // tile's [D][32] block of transposed V written 8 rows (16 B) at a time
+        constexpr int CH = D * (int)sizeof(T) / 16;  // 16-B chunks per row
+        constexpr int EPC = 16 / (int)sizeof(T);     // elements per chunk
+        for (int e = threadIdx.x; e < 32 * CH; e += blockDim.x) {
+            const int r = e / CH, ch = e % CH;
+            const size_t so = (size_t)(r0 + r) * D + ch * EPC;
+            *reinterpret_cast<u32x4*>(dst_k + (size_t)(dst0 + r) * D + ch * EPC) =
+                *reinterpret_cast<const u32x4*>(src_k + so);
+            const u32x4 vv = *reinterpret_cast<const u32x4*>(src_v + so);
+            const T* ve = reinterpret_cast<const T*>(&vv);
+#pragma unroll
+            for (int i = 0; i < EPC; ++i) tile[r][ch * EPC + i] = ve[i];
+        }
+        __syncthreads();
+        T* blk = dst_vt + (size_t)(dst0 / 32) * 32 * D;  // [D][32]
+        for (int e = threadIdx.x; e < D * 32 / EPC; e += blockDim.x) {
+            const int d = e / (32 / EPC), r8 = (e % (32 / EPC)) * EPC;
+            u32x4 w;
+            T* we = reinterpret_cast<T*>(&w);
+#pragma unroll
+            for (int i = 0; i < EPC; ++i) we[i] = tile[r8 + i][d];
+            *reinterpret_cast<u32x4*>(blk + (size_t)d * 32 + r8) = w;
+        }
+        return;
+    }
     for (int e = threadIdx.x; e < rows * D; e += blockDim.x) {
         const int r = e / D, d = e % D;
         dst_k[(size_t)(dst0 + r) * D + d] = src_k[(size_t)(r0 + r) * D + d];

@@ -314,9 +314,9 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
                    void* stream) {
     int st = check_cache(cache);
     if (st != EVA_OK) return st;
-    if (L < 1 || !K || !V) return EVA_ERR_INVALID;
+    if (L < 1 || !K || !V || !aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
     const int n_chunks = L / cache->C;
-    if (n_chunks > 0 && (!Ksum || !Vsum)) return EVA_ERR_INVALID;
+    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
     if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
     eva::CacheView v = view_of(cache);
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -542,7 +542,7 @@ int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const
     if (L < 1 || !K || !V || !lens) return EVA_ERR_INVALID;
     if (!aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
     const int n_chunks = L / cache->C;
-    if (n_chunks > 0 && (!Ksum || !Vsum)) return EVA_ERR_INVALID;
+    if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
     if (cache->S_max < (L < cache->max_tok ? L : cache->max_tok) / cache->C) return EVA_ERR_CAPACITY;
     eva::CacheView v = rview_of(cache);
     const eva::RaggedState r = rstate_of(cache, nullptr);

@@ -179,6 +179,19 @@ def test_rcache_capacity_boundary(lib):
         _lib.EVA_ERR_INVALID
 
 
+def test_cache_fill_rejects_misaligned(lib):
+    c = make_cache()
+    odd = ctypes.c_void_p(0x10008)
+    f = lib.eva_cache_fill
+    assert f(ctypes.byref(c), odd, FAKE, FAKE, FAKE, 64, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.byref(c), FAKE, odd, FAKE, FAKE, 64, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.byref(c), FAKE, FAKE, odd, FAKE, 64, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, odd, 64, None) == _lib.EVA_ERR_INVALID
+    assert c.n_tok == 0
+    r = make_rcache()
+    assert lib.eva_rcache_fill(ctypes.byref(r), FAKE, FAKE, odd, FAKE, 64, FAKE, None) == _lib.EVA_ERR_INVALID
+
+
 def test_rcache_fill_rejects(lib):
     c = make_rcache()
     f = lib.eva_rcache_fill
