@@ -9,7 +9,7 @@
 // attention matrix is stored).
 //
 // Kernels (all bf16 storage, fp32 arithmetic, v_mfma_f32_16x16x32_bf16):
-//   bwd_dq_kernel      per query tile (4 waves x 32 columns of one head): the
+//   bwd_dq_kernel      per query tile (4 waves x 16 columns of one head): the
 //                      columns' D = dO . O (stored for the dK/dV kernels), then key
 //                      blocks of 32 rows (summaries then window band) streamed
 //                      through LDS: S^T = K Q^T, dP^T = V dO^T, dS^T, and
@@ -44,11 +44,14 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdBN = 32;     // rows per streamed block
-// LDS ring stages and blocks requested ahead of the one computed: dQ keeps
-// four stages at two waves per SIMD (its fragments need ~256 VGPRs); dK/dV
-// fits 168 VGPRs, so three stages (50 KB) let three workgroups share a CU
+// dQ: 16 query columns per wave (126 VGPRs), a three-stage ring (50 KB):
+// three workgroups per CU.  Measured on MI355X (LLM workload): 537 us, vs 568
+// with 32 columns at two waves per SIMD and 634 with 32 columns and four
+// stages.
+constexpr int kDqColBlocks = 1, kDqNS = 3, kDqWpe = 3;
+// dK/dV: LDS ring stages and blocks requested ahead of the one computed.
+// It fits 168 VGPRs, so three stages (50 KB) let three workgroups share a CU
 // (measured on MI355X: 631 vs 767 us for the window tiles of the LLM workload)
-constexpr int kDqNS = 4, kDqAhead = 3;
 constexpr int kKvNS = 3, kKvAhead = 2;
 
 // s_waitcnt vmcnt(N) lgkmcnt(0): the kernel's own DMA requests are invisible
@@ -162,18 +165,21 @@ __device__ __forceinline__ bf16x8 pair_to_b(const floatx4& t0, const floatx4& t1
 // ---------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
+template <int D, int NCB, int NS, int WPE>
+__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void bwd_dq_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[kDqNS][2][BLK];  // [stage][K, V]
+    constexpr int CW = 16 * NCB;       // query columns per wave
+    constexpr int AHEAD = NS - 1;      // blocks requested ahead of the one computed
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[NS][2][BLK];  // [stage][K, V]
     __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
     const int L = a.L, W = a.W, C = a.C;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
-    constexpr int POS = kBwdWaves * 32;  // positions per workgroup
+    constexpr int POS = kBwdWaves * CW;  // positions per workgroup
     const int n_pt = (L + POS - 1) / POS;
     const int pt = n_pt - 1 - (int)blockIdx.x % n_pt;  // late (heavy) tiles first
     const int bh = (int)blockIdx.x / n_pt;
@@ -182,9 +188,9 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
     const size_t bg = (size_t)b * a.Hkv + kvh;
     const int n0 = pt * POS;
     const int n_hi = min(n0 + POS - 1, L - 1);
-    const int p0 = n0 + wave * 32;
+    const int p0 = n0 + wave * CW;
     const bool w_active = p0 < L;
-    const int wp_last = min(p0 + 31, L - 1);
+    const int wp_last = min(p0 + CW - 1, L - 1);
 
     // block plan as in the forward: summaries [0, s(n_hi)), then the window band
     const int nsb = (visible_summaries(n_hi, W, C) + kBwdBN - 1) / kBwdBN;
@@ -199,11 +205,11 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
 
     // stationary columns: q and dO fragments (B operands), lse and D
     const size_t row0 = (size_t)bh * L;
-    bf16x8 qf[2][NDC], gf[2][NDC];
-    float lse2[2], dcol[2];
-    int col_n[2], col_s[2];
+    bf16x8 qf[NCB][NDC], gf[NCB][NDC];
+    float lse2[NCB], dcol[NCB];
+    int col_n[NCB], col_s[NCB];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < NCB; ++cb) {
         col_n[cb] = p0 + cb * 16 + c16;
         const int n = min(col_n[cb], L - 1);
         col_s[cb] = visible_summaries(n, W, C);
@@ -226,9 +232,11 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         lse2[cb] = a.lse[row0 + n] * kLog2e;
     }
 
-    floatx4 acc[NDB][2];
+    floatx4 acc[NDB][NCB];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) acc[db][0] = acc[db][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     // block j of the plan into stage j % NS; past the last block the same
     // number of DMA instructions go to the dummy area
@@ -242,33 +250,33 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         const int nv = min(kBwdBN, lim - base);
         const bf16* ksrc = real ? (sum ? Ksbg : Kbg) + (size_t)base * D : Kbg;
         const bf16* vsrc = real ? (sum ? Vsbg : Vbg) + (size_t)base * D : Vbg;
-        st.issue(ksrc, nv, lds_addr_of<D>(real ? lds[j & (kDqNS - 1)][0] : dummy), wave, real);
-        st.issue(vsrc, nv, lds_addr_of<D>(real ? lds[j & (kDqNS - 1)][1] : dummy), wave, real);
+        st.issue(ksrc, nv, lds_addr_of<D>(real ? lds[j % NS][0] : dummy), wave, real);
+        st.issue(vsrc, nv, lds_addr_of<D>(real ? lds[j % NS][1] : dummy), wave, real);
     };
 #pragma unroll
-    for (int k = 0; k < kDqAhead; ++k) stage(k);
+    for (int k = 0; k < AHEAD; ++k) stage(k);
     // the stationary fragments (plain loads) and the first blocks: the
     // compiler does not count the DMA requests, so its own wait for the
     // fragments would otherwise sit inside the loop and drain every request
     bwait_vm<0>();
     for (int j = 0; j < nb; ++j) {
-        // block j landed (the two requested after it may be in flight); the
-        // request below refills the stage of block j-1
-        bsync<(kDqAhead - 1) * REQ>();
-        stage(j + kDqAhead);
+        // block j landed (the AHEAD - 1 requested after it may be in flight);
+        // the request below refills the stage of block j-1
+        bsync<(AHEAD - 1) * REQ>();
+        stage(j + AHEAD);
         const bool sum = j < nsb;
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
         const bool needed =
             w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
         if (!needed) continue;
-        const unsigned char* ks = lds[j & (kDqNS - 1)][0];
-        const unsigned char* vs = lds[j & (kDqNS - 1)][1];
+        const unsigned char* ks = lds[j % NS][0];
+        const unsigned char* vs = lds[j % NS][1];
         // S^T and dP^T: rows = keys base + kb*16 + 4g + i, column = query c16
-        floatx4 s[2][2], dp[2][2];
+        floatx4 s[2][NCB], dp[2][NCB];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) s[kb][cb] = dp[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            for (int cb = 0; cb < NCB; ++cb) s[kb][cb] = dp[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int dc = 0; dc < NDC; ++dc)
 #pragma unroll
@@ -276,7 +284,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
                 const bf16x8 kf = row_frag<D>(ks, kb, dc, c16, g);
                 const bf16x8 vf = row_frag<D>(vs, kb, dc, c16, g);
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
+                for (int cb = 0; cb < NCB; ++cb) {
                     s[kb][cb] = mfma_bf16(kf, qf[cb][dc], s[kb][cb]);
                     dp[kb][cb] = mfma_bf16(vf, gf[cb][dc], dp[kb][cb]);
                 }
@@ -284,7 +292,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
         // P^T and dS^T (masked entries: 0)
         const float bias = sum ? a.log2C : 0.f;
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
+        for (int cb = 0; cb < NCB; ++cb) {
             const int n = col_n[cb];
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -296,15 +304,15 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
                     s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
                 }
         }
-        bf16x8 dsf[2];
+        bf16x8 dsf[NCB];
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) dsf[cb] = pair_to_b(s[0][cb], s[1][cb]);
+        for (int cb = 0; cb < NCB; ++cb) dsf[cb] = pair_to_b(s[0][cb], s[1][cb]);
         // dQ^T += K^T dS^T
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
             const bf16x8 kt = tr_frag<D>(ks, db, c16, g);
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) acc[db][cb] = mfma_bf16(kt, dsf[cb], acc[db][cb]);
+            for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(kt, dsf[cb], acc[db][cb]);
         }
     }
 
@@ -314,7 +322,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) void bwd_dq_kernel(BwdParams a) {
     const float inv_sqrt_d = a.scale_log2 / kLog2e;
     bf16* dQ = static_cast<bf16*>(a.dQ);
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < NCB; ++cb) {
         const int n = col_n[cb];
         if (n >= L) continue;
         bf16* orow = dQ + (row0 + n) * D;
@@ -791,8 +799,10 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
 template <int D>
 hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
     // dQ, and the row dots D = dO . O the dK/dV kernels read
-    const int n_pt = (p.L + kBwdWaves * 32 - 1) / (kBwdWaves * 32);
-    hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64), 0, stream, p);
+    constexpr int POS = kBwdWaves * 16 * kDqColBlocks;
+    const int n_pt = (p.L + POS - 1) / POS;
+    hipLaunchKernelGGL((bwd_dq_kernel<D, kDqColBlocks, kDqNS, kDqWpe>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64),
+                       0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     constexpr int KT = kBwdWaves * 16;
