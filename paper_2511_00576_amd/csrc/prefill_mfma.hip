@@ -15,7 +15,8 @@
 // CU), and 4 waves on 32-key blocks (77 KB, two workgroups per CU, whose
 // barriers and prologues then overlap), used when each kv head serves one
 // query head, where its half-size position tiles also waste fewer blocks at
-// the window's edges.  Either way two waves share each SIMD.
+// the window's edges, and for windows of up to 512 keys (prefill_mfma_narrow).
+// Either way two waves share each SIMD.
 //
 // Per wave and block j one straight-line region runs S^T(j+1) = K Q^T and
 // then O^T += V^T P^T(j) in two 32-key halves on the matrix cores, with the
