@@ -29,6 +29,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -93,11 +94,22 @@ def decode_counts(B, H, Hkv, d, W, C, p, e):
     return B * H * 4 * d * (w + s), B * Hkv * (w + s) * d * 2 * e + 2 * B * H * d * e
 
 
+def _code_only(path, text):
+    """Source text without comments and blank lines: the counters describe
+    the code, which an edited comment does not change."""
+    if path.endswith(".py"):
+        lines = [l for l in text.splitlines() if not l.strip().startswith("#")]
+    else:
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        lines = [re.sub(r"//.*", "", l) for l in text.splitlines()]
+    return "\n".join(l.rstrip() for l in lines if l.strip())
+
+
 def source_sha(paths):
     h = hashlib.sha256()
     for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            h.update(_code_only(p, f.read()).encode())
     return h.hexdigest()[:16]
 
 
