@@ -456,7 +456,8 @@ void prefill_mfma_kernel(PrefillParams a) {
     }
 
     // ---- iteration j: S^T(j+1) and O^T += V^T P^T(j) ----
-    auto iteration = [&](int j, floatx4 (&sc)[NKB][NCB], floatx4 (&sn)[NKB][NCB]) {
+    auto iteration = [&](auto ph_tag, int j, floatx4 (&sc)[NKB][NCB], floatx4 (&sn)[NKB][NCB]) {
+        constexpr int PH = decltype(ph_tag)::value;  // j mod NS: the stages as constants
         // block j+1 landed (the AHEAD-2 blocks after it may stay in flight);
         // the block requested in this iteration refills the stage of block
         // j-1, whose last reads were before this barrier
@@ -472,8 +473,8 @@ void prefill_mfma_kernel(PrefillParams a) {
         const bool do_pv = kc.needed;
         const bool do_qk = has_next && kn.needed;
         const float bias_c = kc.is_sum ? a.log2C : 0.f;
-        const unsigned char* ks = lds[(j + 1) & (NS - 1)][0];
-        const unsigned char* vs = lds[j & (NS - 1)][1];
+        const unsigned char* ks = lds[(PH + 1) & (NS - 1)][0];
+        const unsigned char* vs = lds[PH][1];
         if (!do_pv && !do_qk) {
             // nothing of blocks j, j+1 for this wave: only its share of the request
 #pragma unroll
@@ -592,12 +593,22 @@ void prefill_mfma_kernel(PrefillParams a) {
         }
         kc = kn;
     };
+    // four steps per trip, so that each one's stage indices are constants
+    static_assert(NS == 4, "one trip covers the ring");
+    typedef std::integral_constant<int, 0> P0;
+    typedef std::integral_constant<int, 1> P1;
+    typedef std::integral_constant<int, 2> P2;
+    typedef std::integral_constant<int, 3> P3;
     int j = 0;
-    for (; j + 1 < nb; j += 2) {
-        iteration(j, s0, s1);
-        iteration(j + 1, s1, s0);
+    for (; j + 3 < nb; j += 4) {
+        iteration(P0{}, j, s0, s1);
+        iteration(P1{}, j + 1, s1, s0);
+        iteration(P2{}, j + 2, s0, s1);
+        iteration(P3{}, j + 3, s1, s0);
     }
-    if (j < nb) iteration(j, s0, s1);
+    if (j < nb) iteration(P0{}, j, s0, s1);
+    if (j + 1 < nb) iteration(P1{}, j + 1, s1, s0);
+    if (j + 2 < nb) iteration(P2{}, j + 2, s0, s1);
     if (pending) rescale();
 
     // No request may still be writing LDS when the workgroup ends: wait for
