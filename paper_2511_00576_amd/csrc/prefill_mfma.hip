@@ -285,11 +285,14 @@ void prefill_mfma_kernel(PrefillParams a) {
     // running maxima (log2 units, identical on the four lanes of a column) and
     // denominators: row sums of the bf16-rounded weights on the matrix cores
     // (all-ones A operand, every output row holds the column sum)
-    float m_run[NCB];
+    // m_neg: -m_run, or 0 while m_run is -inf (a column that has seen no key
+    // yet), kept beside it so that each step's exponent offset is one add
+    float m_run[NCB], m_neg[NCB];
     floatx4 l_acc[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
         m_run[cb] = -INFINITY;
+        m_neg[cb] = 0.f;
         l_acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
@@ -394,6 +397,7 @@ void prefill_mfma_kernel(PrefillParams a) {
             const bool up = bm > m_run[cb] + kTau;
             alpha[cb] = up ? fast_exp2(m_run[cb] - bm) : 1.f;
             m_run[cb] = up ? bm : m_run[cb];
+            m_neg[cb] = m_run[cb] == -INFINITY ? 0.f : -m_run[cb];
         }
         return true;
     };
@@ -501,9 +505,9 @@ void prefill_mfma_kernel(PrefillParams a) {
         constexpr int EH = NCB * 8;    // exponentials per 32-key half and lane
         constexpr int MV = NCB * NKB * 4;  // scores per block and lane
         float off[NCB];
+        const float bias_sel = do_pv ? bias_c : -INFINITY;  // wave-uniform
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-            off[cb] = do_pv ? bias_c - (m_run[cb] == -INFINITY ? 0.f : m_run[cb]) : -INFINITY;
+        for (int cb = 0; cb < NCB; ++cb) off[cb] = bias_sel + m_neg[cb];
         // P^T half hf: contraction row 8g + e is key (2hf)*16 + 4g + e for
         // e < 4, (2hf+1)*16 + 4g + e - 4 above (the V^T read uses the same order)
         auto ex = [&](int hf, int ef) {
