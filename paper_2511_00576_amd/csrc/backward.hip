@@ -677,11 +677,12 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
     const int first = chunk * C;
     const bf16* K = static_cast<const bf16*>(a.K) + (bg * (size_t)L + first + r0) * D + cc * 8;
     const bf16* V = static_cast<const bf16*>(a.V) + (bg * (size_t)L + first + r0) * D + cc * 8;
+    // read once: non-temporal loads (measured 183 -> 168 us on the LLM workload)
     u32x4 kw[ROWS], vw[ROWS];
 #pragma unroll
     for (int i = 0; i < ROWS; ++i) {
-        kw[i] = *reinterpret_cast<const u32x4*>(K + (size_t)i * RPS * D);
-        vw[i] = *reinterpret_cast<const u32x4*>(V + (size_t)i * RPS * D);
+        kw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(K + (size_t)i * RPS * D));
+        vw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(V + (size_t)i * RPS * D));
     }
     auto unpack = [&](const u32x4& w, float out[8]) {
 #pragma unroll
