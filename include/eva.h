@@ -43,6 +43,11 @@
  * Errors: functions return EVA_OK (0) or a negative eva_status; invalid
  * arguments are rejected before anything is enqueued.  No C++ exception
  * crosses this boundary.
+ *
+ * Limits: sequence lengths L, a ragged cache's max_tok and a cache's token
+ * count stay at or below 2^30 (UNSUPPORTED for a longer L or max_tok;
+ * CAPACITY once a cache holds 2^30 tokens), and kernel grids below 2^31
+ * workgroups (UNSUPPORTED).
  */
 #ifndef EVA_H
 #define EVA_H
@@ -56,7 +61,7 @@ extern "C" {
 typedef enum {
     EVA_OK = 0,
     EVA_ERR_INVALID = -1,     /* bad shape, window, chunk size or null pointer */
-    EVA_ERR_UNSUPPORTED = -2, /* head dim or element type this build does not handle */
+    EVA_ERR_UNSUPPORTED = -2, /* head dim, element type or size this build does not handle */
     EVA_ERR_CAPACITY = -3,    /* cache ring or summary array too small */
     EVA_ERR_HIP = -4          /* the HIP runtime refused a launch */
 } eva_status;

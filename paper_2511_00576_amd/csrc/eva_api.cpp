@@ -59,6 +59,9 @@ hipError_t dispatch(int d, int dtype, F&& f) {
 
 // Largest C whose logits fit the summary kernel's LDS scratch.
 constexpr int kMaxChunk = 8192;
+// Longest sequence (L) the entry points take: kernel index arithmetic stays
+// in 32 bits with room to spare.
+constexpr int kMaxLen = 1 << 30;
 
 int check_cache(const eva_cache* c) {
     if (!c) return EVA_ERR_INVALID;
@@ -70,6 +73,7 @@ int check_cache(const eva_cache* c) {
     if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
         return EVA_ERR_INVALID;
     if (c->n_tok < 0) return EVA_ERR_INVALID;
+    if (c->n_tok >= kMaxLen) return EVA_ERR_CAPACITY;  // positions stay below 2^30
     if (!valid_window(c->window) || c->window == EVA_WINDOW_NONCAUSAL) return EVA_ERR_INVALID;
     if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
     if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
@@ -121,6 +125,7 @@ int check_rcache(const eva_rcache* c) {
     int st = supported(c->d, c->dtype);
     if (st != EVA_OK) return st;
     if (!c->k_ring || !c->vt_ring || !c->k_sum || !c->vt_sum || !c->n_tok || !c->arrive) return EVA_ERR_INVALID;
+    if (c->max_tok > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!aligned16(c->k_ring) || !aligned16(c->vt_ring) || !aligned16(c->k_sum) || !aligned16(c->vt_sum))
         return EVA_ERR_INVALID;
     if (c->max_tok < 1) return EVA_ERR_INVALID;
@@ -199,6 +204,7 @@ const char* eva_status_string(int status) {
 int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum, int B, int H_kv, int L, int d, int C,
                         int dtype, void* stream) {
     if (B < 1 || H_kv < 1 || L < 1 || C < 1) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
     if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
@@ -216,6 +222,7 @@ int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum, in
 int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float lambda, void* Ksum, void* Vsum,
                            int B, int H_kv, int L, int d, int C, int dtype, void* stream) {
     if (B < 1 || H_kv < 1 || L < 1 || C < 1) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!(lambda >= 0.f) || lambda > 1e30f) return EVA_ERR_INVALID;  // rejects NaN and infinities
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
@@ -253,8 +260,9 @@ static PrefillTiles prefill_tiles(int B, int H, int H_kv, int L, int W, int dtyp
     PrefillTiles t;
     t.Gt = gcd(G, waves);
     t.pos_per_wg = cols * waves / t.Gt;
-    t.n_pos_tiles = (L + t.pos_per_wg - 1) / t.pos_per_wg;
-    t.n_tiles = (long long)B * H_kv * (G / t.Gt) * t.n_pos_tiles;
+    const long long pos_tiles = ((long long)L + t.pos_per_wg - 1) / t.pos_per_wg;  // L near 2^31 must not wrap
+    t.n_pos_tiles = (int)pos_tiles;
+    t.n_tiles = (long long)B * H_kv * (G / t.Gt) * pos_tiles;
     return t;
 }
 
@@ -279,6 +287,7 @@ static int prefill_attention_impl(const void* Q, const void* K, const void* V, c
                                   void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                                   int window, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!valid_window(window)) return EVA_ERR_INVALID;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
@@ -329,6 +338,7 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
     int st = check_cache(cache);
     if (st != EVA_OK) return st;
     if (L < 1 || !K || !V || !aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     const int n_chunks = L / cache->C;
     if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
     if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
@@ -351,6 +361,7 @@ int eva_prefill(const void* Q, const void* K, const void* V, void* O, int B, int
 int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, int H, int H_kv, int L, int d, int W,
                    int C, int dtype, int window, void* Ksum, void* Vsum, eva_cache* cache, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!valid_window(window)) return EVA_ERR_INVALID;
     if (cache && window == EVA_WINDOW_NONCAUSAL) return EVA_ERR_INVALID;  // no causal decode to feed
     int st = supported(d, dtype);
@@ -504,11 +515,13 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
                          size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                          void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
     if (dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (C > kMaxChunk) return EVA_ERR_UNSUPPORTED;
-    if ((long long)B * H * ((L + 127) / 128) > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
+    // grid sizes of the backward kernels (64-row query and key tiles)
+    if ((long long)B * H * ((L + 63) / 64) > 0x7fffffffLL) return EVA_ERR_UNSUPPORTED;
     const void* must[] = {Q, K, V, O, dO, lse, dQ, dK, dV, ws};
     for (const void* ptr : must)
         if (!ptr || !aligned16(ptr)) return EVA_ERR_INVALID;
@@ -560,6 +573,7 @@ int eva_rcache_fill(const eva_rcache* cache, const void* K, const void* V, const
     int st = check_rcache(cache);
     if (st != EVA_OK) return st;
     if (L < 1 || !K || !V || !lens) return EVA_ERR_INVALID;
+    if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!aligned16(K) || !aligned16(V)) return EVA_ERR_INVALID;
     const int n_chunks = L / cache->C;
     if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;

@@ -136,6 +136,29 @@ def test_prefill_cache_mismatch(lib):
     assert prefill_call(lib, L=4 * 33, cache=ctypes.byref(c)) == _lib.EVA_ERR_CAPACITY
 
 
+def test_prefill_validates_before_filling(lib):
+    # the attention stage's limit on its tile count (B * H_kv * position
+    # tiles < 2^31) is checked before the summaries and the cache fill are
+    # launched: the call fails and the cache is left as it was
+    B, L, C, W = 65535, 2 ** 30, 256, 8
+    c = make_cache(B=B, H=1, H_kv=1, W=W, C=C, R=288, S_max=(L // C + 31) // 32 * 32)
+    assert prefill_call(lib, B=B, H=1, H_kv=1, L=L, W=W, C=C, cache=ctypes.byref(c)) == _lib.EVA_ERR_UNSUPPORTED
+    assert c.n_tok == 0
+
+
+def test_length_limits(lib):
+    # sequence lengths above 2^30 are refused before any launch; so is a
+    # cache that already holds 2^30 tokens
+    f = lib.eva_build_summaries
+    assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 2 ** 30 + 1, 64, 4, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert prefill_call(lib, L=2 ** 30 + 1) == _lib.EVA_ERR_UNSUPPORTED
+    c = make_cache(n_tok=2 ** 30)
+    assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_CAPACITY
+    assert c.n_tok == 2 ** 30
+    r = make_rcache(max_tok=2 ** 30 + 1)
+    assert lib.eva_rcache_append(ctypes.byref(r), FAKE, FAKE, None, None) == _lib.EVA_ERR_UNSUPPORTED
+
+
 def test_summaries_rejects(lib):
     f = lib.eva_build_summaries
     assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 64, 64, 0, 0, None) == _lib.EVA_ERR_INVALID
