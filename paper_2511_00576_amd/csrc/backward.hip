@@ -34,6 +34,8 @@
 // products), the stationary rows are B-operand fragments in registers, and
 // the 16x16 score tiles of two key (or query) halves form the next product's
 // B operand in place.
+#include <type_traits>
+
 #include "eva_device.hpp"
 #include "eva_kernels.hpp"
 #include "summary.hpp"
@@ -172,6 +174,7 @@ void bwd_dq_kernel(BwdParams a) {
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
     constexpr int CW = 16 * NCB;       // query columns per wave
     constexpr int AHEAD = NS - 1;      // blocks requested ahead of the one computed
+    static_assert(NS == 3, "the block loop below takes three steps per trip");
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NS][2][BLK];  // [stage][K, V]
     __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
@@ -259,7 +262,8 @@ void bwd_dq_kernel(BwdParams a) {
     // compiler does not count the DMA requests, so its own wait for the
     // fragments would otherwise sit inside the loop and drain every request
     bwait_vm<0>();
-    for (int j = 0; j < nb; ++j) {
+    auto block_step = [&](auto ph_tag, int j) {
+        constexpr int PH = decltype(ph_tag)::value;  // j mod NS: the stage as a constant
         // block j landed (the AHEAD - 1 requested after it may be in flight);
         // the request below refills the stage of block j-1
         bsync<(AHEAD - 1) * REQ>();
@@ -268,9 +272,9 @@ void bwd_dq_kernel(BwdParams a) {
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
         const bool needed =
             w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
-        if (!needed) continue;
-        const unsigned char* ks = lds[j % NS][0];
-        const unsigned char* vs = lds[j % NS][1];
+        if (!needed) return;
+        const unsigned char* ks = lds[PH][0];
+        const unsigned char* vs = lds[PH][1];
         // S^T and dP^T: rows = keys base + kb*16 + 4g + i, column = query c16
         floatx4 s[2][NCB], dp[2][NCB];
 #pragma unroll
@@ -314,7 +318,19 @@ void bwd_dq_kernel(BwdParams a) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) acc[db][cb] = mfma_bf16(kt, dsf[cb], acc[db][cb]);
         }
+    };
+    // three steps per trip, so that each one's stage index is a constant
+    typedef std::integral_constant<int, 0> P0;
+    typedef std::integral_constant<int, 1> P1;
+    typedef std::integral_constant<int, 2> P2;
+    int j = 0;
+    for (; j + 2 < nb; j += 3) {
+        block_step(P0{}, j);
+        block_step(P1{}, j + 1);
+        block_step(P2{}, j + 2);
     }
+    if (j < nb) block_step(P0{}, j);
+    if (j + 1 < nb) block_step(P1{}, j + 1);
 
     bwait_vm<0>();  // no request may still be writing LDS when the workgroup ends
 
@@ -406,6 +422,7 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
     // (one 4-B DMA instruction each, by waves 0 and 1; waves 2 and 3 issue one
     // into the dummy area so that every wave counts the same instructions)
     constexpr int REQ = 2 * Cfg::NI + 1;
+    static_assert(kKvNS == 3, "the step loop below takes three steps per trip");
     auto stage = [&](int j) {
         const bool real = j < steps;
         // past the last step: row 0 of the group's first head (always valid)
@@ -429,15 +446,16 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
     for (int k = 0; k < kKvAhead; ++k) stage(k);
     // see bwd_dq_kernel: the stationary fragments are waited for here
     bwait_vm<0>();
-    for (int j = 0; j < steps; ++j) {
+    auto block_step = [&](auto ph_tag, int j) {
+        constexpr int PH = decltype(ph_tag)::value;  // j mod NS: the stage as a constant
         // step j's rows landed (the request after it may be in flight); the
         // request below refills the stage of step j-1
         bsync<(kKvAhead - 1) * REQ>();
         stage(j + kKvAhead);
         const int qb = qb0 + (j0 + j) % nqb;
         const int r0 = qb * kBwdBN;
-        if (!w_active || r0 > wr_hi || r0 + kBwdBN - 1 < wr_lo) continue;
-        const int st_i = j % kKvNS;
+        if (!w_active || r0 > wr_hi || r0 + kBwdBN - 1 < wr_lo) return;
+        constexpr int st_i = PH;
         // lse and D of this lane's 8 query rows r0 + 16 kb + 4g + i
         float lse2[2][4], dq[2][4];
 #pragma unroll
@@ -480,7 +498,19 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
             dv[db] = mfma_bf16(tr_frag<D>(gs, db, c16, g), pf, dv[db]);
             dk[db] = mfma_bf16(tr_frag<D>(qs, db, c16, g), dsf, dk[db]);
         }
+    };
+    // three steps per trip, so that each one's stage index is a constant
+    typedef std::integral_constant<int, 0> P0;
+    typedef std::integral_constant<int, 1> P1;
+    typedef std::integral_constant<int, 2> P2;
+    int j = 0;
+    for (; j + 2 < steps; j += 3) {
+        block_step(P0{}, j);
+        block_step(P1{}, j + 1);
+        block_step(P2{}, j + 2);
     }
+    if (j < steps) block_step(P0{}, j);
+    if (j + 1 < steps) block_step(P1{}, j + 1);
 
     bwait_vm<0>();  // no request may still be writing LDS when the workgroup ends
     if (key >= lim) return;
