@@ -293,20 +293,36 @@ void bwd_dq_kernel(BwdParams a) {
                     dp[kb][cb] = mfma_bf16(vf, gf[cb][dc], dp[kb][cb]);
                 }
             }
-        // P^T and dS^T (masked entries: 0)
+        // P^T and dS^T (masked entries: 0); a block every pair of which is
+        // visible to this wave's columns skips the per-element test
         const float bias = sum ? a.log2C : 0.f;
+        const bool full = wp_last == p0 + CW - 1 &&
+                          (sum ? base + kBwdBN <= visible_summaries(p0, W, C)
+                               : base + kBwdBN - 1 <= p0 && wp_last - base < W);
+        if (full) {
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            const int n = col_n[cb];
+            for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = base + kb * 16 + g * 4 + i;
-                    const bool ok = n < L && (sum ? key < col_s[cb] : (unsigned)(n - key) < (unsigned)W);
-                    const float p = ok ? fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, bias - lse2[cb])) : 0.f;
-                    s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
-                }
+                    for (int i = 0; i < 4; ++i) {
+                        const float p = fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, bias - lse2[cb]));
+                        s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
+                    }
+        } else {
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int n = col_n[cb];
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = base + kb * 16 + g * 4 + i;
+                        const bool ok = n < L && (sum ? key < col_s[cb] : (unsigned)(n - key) < (unsigned)W);
+                        const float p = ok ? fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, bias - lse2[cb])) : 0.f;
+                        s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
+                    }
+            }
         }
         bf16x8 dsf[NCB];
 #pragma unroll
@@ -481,16 +497,31 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
                 dp[kb] = mfma_bf16(row_frag<D>(gs, kb, dc, c16, g), vf[dc], dp[kb]);
             }
         floatx4 p[2];
+        // a step every pair of which is visible (the wave's 16 keys, the
+        // block's 32 rows: most window steps) skips the per-element test
+        const bool full = wk0 + 15 < lim && r0 + kBwdBN - 1 < L &&
+                          (sum ? wk0 + 16 <= visible_summaries(r0, W, C)
+                               : wk0 + 15 <= r0 && r0 + kBwdBN - 1 - wk0 < W);
+        if (full) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int n = r0 + kb * 16 + g * 4 + i;
-                const bool ok = key < lim && n < L &&
-                                (sum ? key < visible_summaries(n, W, C) : (unsigned)(n - key) < (unsigned)W);
-                p[kb][i] = ok ? fast_exp2(fmaf(s[kb][i], a.scale_log2, bias - lse2[kb][i])) : 0.f;
-                s[kb][i] = p[kb][i] * (dp[kb][i] - dq[kb][i]);  // dS
-            }
+                for (int i = 0; i < 4; ++i) {
+                    p[kb][i] = fast_exp2(fmaf(s[kb][i], a.scale_log2, bias - lse2[kb][i]));
+                    s[kb][i] = p[kb][i] * (dp[kb][i] - dq[kb][i]);  // dS
+                }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int n = r0 + kb * 16 + g * 4 + i;
+                    const bool ok = key < lim && n < L &&
+                                    (sum ? key < visible_summaries(n, W, C) : (unsigned)(n - key) < (unsigned)W);
+                    p[kb][i] = ok ? fast_exp2(fmaf(s[kb][i], a.scale_log2, bias - lse2[kb][i])) : 0.f;
+                    s[kb][i] = p[kb][i] * (dp[kb][i] - dq[kb][i]);  // dS
+                }
+        }
         const bf16x8 pf = pair_to_b(p[0], p[1]);
         const bf16x8 dsf = pair_to_b(s[0], s[1]);
 #pragma unroll
