@@ -358,21 +358,39 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
             key_hi = min(31, geo.p - pos0);
         }
         const bool full = key_lo == 0 && key_hi == 31;
+        const unsigned span = (unsigned)(key_hi - key_lo);
 
         // all 16-B fragment loads of the chunk before any wait: 2*NDC key + NDB
         // value.  Non-temporal: a step reads each cache row once, and keeping
         // the stream out of the caches measured 8% faster (29.7 -> 27.3 us on
-        // 64 sequences x 8 kv heads, 576 rows each)
-        bf16x8 ka[2][NDC], va[NDB];
-        auto ld16 = [](const bf16* p) {
-            return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+        // 64 sequences x 8 kv heads, 576 rows each).  Buffer loads over the
+        // chunk's tiles: a lane whose key row, or whose 8 value slots, lie
+        // outside [key_lo, key_hi] gets an offset past the tile and reads
+        // zeros without a memory access, so the rows a window edge or the last
+        // summary tile does not use are not fetched (no branch, no wait).
+        constexpr int kTileBytes = 32 * D * (int)sizeof(T);
+        constexpr int kSkip = 0x40000000;  // beyond any tile: zeros, no access
+        const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kt), 0, kTileBytes,
+                                                                             0x00020000);
+        const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(vt), 0, kTileBytes,
+                                                                             0x00020000);
+        auto ldb = [](__amdgpu_buffer_rsrc_t r, int byte_off) {
+            return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 2));  // nt
         };
+        bf16x8 ka[2][NDC], va[NDB];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) {
+            const bool use = (unsigned)(krow0 + 4 * kb - key_lo) <= span;
+            const int base = use ? (koff + kb * 4 * D) * (int)sizeof(T) : kSkip;
 #pragma unroll
-            for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = ld16(kt + koff + kb * 4 * D + dc * 32);
+            for (int dc = 0; dc < NDC; ++dc) ka[kb][dc] = ldb(krs, base + dc * 32 * (int)sizeof(T));
+        }
+        {
+            const bool use = g * 8 <= key_hi && g * 8 + 7 >= key_lo;
+            const int base = use ? voff * (int)sizeof(T) : kSkip;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) va[db] = ld16(vt + voff + db * 16 * 32);
+            for (int db = 0; db < NDB; ++db) va[db] = ldb(vrs, base + db * 16 * 32 * (int)sizeof(T));
+        }
         __builtin_amdgcn_sched_barrier(0);
         if (APPEND && geo.fresh && !is_sum && chunk_pos0 + 32 > geo.p) {
             // the chunk holding row p: its ring slot is stale, take the input
@@ -410,7 +428,6 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
         }
         if (!full) {
             // valid chunk keys are [key_lo, key_hi]: unsigned range test, no branches
-            const unsigned span = (unsigned)(key_hi - key_lo);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
