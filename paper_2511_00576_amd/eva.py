@@ -125,18 +125,31 @@ class Cache:
 
 
 def prefill(Q, K, V, W: int, C: int, cache: Cache = None, return_summaries: bool = False,
-            window: int = _lib.EVA_WINDOW_SLIDING):
+            window: int = _lib.EVA_WINDOW_SLIDING, out=None, summaries=None):
     """EVA prefill. Q [B, H, L, d]; K, V [B, Hkv, L, d] -> O [B, H, L, d].
-    `window`: one of the EVA_WINDOW_* variants."""
+    `window`: one of the EVA_WINDOW_* variants.  `out` (O) and `summaries`
+    ((Ks, Vs), [B, Hkv, L // C, d]) may be preallocated."""
     _require_device(Q, K, V)
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
     if K.shape != (B, Hkv, L, d) or V.shape != K.shape or Q.dtype != K.dtype or V.dtype != K.dtype:
         raise ValueError("Q [B,H,L,d], K and V [B,Hkv,L,d] of one dtype expected")
-    O = torch.empty_like(Q)
     n_chunks = L // C
-    Ks = torch.empty(B, Hkv, n_chunks, d, dtype=Q.dtype, device=Q.device)
-    Vs = torch.empty_like(Ks)
+    if out is None:
+        O = torch.empty_like(Q)
+    else:
+        O = out
+        _require_device(O)
+        if O.shape != Q.shape or O.dtype != Q.dtype:
+            raise ValueError("out must be [B, H, L, d] in the dtype of Q")
+    if summaries is None:
+        Ks = torch.empty(B, Hkv, n_chunks, d, dtype=Q.dtype, device=Q.device)
+        Vs = torch.empty_like(Ks)
+    else:
+        Ks, Vs = summaries
+        _require_device(Ks, Vs)
+        if tuple(Ks.shape) != (B, Hkv, n_chunks, d) or Vs.shape != Ks.shape or Ks.dtype != Q.dtype:
+            raise ValueError("summaries must be [B, Hkv, L // C, d] in the dtype of Q")
     lib = _lib.load()
     cref = ctypes.byref(cache.struct) if cache is not None else None
     _lib.check("eva_prefill_ex",

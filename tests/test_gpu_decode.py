@@ -189,3 +189,31 @@ def test_decode_workload_full_size_sampled():
             heads = list(range(g * (w.H // w.Hkv), (g + 1) * (w.H // w.Hkv)))
             ref = oracle.attend_rows(to64(q_new[b, heads]), np.full(len(heads), p), K64, V64, Ks, Vs, w.W, w.C)
             assert_parity(got[b, heads], ref, w.dtype, f"b{b} g{g}")
+
+
+def test_prefill_with_cache_matches_parts_on_a_stream():
+    # eva_prefill with a cache, called on a non-default stream and followed
+    # at once (no host sync) by a decode that reads the cache, gives the
+    # bytes of the separate calls
+    B, H, Hkv, L, d, W, C = 2, 4, 2, 700, 128, 100, 64
+    print(f"prefill+cache on a stream B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C}", flush=True)
+    q, k, v = (t.cuda() for t in inputs.qkv(B, H, Hkv, L, d, torch.bfloat16, seed=43))
+    qn = inputs.normal((B, H, d), 44, torch.bfloat16).cuda()
+    a = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L + 1, fill=0.0)
+    b = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L + 1, fill=0.0)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        O, Ks, Vs = eva.prefill(q, k, v, W, C, cache=a, return_summaries=True)
+        snap = {name: getattr(a, name).clone() for name in ("k_ring", "vt_ring", "k_sum", "vt_sum")}
+        oa = eva.decode_step(a, qn)
+    torch.cuda.current_stream().wait_stream(s)
+    Ks2, Vs2 = eva.build_summaries(k, v, C)
+    eva.cache_fill(b, k, v, Ks2, Vs2)
+    O2 = eva.prefill_attention(q, k, v, Ks2, Vs2, W, C)
+    ob = eva.decode_step(b, qn)
+    torch.cuda.synchronize()
+    assert torch.equal(O, O2) and torch.equal(Ks, Ks2) and torch.equal(Vs, Vs2)
+    for name, t in snap.items():
+        assert torch.equal(t, getattr(b, name)), name
+    assert torch.equal(oa, ob)
