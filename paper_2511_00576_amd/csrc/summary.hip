@@ -165,7 +165,7 @@ hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* V
     const T* v = static_cast<const T*>(V);
     T* ks = static_cast<T*>(Ks);
     T* vs = static_cast<T*>(Vs);
-    if (C % RPS == 0 && C / RPS <= 8) {
+    if (C % RPS == 0 && C / RPS <= 16) {
         const dim3 grid(n_chunks, BH);
         switch (C / RPS) {
             case 1:
@@ -184,6 +184,13 @@ hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* V
                 hipLaunchKernelGGL((summary_kernel_reg<D, T, 8, RF>), grid, dim3(kSummaryThreads), 0, stream, k, v, ks,
                                    vs, L, n_chunks, eps, rf_scale);
                 return hipGetLastError();
+            case 16:
+                if constexpr (sizeof(T) == 2) {  // bf16 only: 16 rows of fp32 would not fit the registers
+                    hipLaunchKernelGGL((summary_kernel_reg<D, T, 16, RF>), grid, dim3(kSummaryThreads), 0, stream, k,
+                                       v, ks, vs, L, n_chunks, eps, rf_scale);
+                    return hipGetLastError();
+                }
+                break;
             default:
                 break;
         }

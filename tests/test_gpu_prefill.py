@@ -100,7 +100,8 @@ def test_prefill_deterministic():
 
 
 # chunk sizes that take the register-resident kernel (C = 256/(d/8) rows per
-# step times 1, 2, 4, 8) and ones that take the three-pass kernel
+# step times 1, 2, 4, 8, and 16 for bf16: C 256 at d 128) and ones that take
+# the three-pass kernel
 @pytest.mark.parametrize("L,C", [(1000, 7), (64, 64), (63, 64), (4096, 256), (300, 16), (300, 32),
                                  (600, 128), (1100, 512), (640, 160)])
 @pytest.mark.parametrize("d", [64, 128])
