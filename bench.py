@@ -164,6 +164,8 @@ def main():
                     help="launch the decode iterations one by one instead of replaying a captured graph "
                          "(for per-dispatch counter runs)")
     ap.add_argument("--no-generate", action="store_true")
+    ap.add_argument("--no-other-prefill", action="store_true",
+                    help="skip the GQA and long-context prefill workloads")
     ap.add_argument("--gen-layers", type=int, default=N_LAYERS,
                     help="layer caches a generation step visits (working set beyond the Infinity Cache)")
     ap.add_argument("--gen-steps", type=int, default=None,
@@ -352,6 +354,8 @@ def main():
     }
     del q, k, v, O, Ks, Vs, cache
 
+    if not args.no_other_prefill:
+        out["prefill_workloads"] = bench_other_prefill(args, torch, eva, inputs, dev)
     if not args.no_decode:
         out["decode"] = bench_decode(args, torch, eva, inputs, dev)
     if not args.no_generate:
@@ -361,6 +365,80 @@ def main():
         print("# oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
+
+
+def bench_other_prefill(args, torch, eva, inputs, dev):
+    """The GQA workload and the long-context workload at C = 64, 128, 256
+    (fixed W = 1024): fused attention time, algorithmic TFLOP/s against the
+    bf16 MFMA peak, and the summaries' time.  For the C sweep also the
+    approximation side of the trade-off: on sampled rows, the relative
+    distance of the EVA output from exact causal softmax attention over the
+    whole prefix (computed here in fp32 with plain torch ops)."""
+    import dataclasses
+    import math
+    res = {}
+    lw = inputs.LONG_BF16
+    cases = [(inputs.GQA_BF16, False)]
+    cases += [(dataclasses.replace(lw, C=c, name=lw.name.replace("C256", f"C{c}")), True) for c in (64, 128, 256)]
+    cached = {}
+    for wk, sample in cases:
+        print(f"# prefill workload {wk.name}", file=sys.stderr, flush=True)
+        key = (wk.B, wk.H, wk.Hkv, wk.L, wk.d, wk.seed)
+        if key not in cached:
+            cached.clear()
+            cached[key] = tuple(t.to(dev) for t in inputs.workload_qkv(wk))
+        q, k, v = cached[key]
+        Ks, Vs = eva.build_summaries(k, v, wk.C)
+        O = torch.empty_like(q)
+        n = max(args.steps, 1)
+
+        def timed(fn):
+            # the clocks drop while the inputs are drawn on the host: warm up
+            # for ~0.2 s of this launch before timing
+            fn()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            for _ in range(min(2000, int(0.2 / max(time.perf_counter() - t0, 1e-5)))):
+                fn()
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record()
+            for _ in range(n):
+                fn()
+            a1.record()
+            torch.cuda.synchronize()
+            return a0.elapsed_time(a1) / n
+
+        ms_summ = timed(lambda: eva.build_summaries(k, v, wk.C, out=(Ks, Vs)))
+        ms_attn = timed(lambda: eva.prefill_attention(q, k, v, Ks, Vs, wk.W, wk.C, out=O))
+        flops = wk.B * wk.H * 4 * wk.d * attended(wk.L, wk.W, wk.C)
+        tf = flops / (ms_attn * 1e-3) / 1e12
+        r = {"attention_ms": ms_attn, "alg_flops": flops, "tflops": tf, "mfma_frac": tf / PEAK_BF16_TFLOPS,
+             "summaries_ms": ms_summ}
+        if sample:
+            G = wk.H // wk.Hkv
+            errs = []
+            for h in (0, 13, wk.H - 1):
+                for row in (wk.W + wk.C, wk.L // 3, wk.L // 2, wk.L - 1):
+                    qr = q[0, h, row].float()
+                    kk = k[0, h // G, : row + 1].float()
+                    vv = v[0, h // G, : row + 1].float()
+                    pr = torch.softmax(kk @ qr / math.sqrt(wk.d), dim=0)
+                    exact = pr @ vv
+                    errs.append(float((O[0, h, row].float() - exact).norm() / exact.norm()))
+            r["rel_dev_from_exact_mean"] = sum(errs) / len(errs)
+            r["rel_dev_from_exact_max"] = max(errs)
+            r["rel_dev_rows"] = "heads 0, 13, 31 x rows W+C, L/3, L/2, L-1"
+        print(f"# {wk.name}: attention {ms_attn * 1e3:.1f} us ({tf:.0f} TFLOP/s, "
+              f"{100 * tf / PEAK_BF16_TFLOPS:.1f}% MFMA), summaries {ms_summ * 1e3:.1f} us"
+              + (f", deviation from exact {r['rel_dev_from_exact_mean']:.3f}" if sample else ""),
+              file=sys.stderr, flush=True)
+        res[wk.name] = r
+        del Ks, Vs, O
+    cached.clear()
+    return res
 
 
 def bench_decode(args, torch, eva, inputs, dev):
