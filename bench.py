@@ -176,7 +176,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path. The EVA step shards "
+        print("bench.py measures one GPU only: the library has no multi-GPU path. The EVA step shards "
               "by (batch, kv head) with no exchange; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 

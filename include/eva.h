@@ -61,7 +61,7 @@ extern "C" {
 typedef enum {
     EVA_OK = 0,
     EVA_ERR_INVALID = -1,     /* bad shape, window, chunk size or null pointer */
-    EVA_ERR_UNSUPPORTED = -2, /* head dim, element type or size this build does not handle */
+    EVA_ERR_UNSUPPORTED = -2, /* head dim, element type or size the library does not handle */
     EVA_ERR_CAPACITY = -3,    /* cache ring or summary array too small */
     EVA_ERR_HIP = -4          /* the HIP runtime refused a launch */
 } eva_status;
