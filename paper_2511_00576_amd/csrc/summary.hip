@@ -155,6 +155,105 @@ __global__ __launch_bounds__(kSummaryThreads) void summary_kernel_reg(const T* _
     }
 }
 
+// One-wave variant (bf16): 64 threads per chunk, ROWS rows per thread, every
+// reduction inside the wave (shuffles only: no LDS, no barrier).
+template <int D, int ROWS, bool RF>
+__global__ __launch_bounds__(64) void summary_kernel_wave(const bf16* __restrict__ K, const bf16* __restrict__ V,
+                                                          bf16* __restrict__ Ks, bf16* __restrict__ Vs, int L,
+                                                          int n_chunks, const float* __restrict__ eps,
+                                                          float rf_scale) {
+    constexpr int TPR = D / 8;
+    constexpr int RPS = 64 / TPR;
+    constexpr int C = ROWS * RPS;
+    const int chunk = blockIdx.x;
+    const size_t bg = blockIdx.y;
+    const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
+    const size_t row0 = bg * (size_t)L + (size_t)chunk * C;
+    const bf16* kp = K + (row0 + r0) * D + cc * 8;
+    const bf16* vp = V + (row0 + r0) * D + cc * 8;
+    u32x4 kw[ROWS], vw[ROWS];
+    floatx4 ew[2];
+    if constexpr (RF) {
+        const float* ep = eps + (bg * n_chunks + chunk) * D + cc * 8;
+        ew[0] = *reinterpret_cast<const floatx4*>(ep);
+        ew[1] = *reinterpret_cast<const floatx4*>(ep + 4);
+    }
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        kw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + (size_t)i * RPS * D));
+        vw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vp + (size_t)i * RPS * D));
+    }
+    auto unpack = [](const u32x4& x, float out[8]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            out[2 * e] = bf16_lo(x[e]);
+            out[2 * e + 1] = bf16_hi(x[e]);
+        }
+    };
+    // sum over the lanes holding the same features (the row groups)
+    auto rows_sum = [](float& x) {
+#pragma unroll
+        for (int off = TPR; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
+    };
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] += k[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        rows_sum(kh[e]);
+        kh[e] *= 1.0f / (float)C;
+    }
+    const float sc = kLog2e * rsqrtf((float)D);
+    float w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        w[e] = RF ? kh[e] + rf_scale * fminf(fmaxf(ew[e >> 2][e & 3], -1.f), 1.f) : kh[e];
+    float s[ROWS];
+    float amax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x += (RF ? w[e] - 0.5f * k[e] : w[e]) * k[e];
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
+        s[i] = x * sc;
+        amax = fmaxf(amax, s[i]);
+    }
+#pragma unroll
+    for (int off = TPR; off < 64; off <<= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float v[8];
+        unpack(vw[i], v);
+        const float p = fast_exp2(s[i] - amax);
+        psum += p;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += p * v[e];
+    }
+    rows_sum(psum);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) rows_sum(acc[e]);
+    if (t < TPR) {
+        const float inv = 1.0f / psum;
+        const size_t out = (bg * n_chunks + chunk) * D + t * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            Ks[out + e] = to_bf16(kh[e]);
+            Vs[out + e] = to_bf16(acc[e] * inv);
+        }
+    }
+}
+
 template <int D, typename T, bool RF>
 hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
                                  const float* eps, float rf_scale, hipStream_t stream) {
@@ -165,6 +264,27 @@ hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* V
     const T* v = static_cast<const T*>(V);
     T* ks = static_cast<T*>(Ks);
     T* vs = static_cast<T*>(Vs);
+    if constexpr (sizeof(T) == 2) {
+        // one wave per chunk when the chunk is 4, 8 or 16 rows per thread of it
+        constexpr int RPW = 64 / (D / 8);
+        const dim3 grid(n_chunks, BH);
+        switch (C % RPW == 0 ? C / RPW : 0) {
+            case 4:
+                hipLaunchKernelGGL((summary_kernel_wave<D, 4, RF>), grid, dim3(64), 0, stream, k, v, ks, vs, L, n_chunks,
+                                   eps, rf_scale);
+                return hipGetLastError();
+            case 8:
+                hipLaunchKernelGGL((summary_kernel_wave<D, 8, RF>), grid, dim3(64), 0, stream, k, v, ks, vs, L, n_chunks,
+                                   eps, rf_scale);
+                return hipGetLastError();
+            case 16:
+                hipLaunchKernelGGL((summary_kernel_wave<D, 16, RF>), grid, dim3(64), 0, stream, k, v, ks, vs, L,
+                                   n_chunks, eps, rf_scale);
+                return hipGetLastError();
+            default:
+                break;
+        }
+    }
     if (C % RPS == 0 && C / RPS <= 16) {
         const dim3 grid(n_chunks, BH);
         switch (C / RPS) {
