@@ -40,6 +40,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 N_CACHES = 4
 N_LAYERS = 8
+WARMUP_S = 0.25
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 PREFILL_SOURCES = ("paper_2511_00576_amd/csrc/prefill_mfma.hip", "paper_2511_00576_amd/csrc/eva_device.hpp")
 DECODE_SOURCES = ("paper_2511_00576_amd/csrc/decode.hip", "paper_2511_00576_amd/csrc/eva_device.hpp",
@@ -133,21 +134,51 @@ def read_traffic(name, sources):
         return None
 
 
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo, as lscpu reports it)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w):
-    """The oracle on a bounded sample of the prefill workload, on this host."""
+    """The oracle on a bounded sample of the prefill workload, on this host:
+    all threads on two batch elements, then one thread on one (b, h) slice."""
+    import numpy as np
+
     import oracle
     from paper_2511_00576_amd import inputs
 
     n_batch = 2  # two of the eight sequences, every head, every row
     q, k, v = inputs.workload_qkv(w)
     qs, ks, vs = q[:n_batch], k[:n_batch], v[:n_batch]
+    threads = oracle.num_threads()
     t0 = time.perf_counter()
     oracle.prefill(qs, ks, vs, w.W, w.C)
     dt = time.perf_counter() - t0
     flops = n_batch * w.H * 4 * w.d * attended(w.L, w.W, w.C)
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+    # one (b, h) slice on one thread: its summaries and every row
+    oracle.set_num_threads(1)
+    try:
+        t1 = time.perf_counter()
+        Kb, Vb = k[0, 0].double().numpy(), v[0, 0].double().numpy()
+        Ks, Vs = oracle.summaries(Kb, Vb, w.C)
+        oracle.attend_rows(q[0, 0].double().numpy(), np.arange(w.L), Kb, Vb, Ks, Vs, w.W, w.C)
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_num_threads(threads)
+    flops1 = 4 * w.d * attended(w.L, w.W, w.C)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "nproc": os.cpu_count(),
             "sample": f"batch elements 0-{n_batch - 1} of {w.name} (all {w.H} heads, all {w.L} rows, "
-                      f"summaries included), {dt:.2f} s wall"}
+                      f"summaries included), {dt:.2f} s wall on {threads} threads",
+            "single_thread_slice": {"slice": f"(b, h) = (0, 0) of {w.name}: summaries and all {w.L} rows",
+                                    "seconds": dt1, "gflops": flops1 / dt1 / 1e9}}
 
 
 def main():
@@ -172,6 +203,9 @@ def main():
                     help="generated tokens per sequence (default: the workload's 1024)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device-to-device copy (counter scaling for profiles)")
+    ap.add_argument("--prefill-only", choices=sorted(PREFILL_ONLY),
+                    help="profiling mode: only this prefill workload's summaries and fused attention "
+                         "(--warmup launches, then --steps timed launches); prints its own JSON line")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -187,6 +221,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     eva._lib.load()
     dev = torch.device("cuda:0")
+    if args.prefill_only:
+        bench_prefill_only(args, torch, eva, inputs, dev)
+        return
     w = inputs.LLM_BF16
     B, H, Hkv, L, d, W, C = w.B, w.H, w.Hkv, w.L, w.d, w.W, w.C
     e = 2
@@ -224,10 +261,17 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    print(f"# warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    # warm-up: at least --warmup steps and at least WARMUP_S seconds of them
+    # (the clocks reach their steady state only after ~0.1 s of load)
+    print(f"# warmup >= {args.warmup} steps and >= {WARMUP_S} s, steps {args.steps}", file=sys.stderr, flush=True)
+    w0 = time.perf_counter()
+    n_warm = 0
+    while n_warm < args.warmup or time.perf_counter() - w0 < WARMUP_S:
+        for _ in range(10):
+            step()
+        n_warm += 10
+        torch.cuda.synchronize()
+    warm_s = time.perf_counter() - w0
     # the step time over K steps with no markers inside them; then K more
     # steps with an event between the parts for the breakdown
     t0 = torch.cuda.Event(enable_timing=True)
@@ -258,17 +302,20 @@ def main():
     ws_b = torch.empty((lib.eva_prefill_backward_workspace_bytes(B, H, Hkv, L, d, C) + 3) // 4, dtype=torch.float32,
                        device=dev)
     dQ_t, dK_t, dV_t = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    # the forward keeps its output's rounding residual, so the backward's row
+    # dots D = dO . O are exact (the training path the tests pin row by row)
+    Olo_t = torch.empty_like(O)
 
     def fwd_bwd(ev=None):
         if ev: ev[0].record()
         eva._lib.check("eva_prefill_forward", lib.eva_prefill_forward(
             eva._ptr(q), eva._ptr(k), eva._ptr(v), eva._ptr(Ks), eva._ptr(Vs), eva._ptr(O), eva._ptr(lse_t),
-            B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
+            eva._ptr(Olo_t), B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
         if ev: ev[1].record()
         eva._lib.check("eva_prefill_backward", lib.eva_prefill_backward(
-            eva._ptr(q), eva._ptr(k), eva._ptr(v), eva._ptr(Ks), eva._ptr(Vs), eva._ptr(O), eva._ptr(dO_t),
-            eva._ptr(lse_t), eva._ptr(dQ_t), eva._ptr(dK_t), eva._ptr(dV_t), eva._ptr(ws_b), ws_b.numel() * 4,
-            B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
+            eva._ptr(q), eva._ptr(k), eva._ptr(v), eva._ptr(Ks), eva._ptr(Vs), eva._ptr(O), eva._ptr(Olo_t),
+            eva._ptr(dO_t), eva._ptr(lse_t), eva._ptr(dQ_t), eva._ptr(dK_t), eva._ptr(dV_t), eva._ptr(ws_b),
+            ws_b.numel() * 4, B, H, Hkv, L, d, W, C, eva._lib.EVA_BF16, eva._stream()))
         if ev: ev[2].record()
 
     fwd_bwd()
@@ -280,10 +327,10 @@ def main():
     ms_fwd_t = sum(e[0].elapsed_time(e[1]) for e in tev) / n_tr
     ms_bwd_t = sum(e[1].elapsed_time(e[2]) for e in tev) / n_tr
     bwd_flops = B * H * 10 * d * attended(L, W, C)
-    training = {"forward_lse_ms": ms_fwd_t, "backward_ms": ms_bwd_t, "backward_alg_flops": bwd_flops,
+    training = {"output_residual": True, "forward_lse_ms": ms_fwd_t, "backward_ms": ms_bwd_t, "backward_alg_flops": bwd_flops,
                 "backward_tflops": bwd_flops / (ms_bwd_t * 1e-3) / 1e12,
                 "backward_mfma_frac": bwd_flops / (ms_bwd_t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
-    del dO_t, dQ_t, dK_t, dV_t, ws_b
+    del dO_t, dQ_t, dK_t, dV_t, ws_b, Olo_t
 
     # window variants of the fused kernel on the same inputs (summaries as built)
     variants = {}
@@ -330,6 +377,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_run": {"steps": n_warm, "seconds": warm_s},
         "ms_per_step": ms_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -365,6 +413,45 @@ def main():
         print("# oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
+
+
+def prefill_only_workload(name, inputs):
+    import dataclasses
+    lw = inputs.LONG_BF16
+    if name.startswith("long"):
+        c = int(name[4:])
+        return dataclasses.replace(lw, C=c, name=lw.name.replace("C256", f"C{c}"))
+    return {"llm": inputs.LLM_BF16, "gqa": inputs.GQA_BF16}[name]
+
+
+def bench_prefill_only(args, torch, eva, inputs, dev):
+    """One prefill workload alone (for per-kernel profiles): summaries once,
+    then --warmup and --steps fused-attention launches."""
+    wk = prefill_only_workload(args.prefill_only, inputs)
+    print(f"# prefill-only {wk.name}", file=sys.stderr, flush=True)
+    q, k, v = (t.to(dev) for t in inputs.workload_qkv(wk))
+    Ks, Vs = eva.build_summaries(k, v, wk.C)
+    O = torch.empty_like(q)
+    for _ in range(args.warmup):
+        eva.prefill_attention(q, k, v, Ks, Vs, wk.W, wk.C, out=O)
+    torch.cuda.synchronize()
+    a0 = torch.cuda.Event(enable_timing=True)
+    a1 = torch.cuda.Event(enable_timing=True)
+    n = max(args.steps, 1)
+    a0.record()
+    for _ in range(n):
+        eva.prefill_attention(q, k, v, Ks, Vs, wk.W, wk.C, out=O)
+    a1.record()
+    torch.cuda.synchronize()
+    ms = a0.elapsed_time(a1) / n
+    flops = wk.B * wk.H * 4 * wk.d * attended(wk.L, wk.W, wk.C)
+    tf = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({"prefill_only": wk.name, "launches": args.warmup + n, "attention_ms": ms, "alg_flops": flops,
+                      "tflops": tf, "mfma_frac": tf / PEAK_BF16_TFLOPS,
+                      "prefill_source_sha": source_sha(PREFILL_SOURCES)}), flush=True)
+
+
+PREFILL_ONLY = ("llm", "gqa", "long64", "long128", "long256")
 
 
 def bench_other_prefill(args, torch, eva, inputs, dev):

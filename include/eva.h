@@ -94,8 +94,13 @@ typedef enum {
 
 /*
  * Decode cache: the state one decoded token needs — the exact keys/values of
- * the window and the chunk summaries (FlashEVA keeps a compressed cache whose
- * size grows with the number of chunks, not tokens).
+ * the window and the chunk summaries.  The paper's cache of compressed past
+ * context (sections "Introduction" and "Conclusion"; section "Related Work":
+ * chunks of tokens summarized into single tokens inside the attention
+ * itself): it grows by one summary per C tokens, plus a fixed window.
+ * Generation reads it once per token, so decode is bound by memory bandwidth
+ * (section "Inference throughput and Memory usage"); the layout below is
+ * chosen for that read.
  *
  * The struct is caller-owned host memory; the four arrays are caller-owned
  * device memory of the cache's dtype.  Position p of (b, g) lives in ring slot
@@ -207,10 +212,18 @@ int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, 
  * for every row, lse[b][h][n] = natural log of the sum of exp(logits) over
  * the row's window keys and summaries (logits q.k / sqrt(d), + ln C for a
  * summary), fp32 [B][H][L], as eva_prefill_backward needs it.
- * Errors: as eva_prefill_attention; INVALID for a null lse.
+ * O_lo (optional, EVA_BF16 only, NULL to skip): [B][H][L][d] receives the
+ * rounding residual of the bf16 output, bf16(o - bf16(o)) for the fp32 row o,
+ * so that O + O_lo holds o to about 16 bits.  Passed to eva_prefill_backward
+ * it makes the row dots D = dO . o exact to that precision; without it D is
+ * taken from the bf16 O, whose rounding moves each gradient row by up to
+ * ~2^-8 |dO| |O| |k| / sqrt(d) whatever the row's own magnitude.
+ * Errors: as eva_prefill_attention; INVALID for a null lse, or an O_lo that
+ * is misaligned or given with EVA_F32.
  */
 int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
-                        float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream);
+                        float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                        void* stream);
 
 /*
  * Backward of the EVA prefill (sliding window, bf16): given dO [B][H][L][d],
@@ -220,7 +233,8 @@ int eva_prefill_forward(const void* Q, const void* K, const void* V, const void*
  * (the mean key, and the softmax(mean . k / sqrt(d))-weighted value; the
  * ln C offset is a constant).  Inputs: the forward's Q, K, V, its summaries
  * Ksum, Vsum [B][H_kv][L / C][d] (eva_build_summaries), its output O and lse
- * (eva_prefill_forward).  The softmax is recomputed from lse, so nothing of
+ * (eva_prefill_forward), and optionally its output residual O_lo (NULL: the
+ * row dots D = dO . O use the bf16 O alone).  The softmax is recomputed from lse, so nothing of
  * size L x L is stored (FlashAttention-style, section "FlashAttention").
  * ws: caller-owned device scratch of eva_prefill_backward_workspace_bytes()
  * bytes (fp32 row dots, summary gradients, and per-chunk and per-key factors
@@ -229,15 +243,18 @@ int eva_prefill_forward(const void* Q, const void* K, const void* V, const void*
  * other than EVA_BF16, d not 64 or 128), CAPACITY (workspace too small).
  */
 int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
-                         const void* O, const void* dO, const float* lse, void* dQ, void* dK, void* dV, void* ws,
-                         size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
-                         void* stream);
+                         const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK,
+                         void* dV, void* ws, size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C,
+                         int dtype, void* stream);
 
 /* Workspace eva_prefill_backward needs (0 for invalid sizes). */
 size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d, int C);
 
 /*
- * Load a decode cache from a prefilled sequence of L tokens: the last
+ * Load a decode cache from a prefilled sequence of L tokens (the prompt of a
+ * generation, section "Experimental setup" / "Inference throughput and Memory
+ * usage"; what the cache holds is the window and summary set of section
+ * "FlashEVA" for the next position): the last
  * min(L, R) keys/values go to ring slots p mod R and the L / C summaries
  * (as built by eva_build_summaries) to the summary arrays; n_tok becomes L.
  * K, V [H_kv][L][d] per batch row as in eva_prefill; all four device
@@ -249,8 +266,10 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
                    int L, void* stream);
 
 /*
- * Append one token per sequence: k_new, v_new [B][H_kv][d].  The token takes
- * position p = cache->n_tok.  If it is the last token of chunk
+ * Append one token per sequence (autoregressive generation, section
+ * "Inference throughput and Memory usage"; the summary it may complete is
+ * the chunk summary of section "EVA Attention", as in eva_build_summaries):
+ * k_new, v_new [B][H_kv][d].  The token takes position p = cache->n_tok.  If it is the last token of chunk
  * S = (p + 1) / C - 1 (p + 1 a multiple of C), that chunk's summary is built
  * from the chunk's other C - 1 rows in the ring and the token itself; the
  * token is written to slot p mod R and n_tok becomes p + 1.  (A chunk is
@@ -261,25 +280,31 @@ int eva_cache_fill(eva_cache* cache, const void* K, const void* V, const void* K
 int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, void* stream);
 
 /*
- * One decode step: q [B][H][d] is the query of position p = n_tok - 1 (the
- * token appended last); o [B][H][d] receives its EVA attention output over
- * the ring window [p-W+1, p] and the summaries c < s(p).  Row p of the
- * prefill of the same tokens gives the same result up to rounding order.
+ * One decode step (section "FlashEVA": the softmax over the window keys and
+ * the visible summaries, for a single query; section "Inference throughput
+ * and Memory usage": one such step per generated token): q [B][H][d] is the
+ * query of position p = n_tok - 1 (the token appended last); o [B][H][d]
+ * receives its EVA attention output over the ring window [p-W+1, p] and the
+ * summaries c < s(p).  Row p of the prefill of the same tokens gives the same
+ * result up to rounding order.
  * `ws` is optional device scratch of `ws_bytes` bytes: with at least
  * eva_decode_workspace_bytes(cache) bytes the rows of each sequence are split
  * over more workgroups (for small B * H_kv); with less (or NULL) the call
  * still works, one workgroup per (b, kv head, 16 query heads).
- * Errors: INVALID (n_tok == 0, null pointers, malformed cache).
+ * Errors: INVALID (n_tok == 0, null pointers, malformed cache), UNSUPPORTED
+ * (a cache of dtype EVA_F32: decode runs on bf16 caches only).
  */
 int eva_decode_step(const eva_cache* cache, const void* q, void* o,
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Fused per-token step: eva_cache_append(k_new, v_new) followed by
+ * Fused per-token step of generation (section "Inference throughput and
+ * Memory usage"): eva_cache_append(k_new, v_new) followed by
  * eva_decode_step(q) in one launch, with the same results (the decoded row
  * reads the new token from k_new, v_new while another workgroup writes it to
  * the ring; the summary the token completes is built beside the decode).
- * Errors: as eva_cache_append and eva_decode_step.
+ * Errors: as eva_cache_append and eva_decode_step (UNSUPPORTED for an
+ * EVA_F32 cache).
  */
 int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o,
                       void* ws, size_t ws_bytes, void* stream);

@@ -52,8 +52,13 @@ def _load():
     lib.eva_ref_backward_group.restype = None
     lib.eva_ref_backward_group.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
                                            ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
+    lib.eva_ref_backward_terms.restype = None
+    lib.eva_ref_backward_terms.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
+                                           ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
     lib.eva_ref_num_threads.restype = ctypes.c_int
     lib.eva_ref_num_threads.argtypes = []
+    lib.eva_ref_set_num_threads.restype = None
+    lib.eva_ref_set_num_threads.argtypes = [ctypes.c_int]
     _lib = lib
     return lib
 
@@ -70,6 +75,11 @@ def _ptr(a):
 
 def num_threads() -> int:
     return int(_load().eva_ref_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on."""
+    _load().eva_ref_set_num_threads(int(n))
 
 
 def visible_summaries(n: int, W: int, C: int) -> int:
@@ -196,3 +206,32 @@ def backward(Q, K, V, dO, W: int, C: int):
             dK[b, g] = dk
             dV[b, g] = dv
     return dQ, dK, dV
+
+
+def backward_terms(Q, K, V, dO, W: int, C: int):
+    """Term magnitudes of backward() (rounding-error scales, not part of the
+    method): for every gradient entry the sum of the absolute values of the
+    terms it sums, carried through the same steps.  Same shapes as
+    backward(); returns (Tq, Tk, Tv)."""
+    Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
+    B, H, L, d = Q.shape
+    Hkv = K.shape[1]
+    G = H // Hkv
+    Tq = np.zeros_like(Q)
+    Tk = np.zeros_like(K)
+    Tv = np.zeros_like(V)
+    lib = _load()
+    for b in range(B):
+        for g in range(Hkv):
+            q = np.ascontiguousarray(Q[b, g * G:(g + 1) * G])
+            go = np.ascontiguousarray(dO[b, g * G:(g + 1) * G])
+            tq = np.zeros_like(q)
+            tk = np.zeros((L, d))
+            tv = np.zeros((L, d))
+            lib.eva_ref_backward_terms(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])),
+                                       _ptr(np.ascontiguousarray(V[b, g])), _ptr(go), G, L, d, W, C, _ptr(tq),
+                                       _ptr(tk), _ptr(tv))
+            Tq[b, g * G:(g + 1) * G] = tq
+            Tk[b, g] = tk
+            Tv[b, g] = tv
+    return Tq, Tk, Tv

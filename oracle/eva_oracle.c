@@ -488,6 +488,136 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
     free(dVs);
 }
 
+/* Term magnitudes of eva_ref_backward_group, for rounding-error bounds (test
+ * infrastructure: not part of the method).  Each gradient entry is a sum of
+ * terms; this returns, per entry, the sum of the terms' absolute values,
+ * carried through the same steps: a term that is itself a sum (the summary
+ * gradients dkhat, dvhat and the chunk-logit gradients da_j) contributes the
+ * magnitude of its own terms.  A floating-point evaluation that rounds each
+ * term to relative precision u is then off by at most about u times this
+ * magnitude, however much the terms cancel.  Same arguments and layouts as
+ * eva_ref_backward_group; Tq, Tk, Tv take the places of dQ, dK, dV. */
+void eva_ref_backward_terms(const double* Q, const double* K, const double* V, const double* dO,
+                            int G, long L, int d, long W, long C,
+                            double* Tq, double* Tk, double* Tv)
+{
+    double inv_sqrt_d = 1.0 / sqrt((double)d);
+    long n_chunks = L / C;
+    size_t nc1 = (size_t)(n_chunks > 0 ? n_chunks : 1);
+    double* Ks = (double*)calloc(nc1 * d, sizeof(double));
+    double* Vs = (double*)calloc(nc1 * d, sizeof(double));
+    double* Tks = (double*)calloc(nc1 * d, sizeof(double));
+    double* Tvs = (double*)calloc(nc1 * d, sizeof(double));
+    eva_ref_summaries(K, V, L, d, C, Ks, Vs);
+    memset(Tk, 0, (size_t)L * d * sizeof(double));
+    memset(Tv, 0, (size_t)L * d * sizeof(double));
+
+    double* logit = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    double* p = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    double* o = (double*)malloc((size_t)d * sizeof(double));
+    for (int h = 0; h < G; ++h) {
+        for (long n = 0; n < L; ++n) {
+            const double* q = Q + ((size_t)h * L + n) * d;
+            const double* g = dO + ((size_t)h * L + n) * d;
+            double* tq = Tq + ((size_t)h * L + n) * d;
+            long lo = n - W + 1 < 0 ? 0 : n - W + 1;
+            long n_win = n - lo + 1;
+            long count = n_win + eva_ref_visible_summaries(n, W, C);
+            double lmax = -INFINITY;
+            for (long i = 0; i < count; ++i) {
+                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                double s = 0.0;
+                for (int e = 0; e < d; ++e) s += q[e] * key[e];
+                logit[i] = s * inv_sqrt_d + (i < n_win ? 0.0 : log((double)C));
+                if (logit[i] > lmax) lmax = logit[i];
+            }
+            double den = 0.0;
+            for (long i = 0; i < count; ++i) {
+                p[i] = exp(logit[i] - lmax);
+                den += p[i];
+            }
+            for (long i = 0; i < count; ++i) p[i] /= den;
+            for (int e = 0; e < d; ++e) {
+                double acc = 0.0;
+                for (long i = 0; i < count; ++i) {
+                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                    acc += p[i] * val[e];
+                }
+                o[e] = acc;
+            }
+            double D = 0.0;
+            for (int e = 0; e < d; ++e) D += g[e] * o[e];
+            for (int e = 0; e < d; ++e) tq[e] = 0.0;
+            for (long i = 0; i < count; ++i) {
+                const int win = i < n_win;
+                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                double* tkey = win ? Tk + (size_t)(lo + i) * d : Tks + (size_t)(i - n_win) * d;
+                double* tval = win ? Tv + (size_t)(lo + i) * d : Tvs + (size_t)(i - n_win) * d;
+                double gv = 0.0;
+                for (int e = 0; e < d; ++e) gv += g[e] * val[e];
+                const double dl = fabs(p[i] * (gv - D));
+                for (int e = 0; e < d; ++e) {
+                    tq[e] += dl * fabs(key[e]) * inv_sqrt_d;
+                    tkey[e] += dl * fabs(q[e]) * inv_sqrt_d;
+                    tval[e] += p[i] * fabs(g[e]);
+                }
+            }
+        }
+    }
+    /* through the summaries, magnitudes of dvhat (Tvs) and dkhat's direct
+     * part (Tks) standing for those sums */
+    double* a = (double*)malloc((size_t)C * sizeof(double));
+    double* b = (double*)malloc((size_t)C * sizeof(double));
+    double* tkh = (double*)malloc((size_t)d * sizeof(double));
+    for (long c = 0; c < n_chunks; ++c) {
+        const double* Kc = K + (size_t)c * C * d;
+        const double* Vc = V + (size_t)c * C * d;
+        const double* kh = Ks + (size_t)c * d;
+        const double* vh = Vs + (size_t)c * d;
+        const double* tgk = Tks + (size_t)c * d;
+        const double* tgv = Tvs + (size_t)c * d;
+        double amax = -INFINITY;
+        for (long j = 0; j < C; ++j) {
+            double s = 0.0;
+            for (int e = 0; e < d; ++e) s += kh[e] * Kc[(size_t)j * d + e];
+            a[j] = s * inv_sqrt_d;
+            if (a[j] > amax) amax = a[j];
+        }
+        double den = 0.0;
+        for (long j = 0; j < C; ++j) {
+            b[j] = exp(a[j] - amax);
+            den += b[j];
+        }
+        for (long j = 0; j < C; ++j) b[j] /= den;
+        double tgv_vh = 0.0;
+        for (int e = 0; e < d; ++e) tgv_vh += tgv[e] * fabs(vh[e]);
+        for (int e = 0; e < d; ++e) tkh[e] = tgk[e];
+        for (long j = 0; j < C; ++j) {
+            double tgv_v = 0.0;
+            for (int e = 0; e < d; ++e) tgv_v += tgv[e] * fabs(Vc[(size_t)j * d + e]);
+            const double tda = b[j] * (tgv_v + tgv_vh);
+            for (int e = 0; e < d; ++e) {
+                Tv[((size_t)c * C + j) * d + e] += b[j] * tgv[e];
+                tkh[e] += tda * fabs(Kc[(size_t)j * d + e]) * inv_sqrt_d;
+                Tk[((size_t)c * C + j) * d + e] += tda * fabs(kh[e]) * inv_sqrt_d;
+            }
+        }
+        for (long j = 0; j < C; ++j)
+            for (int e = 0; e < d; ++e) Tk[((size_t)c * C + j) * d + e] += tkh[e] / (double)C;
+    }
+    free(a);
+    free(b);
+    free(tkh);
+    free(logit);
+    free(p);
+    free(o);
+    free(Ks);
+    free(Vs);
+    free(Tks);
+    free(Tvs);
+}
+
 int eva_ref_num_threads(void)
 {
 #ifdef _OPENMP
@@ -495,5 +625,17 @@ int eva_ref_num_threads(void)
     return omp_get_max_threads();
 #else
     return 1;
+#endif
+}
+
+/* Threads the parallel loops use from now on (timing of a single-thread
+ * slice); n < 1 is ignored. */
+void eva_ref_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
 #endif
 }

@@ -95,10 +95,10 @@ def load():
     lib.eva_prefill_ex.restype = i
     lib.eva_prefill_ex.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_prefill_forward.restype = i
-    lib.eva_prefill_forward.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    lib.eva_prefill_forward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
     lib.eva_prefill_backward.restype = i
-    lib.eva_prefill_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i, i, i,
-                                         vp]
+    lib.eva_prefill_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i, i,
+                                         i, vp]
     lib.eva_prefill_backward_workspace_bytes.restype = sz
     lib.eva_prefill_backward_workspace_bytes.argtypes = [i, i, i, i, i, i]
     lib.eva_cache_fill.restype = i

@@ -219,16 +219,20 @@ void bwd_dq_kernel(BwdParams a) {
         const bf16* qrow = static_cast<const bf16*>(a.Q) + (row0 + n) * D;
         const bf16* grow = static_cast<const bf16*>(a.dO) + (row0 + n) * D;
         const bf16* orow = static_cast<const bf16*>(a.O) + (row0 + n) * D;
-        // D = dO . O of the column: this lane's 8 NDC features, then the four
-        // lanes (g) of the column; stored for the dK/dV kernels
+        const bf16* lrow = a.O_lo ? static_cast<const bf16*>(a.O_lo) + (row0 + n) * D : nullptr;
+        // D = dO . O of the column (O + O_lo when the forward kept its output's
+        // rounding residual): this lane's 8 NDC features, then the four lanes
+        // (g) of the column; stored for the dK/dV kernels
         float dot = 0.f;
 #pragma unroll
         for (int dc = 0; dc < NDC; ++dc) {
             qf[cb][dc] = *reinterpret_cast<const bf16x8*>(qrow + dc * 32 + g * 8);
             gf[cb][dc] = *reinterpret_cast<const bf16x8*>(grow + dc * 32 + g * 8);
             const bf16x8 of = *reinterpret_cast<const bf16x8*>(orow + dc * 32 + g * 8);
+            bf16x8 lf = {};
+            if (lrow) lf = *reinterpret_cast<const bf16x8*>(lrow + dc * 32 + g * 8);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) dot += (float)gf[cb][dc][e] * (float)of[e];
+            for (int e = 0; e < 8; ++e) dot += (float)gf[cb][dc][e] * ((float)of[e] + (float)lf[e]);
         }
         dcol[cb] = xgroup_sum(dot);
         if (g == 0 && col_n[cb] < L) a.Dv[row0 + n] = dcol[cb];

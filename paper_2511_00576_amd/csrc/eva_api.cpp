@@ -267,25 +267,28 @@ static PrefillTiles prefill_tiles(int B, int H, int H_kv, int L, int W, int dtyp
 }
 
 static int prefill_attention_impl(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
-                                  void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
-                                  int window, void* stream);
+                                  void* O, float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C,
+                                  int dtype, int window, void* stream);
 
 int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
                              void* O, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, int window,
                              void* stream) {
-    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, nullptr, B, H, H_kv, L, d, W, C, dtype, window, stream);
-}
-
-int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
-                        float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype, void* stream) {
-    if (!lse) return EVA_ERR_INVALID;
-    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, lse, B, H, H_kv, L, d, W, C, dtype, EVA_WINDOW_SLIDING,
+    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, nullptr, nullptr, B, H, H_kv, L, d, W, C, dtype, window,
                                   stream);
 }
 
+int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                        float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                        void* stream) {
+    if (!lse) return EVA_ERR_INVALID;
+    if (O_lo && (dtype != EVA_BF16 || !aligned16(O_lo))) return EVA_ERR_INVALID;
+    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, lse, O_lo, B, H, H_kv, L, d, W, C, dtype,
+                                  EVA_WINDOW_SLIDING, stream);
+}
+
 static int prefill_attention_impl(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
-                                  void* O, float* lse, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
-                                  int window, void* stream) {
+                                  void* O, float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C,
+                                  int dtype, int window, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
     if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     if (!valid_window(window)) return EVA_ERR_INVALID;
@@ -324,6 +327,7 @@ static int prefill_attention_impl(const void* Q, const void* K, const void* V, c
     p.log2C = (float)log2((double)C);
     p.window = window;
     p.lse = lse;
+    p.O_lo = O_lo;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return hip_status(dispatch(d, dtype, [&](auto dd, auto t) {
         if constexpr (std::is_same<decltype(t), eva::bf16>::value)
@@ -442,13 +446,13 @@ static int uniform_decode(const eva_cache* cache, long long pos, const void* q, 
     const int units = cache->B * cache->H_kv * p.n_hg;
     p.splits = decode_splits(units, n_chunks);
     const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
+    hipStream_t s = static_cast<hipStream_t>(stream);
     if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
     p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
     p.log2C = (float)log2((double)cache->C);
     p.k_new = k_new;
     p.v_new = v_new;
-    hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
     return hip_status(e);
 }
@@ -511,7 +515,8 @@ size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d
 }
 
 int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
-                         const void* O, const void* dO, const float* lse, void* dQ, void* dK, void* dV, void* ws,
+                         const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK, void* dV,
+                         void* ws,
                          size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                          void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
@@ -525,6 +530,7 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
     const void* must[] = {Q, K, V, O, dO, lse, dQ, dK, dV, ws};
     for (const void* ptr : must)
         if (!ptr || !aligned16(ptr)) return EVA_ERR_INVALID;
+    if (O_lo && !aligned16(O_lo)) return EVA_ERR_INVALID;
     const int n_chunks = L / C;
     if (n_chunks > 0 && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum))) return EVA_ERR_INVALID;
     const BwdLayout lay = bwd_layout(B, H, H_kv, L, d, C);
@@ -537,6 +543,7 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
     p.Ks = Ksum;
     p.Vs = Vsum;
     p.O = O;
+    p.O_lo = O_lo;
     p.dO = dO;
     p.lse = lse;
     p.dQ = dQ;

@@ -39,6 +39,8 @@ struct PrefillParams {
     float log2C;      // log2(C): the ln C summary offset in log2 units
     int window;       // window variant (kWin* in eva_device.hpp)
     float* lse;       // optional [B][H][L]: natural log of each row's softmax denominator
+    void* O_lo;       // optional, bf16 only, [B][H][L][d]: the output's rounding residual
+                      // bf16(o - bf16(o)), so that O + O_lo carries o to ~16 bits
 };
 
 template <int D, typename T>
@@ -53,6 +55,7 @@ struct BwdParams {
     const void* Ks;  // [B][Hkv][n_chunks][d], the forward's summaries
     const void* Vs;
     const void* O;
+    const void* O_lo;  // optional [B][H][L][d]: the forward's output residual (D = dO . (O + O_lo))
     const void* dO;
     const float* lse;  // [B][H][L], natural log of each row's softmax denominator
     void* dQ;

@@ -103,7 +103,10 @@ __device__ __forceinline__ int lower_state(int c) { return c >= 16 ? 0 : (c < 0 
 // e = e1 (>= 0) or e = e1 - 16 (< 0), e1 = (W - 1) mod 16.
 __device__ __forceinline__ int upper_state(int e) { return e >= 15 ? 0 : (e < -15 ? 1 : (e >= 0 ? 2 : 3)); }
 
-template <int D, int NW, int NCB, int NS, int BN, int WPE, int VAR>
+// LO: also store the output's rounding residual (training forward); a
+// separate instantiation, since even an untaken branch for it in the epilogue
+// measured 6-8% slower in the 4-wave configuration.
+template <int D, int NW, int NCB, int NS, int BN, int WPE, int VAR, bool LO>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void prefill_mfma_kernel(PrefillParams a) {
     typedef MCfg<D, NW, NCB, NS, BN> Cfg;
@@ -296,7 +299,15 @@ void prefill_mfma_kernel(PrefillParams a) {
         l_acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
-    floatx4 s0[NKB][NCB], s1[NKB][NCB];  // scores of two consecutive blocks
+    // scores of two consecutive blocks.  s1 starts at zero: a wave that needs
+    // neither block 0 nor block 1 skips iteration 0, so s1 is first read (as
+    // the scores of a block it does not need, whose weights must come out 0)
+    // before any product wrote it.
+    floatx4 s0[NKB][NCB], s1[NKB][NCB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) s1[kb][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     bf16x8 pf[NKC][NCB];             // P^T of the current block, per 32-key half
     float lm[NCB], alpha[NCB];
     bool pending = false;            // rescale owed to the accumulators
@@ -629,10 +640,17 @@ void prefill_mfma_kernel(PrefillParams a) {
         // natural log of the softmax denominator: sum 2^(x - m_run) = l
         if (a.lse && g == 0) a.lse[bh * L + n] = (m_run[cb] + __builtin_amdgcn_logf(l_acc[cb][0])) * kLn2;
         bf16* orow = O + (bh * L + (size_t)n) * D;
+        bf16* lorow = LO ? static_cast<bf16*>(a.O_lo) + (bh * L + (size_t)n) * D : nullptr;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
             const floatx4 v = acc[db][cb] * inv;
             u32x2 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+            if constexpr (LO) {
+                // residual of the rounding: what the bf16 output lost
+                const u32x2 r = {pack_bf16x2(v[0] - bf16_lo(w[0]), v[1] - bf16_hi(w[0])),
+                                 pack_bf16x2(v[2] - bf16_lo(w[1]), v[3] - bf16_hi(w[1]))};
+                *reinterpret_cast<u32x2*>(lorow + db * 16 + g * 4) = r;
+            }
             // non-temporal in the 4-wave configuration: measured on MI355X,
             // 347 -> 342 us (LLM workload) there, but 675 -> 720 us with the
             // 8-wave configuration (long workload)
@@ -646,21 +664,27 @@ void prefill_mfma_kernel(PrefillParams a) {
 
 }  // namespace
 
-template <int D, int VAR>
+template <int D, int VAR, bool LO = false>
 void launch_prefill_mfma_var(const PrefillParams& p, hipStream_t stream) {
     if (prefill_mfma_narrow(p.G, p.W)) {
         // 4 waves x 32 columns, 32-key blocks: 77 KB of LDS, two workgroups per CU
-        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2, VAR>), dim3(p.n_tiles),
-                           dim3(kMfmaWavesNarrow * 64), 0, stream, p);
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesNarrow, kMfmaColBlocks, 4, 32, 2, VAR, LO>),
+                           dim3(p.n_tiles), dim3(kMfmaWavesNarrow * 64), 0, stream, p);
     } else {
         // 8 waves x 32 columns, 64-key blocks: 141 KB of LDS, one workgroup per CU
-        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesWide, kMfmaColBlocks, 4, 64, 2, VAR>), dim3(p.n_tiles),
-                           dim3(kMfmaWavesWide * 64), 0, stream, p);
+        hipLaunchKernelGGL((prefill_mfma_kernel<D, kMfmaWavesWide, kMfmaColBlocks, 4, 64, 2, VAR, LO>),
+                           dim3(p.n_tiles), dim3(kMfmaWavesWide * 64), 0, stream, p);
     }
 }
 
 template <int D>
 hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
+    if (p.O_lo) {
+        // the training forward (sliding window only)
+        if (p.window != kWinSliding) return hipErrorInvalidValue;
+        launch_prefill_mfma_var<D, kWinSliding, true>(p, stream);
+        return hipGetLastError();
+    }
     switch (p.window) {
         case kWinChunkAligned: launch_prefill_mfma_var<D, kWinChunkAligned>(p, stream); break;
         case kWinBlocked: launch_prefill_mfma_var<D, kWinBlocked>(p, stream); break;

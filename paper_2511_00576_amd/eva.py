@@ -357,27 +357,37 @@ def generate(cache: RaggedCache, q, k, v, active=None, out=None, use_workspace=T
     return o
 
 
-def prefill_forward(Q, K, V, W: int, C: int):
+def prefill_forward(Q, K, V, W: int, C: int, residual: bool = False):
     """Training forward (sliding window): summaries, O and the per-row
-    log-sum-exp.  Returns (O, lse, Ks, Vs); lse is fp32 [B, H, L]."""
+    log-sum-exp.  Returns (O, lse, Ks, Vs); lse is fp32 [B, H, L].  With
+    `residual` (bf16) also the output's rounding residual O_lo:
+    (O, lse, Ks, Vs, O_lo)."""
     _require_device(Q, K, V)
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
     Ks, Vs = build_summaries(K, V, C)
     O = torch.empty_like(Q)
+    O_lo = torch.empty_like(Q) if residual else None
     lse = torch.empty(B, H, L, dtype=torch.float32, device=Q.device)
     n_chunks = L // C
     _lib.check("eva_prefill_forward",
                _lib.load().eva_prefill_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
-                                               _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(lse), B, H, Hkv, L, d, W,
-                                               C, _dtype_code(Q), _stream()))
+                                               _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(lse), _ptr(O_lo), B, H,
+                                               Hkv, L, d, W, C, _dtype_code(Q), _stream()))
+    if residual:
+        return O, lse, Ks, Vs, O_lo
     return O, lse, Ks, Vs
 
 
-def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None):
+def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None, O_lo=None):
     """Gradients (dQ, dK, dV) of the EVA prefill for the output gradient dO
-    (bf16, sliding window), from the training forward's O, lse and summaries."""
+    (bf16, sliding window), from the training forward's O, lse and summaries
+    (and, if it kept one, its output residual O_lo)."""
     _require_device(Q, K, V, O, lse, dO)
+    if O_lo is not None:
+        _require_device(O_lo)
+        if O_lo.shape != O.shape or O_lo.dtype != O.dtype:
+            raise ValueError("O_lo must match O")
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
     if dO.shape != Q.shape or O.shape != Q.shape or tuple(lse.shape) != (B, H, L) or lse.dtype != torch.float32:
@@ -393,7 +403,8 @@ def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None
     n_chunks = L // C
     _lib.check("eva_prefill_backward",
                lib.eva_prefill_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
-                                        _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(dO), _ptr(lse), _ptr(dQ),
+                                        _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(O_lo), _ptr(dO), _ptr(lse),
+                                        _ptr(dQ),
                                         _ptr(dK), _ptr(dV), _ptr(ws), ws.numel() * ws.element_size(), B, H, Hkv, L, d,
                                         W, C, _dtype_code(Q), _stream()))
     return dQ, dK, dV

@@ -138,3 +138,40 @@ def spike_qkv(B, H, Hkv, L, d, dtype=torch.bfloat16, seed=0, alpha=3.0):
             k[b, hk, pos[b, hk]] = alpha * u
     q = q * 0.25 + alpha * u
     return q.to(dtype), k.to(dtype), v.to(dtype)
+
+
+def spike_at_qkv(B, H, Hkv, L, d, positions, chunks=(), C=1, dtype=torch.bfloat16, seed=0, alpha=3.0):
+    """Mask probe with spikes at chosen places: N(0,1) Q, K, V; the keys at
+    `positions`, and every key of the chunks in `chunks` (chunk c covers
+    [cC, cC + C)), are set to alpha * u in every (b, kv head), and every query
+    gets + alpha * u (u a seeded direction of norm sqrt(d)).  A row that
+    attends one of those keys, or the summary of a wholly spiked chunk, is
+    dominated by it, so a single key wrongly in or out of a window, or a
+    summary wrongly visible or hidden, moves the row by O(1)."""
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(B, H, L, d, generator=g)
+    k = torch.randn(B, Hkv, L, d, generator=g)
+    v = torch.randn(B, Hkv, L, d, generator=g)
+    u = torch.randn(d, generator=g)
+    u = u / u.norm() * (d ** 0.5)
+    idx = sorted({int(p) for p in positions if 0 <= p < L})
+    for c in chunks:
+        idx.extend(range(c * C, min((c + 1) * C, L)))
+    if idx:
+        k[:, :, torch.tensor(sorted(set(idx)))] = alpha * u
+    q = q * 0.25 + alpha * u
+    return q.to(dtype), k.to(dtype), v.to(dtype)
+
+
+def window_edge_positions(L, W, C, anchors):
+    """Key positions that sit on the window and chunk edges of the rows in
+    `anchors`: for row n the first and the last key before its window
+    (n - W + 1, n - W), the key two before it, and the last token of the
+    last chunk wholly before the window.  Geometry only."""
+    pos = set()
+    for n in anchors:
+        lo = n - W + 1
+        pos.update((lo, lo - 1, lo - 2))
+        if lo > 0 and lo // C > 0:
+            pos.add((lo // C) * C - 1)
+    return sorted(p for p in pos if 0 <= p < L)

@@ -247,3 +247,94 @@ def test_full_size_mask_probe():
     torch.cuda.synchronize()
     ref = oracle.prefill(q, k, v, w.W, w.C)
     assert_parity(to64(O), ref, w.dtype, "needles")
+
+
+# ---- the 8-wave, 64-key-block configuration of the bf16 kernel ----
+# The kernel takes it when a kv head serves several query heads (G > 1) and
+# the window exceeds 512 keys (the long-context workload's case); every shape
+# here does.  Compared element by element over every row.
+WIDE = [
+    # B, H, Hkv, L, d, W, C
+    (1, 8, 2, 1500, 128, 600, 32),
+    (1, 16, 4, 2100, 64, 777, 48),    # d = 64, ragged tail, W mod 16 = 9
+    (1, 8, 2, 800, 128, 799, 16),     # W = L - 1: only the last row drops token 0 (a gap token)
+    (2, 4, 2, 1100, 128, 1024, 64),   # W mod 16 = 0, G = 2
+    (1, 24, 8, 1400, 128, 520, 24),   # G = 3: one head per workgroup, 256 positions
+    (1, 8, 2, 1300, 128, 513, 1),     # C = 1: exact causal attention
+]
+
+
+@pytest.mark.parametrize("shape", WIDE)
+def test_prefill_bf16_wide_config(shape):
+    check_prefill(*shape, torch.bfloat16, seed=40)
+
+
+def _spike_check(B, H, Hkv, L, d, W, C, positions, chunks, seed, variant=oracle.SLIDING):
+    print(f"spikes B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C} variant {variant} positions {len(positions)} "
+          f"chunks {list(chunks)}", flush=True)
+    q, k, v = inputs.spike_at_qkv(B, H, Hkv, L, d, positions, chunks, C, torch.bfloat16, seed)
+    O = eva.prefill(*cuda(q, k, v), W, C, window=variant)
+    torch.cuda.synchronize()
+    ref = oracle.prefill_variant(q, k, v, W, C, variant)
+    assert_parity(to64(O), ref, torch.bfloat16, f"spikes variant {variant}")
+
+
+def _anchor_rows(L, W, C):
+    # rows whose window edges are probed: the first rows with a summary, rows
+    # at every 16-row offset class of a tile, and the last rows
+    rows = [W - 1, W, W + C - 1, W + C, 2 * C + W - 1, L - 1, L - 2]
+    rows += [W + 64 * t + off for t, off in ((1, 0), (2, 1), (3, 15), (4, 16), (5, 31), (6, 47), (7, 63))]
+    return [r for r in rows if W <= r < L]
+
+
+@pytest.mark.parametrize("shape", [WIDE[0], WIDE[1], WIDE[3], (1, 4, 4, 1500, 128, 300, 32)])
+def test_spiked_window_edges(shape):
+    # dominant keys on the first and last window positions, the token before
+    # the window (a gap token or a chunk's last token) and chunk last tokens:
+    # a one-token slip of the window's lower edge, the diagonal or s(n) moves
+    # a row by O(1) at any window length
+    B, H, Hkv, L, d, W, C = shape
+    pos = inputs.window_edge_positions(L, W, C, _anchor_rows(L, W, C))
+    _spike_check(B, H, Hkv, L, d, W, C, pos, (), seed=41)
+
+
+@pytest.mark.parametrize("shape", [WIDE[0], WIDE[1], WIDE[3], (1, 4, 4, 1500, 128, 300, 32)])
+def test_spiked_whole_chunk(shape):
+    # every key of a chunk spiked: its summary key dominates exactly the rows
+    # with s(n) > c, and the chunk's own keys the rows whose window holds them
+    B, H, Hkv, L, d, W, C = shape
+    n_chunks = L // C
+    chunks = sorted({1, n_chunks // 3}) if n_chunks > 1 else []
+    _spike_check(B, H, Hkv, L, d, W, C, (), chunks, seed=42)
+
+
+VARIANT_WIDE = [WIDE[0], WIDE[1]]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", VARIANT_WIDE)
+def test_prefill_variants_wide_config(variant, shape):
+    check_variant(*shape, torch.bfloat16, variant, seed=43)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", VARIANT_WIDE)
+def test_spiked_variants_wide_config(variant, shape):
+    # spikes on the variants' own edges (block starts kW, chunk starts kC and
+    # the tokens beside them) plus a regular comb, and one wholly spiked chunk
+    B, H, Hkv, L, d, W, C = shape
+    pos = set(range(7, L, 53))
+    for kk in range(1, L // W + 1):
+        pos.update((kk * W - 1, kk * W, kk * W + 1))
+    for kk in range(1, L // C + 1, 5):
+        pos.update((kk * C - 1, kk * C))
+    _spike_check(B, H, Hkv, L, d, W, C, sorted(pos), (), seed=44, variant=variant)
+    _spike_check(B, H, Hkv, L, d, W, C, (), (L // C // 2,), seed=45, variant=variant)
+
+
+# ---- 4-wave configuration without any summary block: waves whose first two
+# blocks are both outside their window start from untouched score registers
+@pytest.mark.parametrize("W,C", [(64, 2048), (33, 4096)])
+def test_prefill_bf16_no_summary_blocks(W, C):
+    check_prefill(1, 2, 2, 1024, 128, W, C, torch.bfloat16, seed=46)
+    check_prefill(1, 2, 2, 1024, 128, W, C, torch.bfloat16, seed=47, maker=inputs.needle_qkv)

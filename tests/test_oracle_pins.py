@@ -518,3 +518,46 @@ def test_backward_chunk_of_one_is_exact_attention_autograd():
     np.testing.assert_allclose(dq, tq.grad.numpy(), rtol=1e-10, atol=1e-11)
     np.testing.assert_allclose(dk, tk.grad.numpy(), rtol=1e-10, atol=1e-11)
     np.testing.assert_allclose(dv, tv.grad.numpy(), rtol=1e-10, atol=1e-11)
+
+
+# Term magnitudes of the backward (oracle.backward_terms): the scale of the
+# GPU gradients' rounding-error bound.  Not part of the method; pinned by
+# the properties such a magnitude must have.
+@pytest.mark.parametrize("L,W,C", [(40, 6, 4), (33, 50, 5), (30, 1, 3), (41, 8, 1)])
+def test_backward_terms_bound_the_gradients(L, W, C):
+    # a sum's absolute value never exceeds the sum of its terms' absolute values
+    B, H, Hkv, d = 1, 4, 2, 6
+    q, k, v = rand((B, H, L, d), 90), rand((B, Hkv, L, d), 91), rand((B, Hkv, L, d), 92)
+    R = rand((B, H, L, d), 93)
+    for g, t in zip(oracle.backward(q, k, v, R, W, C), oracle.backward_terms(q, k, v, R, W, C)):
+        assert np.all(t >= np.abs(g) * (1 - 1e-12))
+        assert t.max() > 0
+
+
+def test_backward_terms_exact_without_cancellation():
+    # dV: with an all-positive output gradient every term of every dV entry
+    # (p dO, and b_j dvhat through the summaries) is non-negative, so the
+    # magnitude is the gradient itself
+    B, H, Hkv, L, d, W, C = 1, 2, 1, 30, 5, 6, 4
+    q, k, v = rand((B, H, L, d), 94), rand((B, Hkv, L, d), 95), rand((B, Hkv, L, d), 96)
+    R = np.abs(rand((B, H, L, d), 97)) + 0.1
+    np.testing.assert_allclose(oracle.backward_terms(q, k, v, R, W, C)[2], oracle.backward(q, k, v, R, W, C)[2],
+                               rtol=1e-12, atol=0)
+    # dQ: with a two-token window and no chunk, row n's gradient is
+    # dl (k_{n-1} - k_n) / sqrt(d) (its two logit gradients cancel); keys of
+    # alternating sign make |k_{n-1} - k_n| = |k_{n-1}| + |k_n| entry by entry
+    L = 12
+    q, v = rand((B, H, L, d), 98), rand((B, Hkv, L, d), 99)
+    k = np.abs(rand((B, Hkv, L, d), 100)) + 0.1
+    k[:, :, 1::2] *= -1
+    R = rand((B, H, L, d), 101)
+    np.testing.assert_allclose(oracle.backward_terms(q, k, v, R, 2, L + 1)[0],
+                               np.abs(oracle.backward(q, k, v, R, 2, L + 1)[0]), rtol=1e-12, atol=1e-15)
+
+
+def test_backward_terms_scale_with_the_output_gradient():
+    B, H, Hkv, L, d, W, C = 1, 2, 2, 25, 4, 5, 3
+    q, k, v = rand((B, H, L, d), 102), rand((B, Hkv, L, d), 103), rand((B, Hkv, L, d), 104)
+    R = rand((B, H, L, d), 105)
+    for t1, t2 in zip(oracle.backward_terms(q, k, v, R, W, C), oracle.backward_terms(q, k, v, -2.5 * R, W, C)):
+        np.testing.assert_allclose(t2, 2.5 * t1, rtol=1e-12, atol=0)
