@@ -314,6 +314,25 @@ int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const 
 size_t eva_decode_workspace_bytes(const eva_cache* cache);
 
 /*
+ * eva_append_decode for callers that cannot allocate (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): no workspace
+ * argument.  When the rows are split over workgroups, the partial results go
+ * to a fixed array of 6.25 MiB (6553600 bytes) of device memory inside the
+ * library, one copy per GPU, held until the process ends; its device
+ * address is looked up on the first call on each GPU (the device of
+ * `stream`).  The call allocates nothing.  Every slot a call reads is
+ * written earlier in the same call, so no state carries over; but calls
+ * that overlap on one GPU (concurrent streams, or threads) share the array
+ * and race: serialize them.  Results are those of eva_append_decode with a
+ * workspace of eva_decode_workspace_bytes(cache) bytes.
+ * Errors: as eva_append_decode; CAPACITY if the partials exceed the fixed
+ * array (they never do for the shapes this library accepts: at most
+ * 766 * 16 * (d + 2) floats); HIP if the array's address cannot be found.
+ */
+int eva_append_decode_noalloc(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                              void* stream);
+
+/*
  * Ragged decode cache: batched generation where every sequence of the batch
  * holds its own number of tokens (section "Inference throughput and Memory
  * usage": many sequences generated in parallel after a prompt; prompts of

@@ -37,6 +37,7 @@ SYMBOLS = (
     "eva_decode_step",
     "eva_decode_workspace_bytes",
     "eva_append_decode",
+    "eva_append_decode_noalloc",
     "eva_rcache_fill",
     "eva_rcache_append",
     "eva_rdecode_step",
@@ -109,6 +110,8 @@ def load():
     lib.eva_decode_step.argtypes = [cp, vp, vp, vp, sz, vp]
     lib.eva_append_decode.restype = i
     lib.eva_append_decode.argtypes = [cp, vp, vp, vp, vp, vp, sz, vp]
+    lib.eva_append_decode_noalloc.restype = i
+    lib.eva_append_decode_noalloc.argtypes = [cp, vp, vp, vp, vp, vp]
     lib.eva_decode_workspace_bytes.restype = sz
     lib.eva_decode_workspace_bytes.argtypes = [cp]
     rp = ctypes.POINTER(EvaRCacheStruct)

@@ -16,6 +16,8 @@
 // 16 B per lane, and never staged through LDS.  Query heads sharing a kv head
 // (up to 16) are the MFMA columns, so the keys and values are read once for
 // all of them.
+#include <mutex>
+
 #include "eva_kernels.hpp"
 #include "summary.hpp"
 
@@ -567,6 +569,48 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
 }
 
 }  // namespace
+
+// ---- scratch of the allocation-free fused decode step ----
+// The split partials [m, l, o[D]] of every (b, kv head, head group, split,
+// column) of one call, in a fixed array of device memory instead of a
+// caller's workspace: each GPU the library runs on holds its own copy until
+// the process ends.  Every slot the combine kernel reads is written by the
+// same call's decode kernel first, so nothing needs clearing between calls;
+// calls that overlap on one GPU share the array and race.
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+hipError_t decode_scratch(hipStream_t stream, float** out) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float* addr[kMaxDevices] = {};
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    int dev = cur;
+    if (stream) {
+        hipDevice_t sd;
+        e = hipStreamGetDevice(stream, &sd);
+        if (e != hipSuccess) return e;
+        dev = (int)sd;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        // the array's host-side name is no device address: look the address
+        // up once per device, with that device current
+        if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (dev != cur) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<float*>(ptr);
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
 
 template <int D, typename T>
 hipError_t launch_cache_fill(const CacheView& c, const void* K, const void* V, const void* Ks, const void* Vs,

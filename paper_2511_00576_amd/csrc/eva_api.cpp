@@ -429,8 +429,10 @@ size_t eva_decode_workspace_bytes(const eva_cache* cache) {
 }
 
 // Decode (or fused append + decode) of position pos of a uniform cache.
+// With `fixed` the split partials go to the library's fixed device array
+// instead of ws (which is then unused).
 static int uniform_decode(const eva_cache* cache, long long pos, const void* q, void* o, const void* k_new,
-                          const void* v_new, void* ws, size_t ws_bytes, void* stream) {
+                          const void* v_new, void* ws, size_t ws_bytes, void* stream, bool fixed = false) {
     if (pos > 0x7fffffffLL - 64) return EVA_ERR_CAPACITY;
     if (cache->B > (k_new ? 32767 : 65535)) return EVA_ERR_UNSUPPORTED;  // grid z: B (x2 when appending)
     eva::DecodeParams p{};
@@ -447,8 +449,16 @@ static int uniform_decode(const eva_cache* cache, long long pos, const void* q, 
     p.splits = decode_splits(units, n_chunks);
     const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
-    p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
+    if (fixed) {
+        p.ws = nullptr;
+        if (p.splits > 1) {
+            if (need > eva::kDecodeScratchBytes) return EVA_ERR_CAPACITY;
+            if (eva::decode_scratch(s, &p.ws) != hipSuccess) return EVA_ERR_HIP;
+        }
+    } else {
+        if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
+        p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
+    }
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)cache->d));
     p.log2C = (float)log2((double)cache->C);
     p.k_new = k_new;
@@ -466,18 +476,28 @@ int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, si
     return uniform_decode(cache, cache->n_tok - 1, q, o, nullptr, nullptr, ws, ws_bytes, stream);
 }
 
-int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o, void* ws,
-                      size_t ws_bytes, void* stream) {
+static int append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o, void* ws,
+                         size_t ws_bytes, void* stream, bool fixed) {
     int st = check_cache(cache);
     if (st != EVA_OK) return st;
     if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (!q || !o || !k_new || !v_new || !aligned16(q) || !aligned16(k_new)) return EVA_ERR_INVALID;
     const long long p = cache->n_tok;
     if (completed_chunk(p, cache->C) >= cache->S_max) return EVA_ERR_CAPACITY;
-    st = uniform_decode(cache, p, q, o, k_new, v_new, ws, ws_bytes, stream);
+    st = uniform_decode(cache, p, q, o, k_new, v_new, ws, ws_bytes, stream, fixed);
     if (st != EVA_OK) return st;
     cache->n_tok = p + 1;
     return EVA_OK;
+}
+
+int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o, void* ws,
+                      size_t ws_bytes, void* stream) {
+    return append_decode(cache, q, k_new, v_new, o, ws, ws_bytes, stream, false);
+}
+
+int eva_append_decode_noalloc(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o,
+                              void* stream) {
+    return append_decode(cache, q, k_new, v_new, o, nullptr, 0, stream, true);
 }
 
 // ---------------------------------------------------------------------------

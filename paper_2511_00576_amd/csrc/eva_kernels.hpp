@@ -171,4 +171,12 @@ struct DecodeParams {
 template <int D, typename T>
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
 
+// Fixed device array for the split partials of the allocation-free fused
+// decode step: 6.25 MiB, enough for any cache (splits happen only for fewer
+// than 256 (b, kv head, head group) units, and then units * splits < 256 +
+// 512, each taking 16 * (d + 2) floats).  decode_scratch returns its address
+// on the device of `stream` (looked up once per device).
+constexpr size_t kDecodeScratchBytes = (size_t)6400 * 1024;
+hipError_t decode_scratch(hipStream_t stream, float** out);
+
 }  // namespace eva

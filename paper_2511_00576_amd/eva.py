@@ -217,6 +217,24 @@ def append_decode(cache: Cache, q, k_new, v_new, use_workspace: bool = True, out
     return o
 
 
+def append_decode_noalloc(cache: Cache, q, k_new, v_new, out=None):
+    """append_decode without a workspace: split partials go to the library's
+    fixed device array (eva_append_decode_noalloc).  With `out` given the
+    call allocates nothing."""
+    _require_device(q, k_new, v_new)
+    s = cache.struct
+    if tuple(q.shape) != (s.B, s.H, s.d) or q.dtype != cache.dtype:
+        raise ValueError("q must be [B, H, d] in the cache dtype")
+    if tuple(k_new.shape) != (s.B, s.H_kv, s.d) or v_new.shape != k_new.shape or k_new.dtype != cache.dtype:
+        raise ValueError("k_new, v_new must be [B, Hkv, d] in the cache dtype")
+    o = torch.empty_like(q) if out is None else out
+    _require_device(o)
+    _lib.check("eva_append_decode_noalloc",
+               _lib.load().eva_append_decode_noalloc(ctypes.byref(s), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o),
+                                                     _stream()))
+    return o
+
+
 def decode_step(cache: Cache, q, use_workspace: bool = True, out=None):
     """Attention output of the last appended position: q [B, H, d] -> o [B, H, d]."""
     _require_device(q)
