@@ -104,14 +104,16 @@ typedef enum {
  *
  * The struct is caller-owned host memory; the four arrays are caller-owned
  * device memory of the cache's dtype.  Position p of (b, g) lives in ring slot
- * p mod R.  Values are stored transposed (feature-major) in tiles of 32 slots
- * so the decode kernel can feed them to the matrix cores straight from HBM,
- * each tile's keys and values being two contiguous blocks:
+ * p mod R.  Values are stored transposed (feature-major) in tiles of 8 slots
+ * so the decode kernel can feed them to the matrix cores straight from HBM
+ * (each feature's 8 slots are one 16-byte operand fragment), 32 aligned slots'
+ * keys and values being two contiguous blocks; appending one token's values
+ * touches d / 8 cache lines of 128 bytes:
  *   k_ring   [B][H_kv][R][d]           keys, row per slot
- *   vt_ring  [B][H_kv][R/32][d][32]    values: slot s, feature f at
- *                                      [s/32][f][s%32]
+ *   vt_ring  [B][H_kv][R/8][d][8]      values: slot s, feature f at
+ *                                      [s/8][f][s%8]
  *   k_sum    [B][H_kv][S_max][d]       summary keys
- *   vt_sum   [B][H_kv][S_max/32][d][32] summary values, tiled the same way
+ *   vt_sum   [B][H_kv][S_max/8][d][8]  summary values, tiled the same way
  * Requirements: R >= W + C - 1 and R a multiple of 32; S_max a multiple of 32.
  * n_tok counts the tokens the cache has absorbed (the same for every
  * sequence of the batch); the library updates it.  `window` is the causal

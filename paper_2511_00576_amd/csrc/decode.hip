@@ -2,10 +2,10 @@
 // chunk summary that becomes due), and the bandwidth-bound decode step.
 //
 // Cache layout (per (b, kv head)): keys row-major by ring slot [R][D], values
-// transposed per 32-slot tile [R/32][D][32]; summary keys [S_max][D], summary
-// values [S_max/32][D][32].  Position p lives in slot p mod R; R is a
-// multiple of 32 so a 32-aligned run of positions is one tile of slots, and
-// its keys and values are two contiguous 32*D blocks.
+// transposed per 8-slot tile [R/8][D][8]; summary keys [S_max][D], summary
+// values [S_max/8][D][8].  Position p lives in slot p mod R; R is a multiple
+// of 32 so a 32-aligned run of positions is 32 consecutive slots, and its
+// keys and values are two contiguous 32*D blocks.
 //
 // Decode works on 32-row chunks: summary chunks (rows of the summary arrays)
 // and window chunks (32-aligned position runs of the ring).  Per chunk a wave
@@ -28,10 +28,10 @@ namespace {
 // ---------------------------------------------------------------------------
 // cache fill
 // ---------------------------------------------------------------------------
-// One workgroup moves one 32-row tile: 32 ring positions (32-aligned, so
-// they occupy 32 consecutive slots) or 32 summaries.  Keys are copied row by
-// row; values go through LDS so the transposed store writes the tile's
-// contiguous [D][32] block instead of scattered elements.
+// One workgroup moves 32 rows: 32 ring positions (32-aligned, so they occupy
+// 32 consecutive slots) or 32 summaries.  Keys are copied row by row; values
+// go through LDS so the transposed store writes the rows' four contiguous
+// [D][8] tiles instead of scattered elements.
 // Source arrays have L rows (K, V) and n_chunks rows (Ks, Vs) per (b, g).
 // With `lens` each sequence copies only its own valid prefix: the tiles are
 // counted from that sequence's first ring position, and tiles past its
@@ -77,8 +77,9 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
     }
     const int rows = max(r1 - r0, 0);
     if (rows == 32 && dst0 % 32 == 0) {
-        // whole 32-row tile of the destination: 16-B row copies of K, and the
-        // tile's [D][32] block of transposed V written 8 rows (16 B) at a time
+        // 32 whole rows of the destination: 16-B row copies of K, and their four
+        // [D][8] blocks of transposed V written 16 B (one feature's slots, bf16)
+        // at a time, consecutive threads on consecutive features
         constexpr int CH = D * (int)sizeof(T) / 16;  // 16-B chunks per row
         constexpr int EPC = 16 / (int)sizeof(T);     // elements per chunk
         for (int e = threadIdx.x; e < 32 * CH; e += blockDim.x) {
@@ -92,14 +93,14 @@ __global__ __launch_bounds__(256) void cache_fill_kernel(CacheView c, const T* _
             for (int i = 0; i < EPC; ++i) tile[r][ch * EPC + i] = ve[i];
         }
         __syncthreads();
-        T* blk = dst_vt + (size_t)(dst0 / 32) * 32 * D;  // [D][32]
+        T* blk = dst_vt + vt_index<D>(0, dst0);
         for (int e = threadIdx.x; e < D * 32 / EPC; e += blockDim.x) {
-            const int d = e / (32 / EPC), r8 = (e % (32 / EPC)) * EPC;
+            const int d = e % D, r8 = (e / D) * EPC;
             u32x4 w;
             T* we = reinterpret_cast<T*>(&w);
 #pragma unroll
             for (int i = 0; i < EPC; ++i) we[i] = tile[r8 + i][d];
-            *reinterpret_cast<u32x4*>(blk + (size_t)d * 32 + r8) = w;
+            *reinterpret_cast<u32x4*>(blk + vt_index<D>(d, r8)) = w;
         }
         return;
     }
@@ -333,15 +334,16 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
     // Per-lane element offsets inside a 32-row tile.  A operand of S^T = K Q^T
     // for key block kb: row c16 of the block is key krow0 + 4kb, so the keys
     // of lane group g' = c16/4 land on 8 consecutive keys 8g'..8g'+7.
-    // A operand of O^T += V^T P^T: feature db*16 + c16, keys 8g .. 8g+7.
+    // A operand of O^T += V^T P^T: feature db*16 + c16, keys 8g .. 8g+7 (the
+    // 16 bytes of that feature in the chunk's value tile g).
     const int krow0 = (c16 >> 2) * 8 + (c16 & 3);
     const int koff = krow0 * D + g * 8;
-    const int voff = c16 * 32 + g * 8;
+    const int voff = (int)vt_index<D>(c16, 8 * g);
 
     for (int ch = worker; ch < n_chunks; ch += n_workers) {
         const bool is_sum = ch < geo.n_sum_chunks;
         const T* kt;  // the chunk's key tile [32][D]
-        const T* vt;  // the chunk's value tile [D][32]
+        const T* vt;  // the chunk's values: four [D][8] tiles
         int key_lo, key_hi;  // valid chunk keys: [key_lo, key_hi]
         int chunk_pos0 = 0;  // first position of a window chunk
         if (is_sum) {
@@ -391,7 +393,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeParams a) {
             const bool use = g * 8 <= key_hi && g * 8 + 7 >= key_lo;
             const int base = use ? voff * (int)sizeof(T) : kSkip;
 #pragma unroll
-            for (int db = 0; db < NDB; ++db) va[db] = ldb(vrs, base + db * 16 * 32 * (int)sizeof(T));
+            for (int db = 0; db < NDB; ++db) va[db] = ldb(vrs, base + db * 16 * kVtTile * (int)sizeof(T));
         }
         __builtin_amdgcn_sched_barrier(0);
         if (APPEND && geo.fresh && !is_sum && chunk_pos0 + 32 > geo.p) {

@@ -91,13 +91,17 @@ __device__ __forceinline__ shortx4 lds_read_tr16(const bf16* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(p));
 }
 
-// Transposed value arrays of the decode cache are tiled by 32 rows: row
-// (slot or summary index) r, feature f lives at element
-//   (r / 32) * 32 * D + f * 32 + r % 32,
-// so the 32 rows of a tile form one contiguous [D][32] block.
+// Transposed value arrays of the decode cache are tiled by 8 rows: row (slot
+// or summary index) r, feature f lives at element
+//   (r / 8) * 8 * D + f * 8 + r % 8,
+// so a tile is one contiguous [D][8] block, each feature's 8 slots one
+// 16-byte piece (one matrix-core operand fragment), and 32 consecutive rows
+// (the decode's unit) 4 consecutive tiles.  Short tiles keep the write of a
+// single appended row to D / 8 cache lines (D / 2 with 32-row tiles).
+constexpr int kVtTile = 8;
 template <int D>
 __host__ __device__ __forceinline__ size_t vt_index(int f, int r) {
-    return (size_t)(r >> 5) * (32 * D) + (size_t)f * 32 + (r & 31);
+    return (size_t)(r >> 3) * (kVtTile * D) + (size_t)f * kVtTile + (r & 7);
 }
 
 __device__ __forceinline__ int visible_summaries(int n, int W, int C) {

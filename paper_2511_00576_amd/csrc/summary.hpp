@@ -49,12 +49,12 @@ struct RowMajorChunk {
 };
 
 // Cache ring source: row r of the chunk is position pos0 + r, stored in slot
-// (pos0 + r) mod R; keys row-major [R][D], values transposed per 32-slot tile
-// [R/32][D][32] (vt_index).
+// (pos0 + r) mod R; keys row-major [R][D], values transposed per 8-slot tile
+// [R/8][D][8] (vt_index).
 template <int D, typename T>
 struct RingChunk {
     const T* k_ring;   // this (b, g): [R][D]
-    const T* vt_ring;  // this (b, g): [R/32][D][32]
+    const T* vt_ring;  // this (b, g): [R/8][D][8]
     long long pos0;
     int R;
     __device__ int slot(int r) const { return (int)((pos0 + r) % R); }

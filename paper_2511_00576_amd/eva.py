@@ -77,8 +77,8 @@ def build_summaries_rf(K: torch.Tensor, V: torch.Tensor, eps: torch.Tensor, C: i
 class Cache:
     """Window + summary decode cache in device memory (see eva_cache in eva.h).
 
-    k_ring [B, Hkv, R, d], vt_ring [B, Hkv, R // 32, d, 32] (values transposed
-    per 32-slot tile), k_sum [B, Hkv, S_max, d], vt_sum [B, Hkv, S_max // 32, d, 32].
+    k_ring [B, Hkv, R, d], vt_ring [B, Hkv, R // 8, d, 8] (values transposed
+    per 8-slot tile), k_sum [B, Hkv, S_max, d], vt_sum [B, Hkv, S_max // 8, d, 8].
     The ring holds the
     last R positions (R >= W + C - 1, a multiple of 32); S_max bounds the number
     of chunk summaries, i.e. the tokens the cache can ever absorb.
@@ -92,9 +92,9 @@ class Cache:
         mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
             (lambda *s: torch.empty(*s, dtype=dtype, device=device))
         self.k_ring = mk(B, Hkv, R, d)
-        self.vt_ring = mk(B, Hkv, R // 32, d, 32)
+        self.vt_ring = mk(B, Hkv, R // 8, d, 8)
         self.k_sum = mk(B, Hkv, S_max, d)
-        self.vt_sum = mk(B, Hkv, S_max // 32, d, 32)
+        self.vt_sum = mk(B, Hkv, S_max // 8, d, 8)
         self.dtype = dtype
         self.struct = _lib.EvaCacheStruct(B=B, H=H, H_kv=Hkv, d=d, W=W, C=C, dtype=_DTYPES[dtype], window=window,
                                           R=R, S_max=S_max, n_tok=0, k_ring=self.k_ring.data_ptr(),
@@ -263,9 +263,9 @@ class RaggedCache:
         mk = (lambda *s: torch.full(s, fill, dtype=dtype, device=device)) if fill is not None else \
             (lambda *s: torch.empty(*s, dtype=dtype, device=device))
         self.k_ring = mk(B, Hkv, R, d)
-        self.vt_ring = mk(B, Hkv, R // 32, d, 32)
+        self.vt_ring = mk(B, Hkv, R // 8, d, 8)
         self.k_sum = mk(B, Hkv, S_max, d)
-        self.vt_sum = mk(B, Hkv, S_max // 32, d, 32)
+        self.vt_sum = mk(B, Hkv, S_max // 8, d, 8)
         self.n_tok = torch.zeros(B, dtype=torch.int32, device=device)
         self.arrive = torch.zeros(B, dtype=torch.int32, device=device)
         self.dtype = dtype
