@@ -293,8 +293,10 @@ int eva_cache_append(eva_cache* cache, const void* k_new, const void* v_new, voi
  * eva_decode_workspace_bytes(cache) bytes the rows of each sequence are split
  * over more workgroups (for small B * H_kv); with less (or NULL) the call
  * still works, one workgroup per (b, kv head, 16 query heads).
- * Errors: INVALID (n_tok == 0, null pointers, malformed cache), UNSUPPORTED
- * (a cache of dtype EVA_F32: decode runs on bf16 caches only).
+ * Both cache dtypes decode: bf16 caches with bf16 matrix-core products and
+ * fp32 accumulation, fp32 caches with fp32 products (their own kernel, no
+ * row splits: `ws` is not used).
+ * Errors: INVALID (n_tok == 0, null pointers, malformed cache).
  */
 int eva_decode_step(const eva_cache* cache, const void* q, void* o,
                     void* ws, size_t ws_bytes, void* stream);
@@ -305,8 +307,8 @@ int eva_decode_step(const eva_cache* cache, const void* q, void* o,
  * eva_decode_step(q) in one launch, with the same results (the decoded row
  * reads the new token from k_new, v_new while another workgroup writes it to
  * the ring; the summary the token completes is built beside the decode).
- * Errors: as eva_cache_append and eva_decode_step (UNSUPPORTED for an
- * EVA_F32 cache).
+ * (On an EVA_F32 cache the append and the decode are two launches.)
+ * Errors: as eva_cache_append and eva_decode_step.
  */
 int eva_append_decode(eva_cache* cache, const void* q, const void* k_new, const void* v_new, void* o,
                       void* ws, size_t ws_bytes, void* stream);
@@ -355,7 +357,7 @@ int eva_append_decode_noalloc(eva_cache* cache, const void* q, const void* k_new
  */
 typedef struct eva_rcache {
     int B, H, H_kv, d, W, C;
-    int dtype;        /* eva_dtype; decode needs EVA_BF16 */
+    int dtype;        /* eva_dtype */
     int window;       /* eva_window, causal */
     int R;
     int S_max;
@@ -404,8 +406,8 @@ int eva_rcache_append(const eva_rcache* cache, const void* k_new, const void* v_
  * not written.  `ws` as in eva_decode_step, sized by
  * eva_rdecode_workspace_bytes (splits are chosen for the longest sequence a
  * cache of max_tok tokens may hold).
- * Errors: INVALID (malformed cache, null pointers), UNSUPPORTED (dtype other
- * than EVA_BF16).
+ * fp32 caches decode with their own kernel (no row splits).
+ * Errors: INVALID (malformed cache, null pointers).
  */
 int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int* active, void* ws,
                      size_t ws_bytes, void* stream);

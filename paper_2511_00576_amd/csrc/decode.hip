@@ -570,6 +570,170 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams a) {
     }
 }
 
+// fp32 caches: the same decode with fp32 matrix-core products
+// (v_mfma_f32_16x16x4_f32), one workgroup per (sequence, kv head, head group
+// of 16) and four waves striding over the row's 32-row chunks.  Per lane
+// (g, c16), column c16 is query head h0 + c16.  S^T = K Q^T: contraction step
+// (j, e) pairs feature 16j + 4g + e of key row c16 (+16 kb) with the same
+// feature of the query, so each lane's key operands for four steps are one
+// 16-byte load; the result holds keys 16 kb + 4g + i.  O^T += V^T P^T:
+// contraction step (kb, i) is key 16 kb + 4g + i, whose weight the lane
+// already holds, and whose value of feature 16 db + c16 sits in an 8-slot
+// value tile next to the lane's other three keys: again one 16-byte load.
+// Slots outside the row's valid range are zeroed before the products (a stale
+// ring slot may hold any bit pattern, and 0 * NaN is NaN).
+template <int D, bool RAGGED>
+__global__ __launch_bounds__(256) void decode_f32_kernel(DecodeParams a) {
+    constexpr int NJ = D / 16;  // 16-feature blocks (contraction and output)
+    __shared__ float red_m[kDecWaves][16];
+    __shared__ float red_l[kDecWaves][16];
+    __shared__ float red_o[kDecWaves][D][17];
+
+    const int kvh = blockIdx.y / a.n_hg;
+    const int hg = blockIdx.y % a.n_hg;
+    const int b = blockIdx.z;
+    const CacheView& c = a.c;
+    bool valid;
+    const DecodeGeom geo = decode_geom<RAGGED, false>(a, b, valid);
+    if (!valid) return;  // uniform across the workgroup
+    const size_t bg = (size_t)b * c.Hkv + kvh;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const int h0 = kvh * a.G + hg * 16;
+    const int ncols = min(16, a.G - hg * 16);
+
+    const float* kring = static_cast<const float*>(c.k_ring) + bg * (size_t)c.R * D;
+    const float* vring = static_cast<const float*>(c.vt_ring) + bg * (size_t)c.R * D;
+    const float* ksum = static_cast<const float*>(c.k_sum) + bg * (size_t)c.S_max * D;
+    const float* vsum = static_cast<const float*>(c.vt_sum) + bg * (size_t)c.S_max * D;
+
+    // query fragments (columns past ncols repeat the last head; their
+    // outputs are not stored)
+    floatx4 qf[NJ];
+    {
+        const float* qrow = static_cast<const float*>(a.q) + ((size_t)b * c.H + h0 + min(c16, ncols - 1)) * D;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) qf[j] = *reinterpret_cast<const floatx4*>(qrow + 16 * j + 4 * g);
+    }
+    floatx4 acc[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const int n_chunks = geo.n_sum_chunks + geo.n_win_chunks;
+    for (int ch = wave; ch < n_chunks; ch += kDecWaves) {
+        const bool is_sum = ch < geo.n_sum_chunks;
+        const float *kt, *vt;  // the chunk's 32 key rows and four [D][8] value tiles
+        int key_lo, key_hi;    // valid chunk keys: [key_lo, key_hi]
+        if (is_sum) {
+            const int r0 = ch * 32;
+            kt = ksum + (size_t)r0 * D;
+            vt = vsum + (size_t)r0 * D;
+            key_lo = 0;
+            key_hi = min(31, geo.n_sum - 1 - r0);
+        } else {
+            const int pos0 = (geo.first_win_chunk + ch - geo.n_sum_chunks) * 32;
+            const int slot0 = pos0 % c.R;
+            kt = kring + (size_t)slot0 * D;
+            vt = vring + (size_t)slot0 * D;
+            key_lo = max(0, geo.win_lo - pos0);
+            key_hi = min(31, geo.p - pos0);
+        }
+        const unsigned span = (unsigned)(key_hi - key_lo);
+        floatx4 s[2];
+        float pw[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            const float* krow = kt + (size_t)(16 * kb + c16) * D + 4 * g;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const floatx4 kf = *reinterpret_cast<const floatx4*>(krow + 16 * j);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) s[kb] = mfma_f32(kf[e], qf[j][e], s[kb]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const unsigned rel = (unsigned)(16 * kb + 4 * g + i - key_lo);
+                s[kb][i] = rel <= span ? s[kb][i] : -INFINITY;
+            }
+        }
+        // online softmax in log2 units (the chunk always has a valid key)
+        const float bias = is_sum ? a.log2C : 0.f;
+        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        mx = xgroup_max(mx) * a.scale_log2 + bias;
+        if (mx > m_run) {
+            const float alpha = fast_exp2(m_run - mx);  // first chunk: exp2(-inf) = 0
+            l_run *= alpha;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[j] *= alpha;
+            m_run = mx;
+        }
+        const float off = bias - m_run;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pw[kb][i] = fast_exp2(fmaf(s[kb][i], a.scale_log2, off));
+                l_run += pw[kb][i];
+            }
+        // O^T += V^T P^T
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const float* vtile = vt + (size_t)(2 * kb + (g >> 1)) * (kVtTile * D) + 4 * (g & 1);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                floatx4 vf = *reinterpret_cast<const floatx4*>(vtile + (16 * j + c16) * kVtTile);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const unsigned rel = (unsigned)(16 * kb + 4 * g + i - key_lo);
+                    vf[i] = rel <= span ? vf[i] : 0.f;
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[j] = mfma_f32(vf[i], pw[kb][i], acc[j]);
+            }
+        }
+    }
+
+    // ---- combine the four waves (as in decode_kernel) ----
+    const float l_wave = xgroup_sum(l_run);
+    if (g == 0) {
+        red_m[wave][c16] = m_run;
+        red_l[wave][c16] = l_wave;
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red_o[wave][j * 16 + g * 4 + i][c16] = acc[j][i];
+    __syncthreads();
+    const int col = tid & 15;
+    const int run = tid >> 4;
+    if (col >= ncols) return;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, red_m[w][col]);
+    float wgt[kDecWaves];
+    float lsum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+        wgt[w] = red_m[w][col] == -INFINITY ? 0.f : fast_exp2(red_m[w][col] - M);
+        lsum += wgt[w] * red_l[w][col];
+    }
+    constexpr int FPT = D / 16;
+    const float inv = 1.f / lsum;
+    float* orow = static_cast<float*>(a.o) + ((size_t)b * c.H + h0 + col) * D + run * FPT;
+#pragma unroll
+    for (int f = 0; f < FPT; ++f) {
+        const int d = run * FPT + f;
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < kDecWaves; ++w) v += wgt[w] * red_o[w][d][col];
+        orow[f] = v * inv;
+    }
+}
+
 }  // namespace
 
 // ---- scratch of the allocation-free fused decode step ----
@@ -667,10 +831,21 @@ hipError_t launch_decode_impl(const DecodeParams& p, hipStream_t stream) {
 
 template <int D, typename T>
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
-    static_assert(sizeof(T) == 2, "decode runs on bf16 caches");
-    if (p.k_new)
-        return p.n_tok ? launch_decode_impl<D, true, true>(p, stream) : launch_decode_impl<D, false, true>(p, stream);
-    return p.n_tok ? launch_decode_impl<D, true, false>(p, stream) : launch_decode_impl<D, false, false>(p, stream);
+    if constexpr (sizeof(T) == 4) {
+        // fp32 caches: plain decode only (the fused calls append first), no splits
+        if (p.k_new || p.splits != 1) return hipErrorInvalidValue;
+        dim3 grid(1, p.c.Hkv * p.n_hg, p.c.B);
+        if (p.n_tok)
+            hipLaunchKernelGGL((decode_f32_kernel<D, true>), grid, dim3(256), 0, stream, p);
+        else
+            hipLaunchKernelGGL((decode_f32_kernel<D, false>), grid, dim3(256), 0, stream, p);
+        return hipGetLastError();
+    } else {
+        if (p.k_new)
+            return p.n_tok ? launch_decode_impl<D, true, true>(p, stream)
+                           : launch_decode_impl<D, false, true>(p, stream);
+        return p.n_tok ? launch_decode_impl<D, true, false>(p, stream) : launch_decode_impl<D, false, false>(p, stream);
+    }
 }
 
 #define EVA_FILL(D, T)                                                                                      \
@@ -695,5 +870,7 @@ template hipError_t launch_cache_append<64, float>(const CacheView&, const void*
 template hipError_t launch_cache_append<128, float>(const CacheView&, const void*, const void*, int, hipStream_t);
 template hipError_t launch_decode<64, bf16>(const DecodeParams&, hipStream_t);
 template hipError_t launch_decode<128, bf16>(const DecodeParams&, hipStream_t);
+template hipError_t launch_decode<64, float>(const DecodeParams&, hipStream_t);
+template hipError_t launch_decode<128, float>(const DecodeParams&, hipStream_t);
 
 }  // namespace eva

@@ -446,7 +446,8 @@ static int uniform_decode(const eva_cache* cache, long long pos, const void* q, 
     p.G = cache->H / cache->H_kv;
     p.n_hg = (p.G + 15) / 16;
     const int units = cache->B * cache->H_kv * p.n_hg;
-    p.splits = decode_splits(units, n_chunks);
+    // fp32 caches: one workgroup per (b, kv head, head group), no split partials
+    p.splits = cache->dtype == EVA_F32 ? 1 : decode_splits(units, n_chunks);
     const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (fixed) {
@@ -463,14 +464,26 @@ static int uniform_decode(const eva_cache* cache, long long pos, const void* q, 
     p.log2C = (float)log2((double)cache->C);
     p.k_new = k_new;
     p.v_new = v_new;
-    hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    hipError_t e;
+    if (cache->dtype == EVA_F32) {
+        // fused step on an fp32 cache: the append, then a plain decode of the
+        // appended position (same results as the one-launch bf16 form)
+        if (k_new) {
+            e = cache->d == 64 ? eva::launch_cache_append<64, float>(p.c, k_new, v_new, p.p, s)
+                               : eva::launch_cache_append<128, float>(p.c, k_new, v_new, p.p, s);
+            if (e != hipSuccess) return EVA_ERR_HIP;
+            p.k_new = p.v_new = nullptr;
+        }
+        e = cache->d == 64 ? eva::launch_decode<64, float>(p, s) : eva::launch_decode<128, float>(p, s);
+    } else {
+        e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    }
     return hip_status(e);
 }
 
 int eva_decode_step(const eva_cache* cache, const void* q, void* o, void* ws, size_t ws_bytes, void* stream) {
     int st = check_cache(cache);
     if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
     if (cache->n_tok < 1) return EVA_ERR_INVALID;
     return uniform_decode(cache, cache->n_tok - 1, q, o, nullptr, nullptr, ws, ws_bytes, stream);
@@ -480,7 +493,6 @@ static int append_decode(eva_cache* cache, const void* q, const void* k_new, con
                          size_t ws_bytes, void* stream, bool fixed) {
     int st = check_cache(cache);
     if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (!q || !o || !k_new || !v_new || !aligned16(q) || !aligned16(k_new)) return EVA_ERR_INVALID;
     const long long p = cache->n_tok;
     if (completed_chunk(p, cache->C) >= cache->S_max) return EVA_ERR_CAPACITY;
@@ -647,7 +659,7 @@ static int ragged_decode(const eva_rcache* cache, const void* q, const void* k_n
     p.G = cache->H / cache->H_kv;
     p.n_hg = (p.G + 15) / 16;
     const int units = cache->B * cache->H_kv * p.n_hg;
-    p.splits = decode_splits(units, rdecode_max_chunks(cache));
+    p.splits = cache->dtype == EVA_F32 ? 1 : decode_splits(units, rdecode_max_chunks(cache));
     const size_t need = (size_t)units * p.splits * 16 * (cache->d + 2) * sizeof(float);
     if (p.splits > 1 && (!ws || ws_bytes < need || !aligned16(ws))) p.splits = 1;
     p.ws = p.splits > 1 ? static_cast<float*>(ws) : nullptr;
@@ -661,7 +673,21 @@ static int ragged_decode(const eva_rcache* cache, const void* q, const void* k_n
     p.arrive = cache->arrive;
     p.arrivals = p.splits * cache->H_kv * p.n_hg + cache->H_kv;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    hipError_t e;
+    if (cache->dtype == EVA_F32) {
+        // fused step on an fp32 cache: the ragged append (which advances
+        // n_tok), then a plain decode of each sequence's last position
+        if (k_new) {
+            const eva::RaggedState r = rstate_of(cache, active);
+            e = cache->d == 64 ? eva::launch_rcache_append<64, float>(p.c, r, k_new, v_new, s)
+                               : eva::launch_rcache_append<128, float>(p.c, r, k_new, v_new, s);
+            if (e != hipSuccess) return EVA_ERR_HIP;
+            p.k_new = p.v_new = nullptr;
+        }
+        e = cache->d == 64 ? eva::launch_decode<64, float>(p, s) : eva::launch_decode<128, float>(p, s);
+    } else {
+        e = cache->d == 64 ? eva::launch_decode<64, bf16>(p, s) : eva::launch_decode<128, bf16>(p, s);
+    }
     return hip_status(e);
 }
 
@@ -669,7 +695,6 @@ int eva_rdecode_step(const eva_rcache* cache, const void* q, void* o, const int*
                      size_t ws_bytes, void* stream) {
     int st = check_rcache(cache);
     if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (!q || !o || !aligned16(q)) return EVA_ERR_INVALID;
     return ragged_decode(cache, q, nullptr, nullptr, o, active, ws, ws_bytes, stream);
 }
@@ -678,7 +703,6 @@ int eva_rappend_decode(const eva_rcache* cache, const void* q, const void* k_new
                        const int* active, void* ws, size_t ws_bytes, void* stream) {
     int st = check_rcache(cache);
     if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (!q || !o || !k_new || !v_new || !aligned16(q) || !aligned16(k_new)) return EVA_ERR_INVALID;
     return ragged_decode(cache, q, k_new, v_new, o, active, ws, ws_bytes, stream);
 }
@@ -687,10 +711,9 @@ int eva_generate(const eva_rcache* cache, const void* q, const void* k, const vo
                  const int* active, void* ws, size_t ws_bytes, void* stream) {
     int st = check_rcache(cache);
     if (st != EVA_OK) return st;
-    if (cache->dtype != EVA_BF16) return EVA_ERR_UNSUPPORTED;
     if (T < 1 || !q || !k || !v || !o) return EVA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k)) return EVA_ERR_INVALID;
-    const size_t es = 2;  // bf16
+    const size_t es = cache->dtype == EVA_F32 ? 4 : 2;
     const size_t q_step = (size_t)cache->B * cache->H * cache->d * es;
     const size_t kv_step = (size_t)cache->B * cache->H_kv * cache->d * es;
     const char* qc = static_cast<const char*>(q);

@@ -101,9 +101,15 @@ def test_decode_needs_a_token(lib):
     assert lib.eva_decode_workspace_bytes(ctypes.byref(c)) == 0
 
 
-def test_decode_rejects_fp32_cache(lib):
+def test_decode_fp32_cache_validates_before_launch(lib):
+    # fp32 caches decode too (their own kernel); malformed calls are still
+    # refused before anything is enqueued
+    c = make_cache(dtype=_lib.EVA_F32, n_tok=0)
+    assert lib.eva_decode_step(ctypes.byref(c), FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
     c = make_cache(dtype=_lib.EVA_F32, n_tok=5)
-    assert lib.eva_decode_step(ctypes.byref(c), FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert lib.eva_decode_step(ctypes.byref(c), None, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert lib.eva_append_decode(ctypes.byref(c), FAKE, None, FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
+    assert c.n_tok == 5
 
 
 def test_append_capacity(lib):
@@ -125,7 +131,7 @@ def test_append_decode_rejects(lib):
     assert f(ctypes.byref(c), FAKE, None, FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
     assert f(ctypes.byref(c), FAKE, FAKE, FAKE, None, None, 0, None) == _lib.EVA_ERR_INVALID
     c = make_cache(n_tok=5, dtype=_lib.EVA_F32)
-    assert f(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert f(ctypes.byref(c), FAKE, FAKE, None, FAKE, None, 0, None) == _lib.EVA_ERR_INVALID
     assert c.n_tok == 5
 
 
@@ -228,7 +234,7 @@ def test_rcache_fill_rejects(lib):
 
 def test_rdecode_and_generate_reject(lib):
     c = make_rcache(dtype=_lib.EVA_F32)
-    assert lib.eva_rdecode_step(ctypes.byref(c), FAKE, FAKE, None, None, 0, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert lib.eva_rdecode_step(ctypes.byref(c), None, FAKE, None, None, 0, None) == _lib.EVA_ERR_INVALID
     c = make_rcache()
     g = lib.eva_generate
     assert g(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, 0, None, None, 0, None) == _lib.EVA_ERR_INVALID

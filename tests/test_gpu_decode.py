@@ -33,13 +33,12 @@ def oracle_row(qrow, K, V, p, W, C, window=oracle.SLIDING):
 
 
 def run_sequence(B, H, Hkv, d, W, C, L0, steps, seed, fill=None, use_ws=True, check_every=1, fused=False,
-                 window=oracle.SLIDING):
+                 window=oracle.SLIDING, dtype=torch.bfloat16):
     """Prefill L0 tokens (if L0 > 0) into a cache, then append + decode `steps`
     tokens (two calls, or the fused call); compare every `check_every`-th
     decode output with the oracle."""
-    print(f"decode B{B} H{H}/{Hkv} d{d} W{W} C{C} L0={L0} steps={steps} fill={fill} ws={use_ws} fused={fused}",
-          flush=True)
-    dtype = torch.bfloat16
+    print(f"decode B{B} H{H}/{Hkv} d{d} W{W} C{C} L0={L0} steps={steps} fill={fill} ws={use_ws} fused={fused} "
+          f"{dtype}", flush=True)
     total = L0 + steps
     q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
     cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=total, dtype=dtype, fill=fill, window=window)
@@ -217,3 +216,42 @@ def test_prefill_with_cache_matches_parts_on_a_stream():
     for name, t in snap.items():
         assert torch.equal(t, getattr(b, name)), name
     assert torch.equal(oa, ob)
+
+
+# ---- fp32 caches (their own decode kernel, fp32 matrix-core products):
+# held to the fp32 bound, 1e-5 row-normwise relative error
+F32_DECODE = [
+    # B, H, Hkv, d, W, C, L0, steps, check_every, fill, window
+    (2, 8, 2, 128, 64, 16, 300, 1, 1, None, oracle.SLIDING),
+    (1, 4, 2, 128, 64, 16, 100, 260, 7, None, oracle.SLIDING),       # chunk completions, ring wraps
+    (2, 4, 2, 64, 40, 8, 77, 60, 3, float("nan"), oracle.SLIDING),   # stale slots must not leak
+    (1, 4, 2, 128, 1, 8, 30, 40, 1, None, oracle.SLIDING),           # W = 1
+    (1, 48, 1, 128, 48, 16, 200, 20, 6, None, oracle.SLIDING),       # G = 48: three head groups
+    (1, 4, 1, 64, 24, 8, 0, 120, 5, None, oracle.SLIDING),           # from an empty cache
+    (1, 8, 2, 128, 64, 16, 150, 140, 3, None, oracle.CHUNK_ALIGNED),
+    (1, 8, 2, 128, 64, 16, 150, 140, 3, None, oracle.BLOCKED),
+]
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("shape", F32_DECODE)
+def test_decode_fp32(shape, fused):
+    B, H, Hkv, d, W, C, L0, steps, every, fill, window = shape
+    run_sequence(B, H, Hkv, d, W, C, L0=L0, steps=steps, seed=34, fill=fill, check_every=every, fused=fused,
+                 window=window, dtype=torch.float32)
+
+
+def test_noalloc_fp32_cache():
+    # the allocation-free fused step on an fp32 cache (no split partials):
+    # the bytes of eva_append_decode
+    B, H, Hkv, d, W, C, L0 = 2, 8, 2, 128, 64, 16, 300
+    q, k, v = inputs.qkv(B, H, Hkv, L0 + 1, d, torch.float32, seed=35)
+    outs = []
+    for noalloc in (False, True):
+        cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L0 + 1, dtype=torch.float32)
+        eva.prefill(q[:, :, :L0].contiguous().cuda(), k[:, :, :L0].contiguous().cuda(),
+                    v[:, :, :L0].contiguous().cuda(), W, C, cache=cache)
+        qn, kn, vn = (x[:, :, L0].contiguous().cuda() for x in (q, k, v))
+        outs.append(eva.append_decode_noalloc(cache, qn, kn, vn) if noalloc else eva.append_decode(cache, qn, kn, vn))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])

@@ -93,18 +93,18 @@ def step_inputs(q, k, v, pos):
 
 
 def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, use_ws=True, max_tokens=None,
-              check_every=1, fused=False, window=oracle.SLIDING):
+              check_every=1, fused=False, window=oracle.SLIDING, dtype=torch.bfloat16):
     print(f"ragged B{B} H{H}/{Hkv} d{d} W{W} C{C} lens={lens} steps={steps} fill={fill} ws={use_ws} "
-          f"fused={fused}", flush=True)
+          f"fused={fused} {dtype}", flush=True)
     total = max(lens) + steps
-    q, k, v = inputs.qkv(B, H, Hkv, total, d, torch.bfloat16, seed=seed)
+    q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
     if max_tokens is None:
         max_tokens = total
     cache = load_ragged(q, k, v, lens, W, C, max_tokens, seed, fill=fill, window=window)
     assert cache.n_tok.cpu().tolist() == [min(n, max_tokens) for n in lens]
     orc = SequenceOracle(q, k, v, W, C, window)
     n = [min(x, max_tokens) for x in lens]
-    sentinel = torch.full((B, H, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    sentinel = torch.full((B, H, d), 7.0, dtype=dtype, device="cuda")
     for t in range(steps):
         act = [True] * B if active_fn is None else [bool(active_fn(t, b)) for b in range(B)]
         active = None if active_fn is None else torch.tensor(act, dtype=torch.int32, device="cuda")
@@ -130,7 +130,7 @@ def run_steps(B, H, Hkv, d, W, C, lens, steps, seed, fill=None, active_fn=None, 
             p = n[b] - 1  # a full sequence decodes this step's query over its last position
             for h in range(H):
                 ref = orc.rows(b, h, [p], qrows=qs[b, h][None].cpu())
-                assert_parity(got[b, h][None], ref, torch.bfloat16, f"step {t} b{b} h{h} p={p}")
+                assert_parity(got[b, h][None], ref, dtype, f"step {t} b{b} h{h} p={p}")
     return cache
 
 
@@ -182,12 +182,13 @@ def test_ragged_head_groupings(H, Hkv):
     run_steps(2, H, Hkv, 128, 48, 16, lens=[200, 90], steps=12, seed=46, check_every=5)
 
 
-def test_generate_equals_step_loop_and_oracle():
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_generate_equals_step_loop_and_oracle(dtype):
     B, H, Hkv, d, W, C, T = 3, 8, 2, 128, 64, 16, 40
     lens = [150, 33, 90]
     seed = 47
     total = max(lens) + T
-    q, k, v = inputs.qkv(B, H, Hkv, total, d, torch.bfloat16, seed=seed)
+    q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=seed)
     pos = [[n + t for n in lens] for t in range(T)]
     qs = torch.stack([step_inputs(q, k, v, p)[0] for p in pos]).cuda()
     ks = torch.stack([step_inputs(q, k, v, p)[1] for p in pos]).cuda()
@@ -205,7 +206,7 @@ def test_generate_equals_step_loop_and_oracle():
     for b in range(B):
         for h in (0, H - 1):
             ref = orc.rows(b, h, [lens[b] + t for t in range(T)])
-            assert_parity(got[:, b, h], ref, torch.bfloat16, f"b{b} h{h}")
+            assert_parity(got[:, b, h], ref, dtype, f"b{b} h{h}")
 
 
 def test_generate_graph_replays():
@@ -273,3 +274,14 @@ def test_generation_workload_sampled():
             ts = [0, steps // 2, steps - 1]
             ref = orc.rows(b, h, [lens[b] + t for t in ts])
             assert_parity(got[ts, b, h], ref, w.dtype, f"b{b} h{h}")
+
+
+# fp32 ragged caches (fp32 decode kernel; the fused calls append, then decode)
+@pytest.mark.parametrize("fused", [False, True])
+def test_ragged_generation_fp32(fused):
+    def active(t, b):
+        return not (b == 1 and 5 <= t < 25)
+    run_steps(4, 8, 2, 128, 64, 16, lens=[100, 37, 250, 1], steps=120, seed=45, check_every=7, fused=fused,
+              active_fn=active, dtype=torch.float32)
+    run_steps(3, 4, 2, 64, 40, 8, lens=[0, 77, 9], steps=50, seed=46, fill=float("nan"), check_every=5,
+              fused=fused, max_tokens=110, dtype=torch.float32)
