@@ -118,6 +118,13 @@ typedef enum {
  * n_tok counts the tokens the cache has absorbed (the same for every
  * sequence of the batch); the library updates it.  `window` is the causal
  * window variant the cache serves (any eva_window but EVA_WINDOW_NONCAUSAL).
+ * With rf = 1 the summaries are the paper's stochastic single-sample ones
+ * throughout: the caller fills the cache (eva_cache_fill) with summaries
+ * from eva_build_summaries_rf(eps = eva_rf_noise(rf_seed), rf_lambda), and
+ * every chunk an append completes gets its summary from the same estimator
+ * and the same counter-based draw (eva_rf_noise's, for that chunk), so the
+ * cache holds what eva_build_summaries_rf over the whole sequence would.
+ * rf must be 0 or 1 and rf_lambda finite and >= 0 (INVALID otherwise).
  */
 typedef struct eva_cache {
     int B, H, H_kv, d, W, C;
@@ -130,6 +137,12 @@ typedef struct eva_cache {
     void* vt_ring;
     void* k_sum;
     void* vt_sum;
+    int rf;           /* summaries of chunks completed by appends: 0 the
+                         deterministic ones (eva_build_summaries), 1 the
+                         stochastic ones (eva_build_summaries_rf) with the
+                         noise eva_rf_noise draws for that chunk */
+    float rf_lambda;  /* lambda of the stochastic summaries (rf = 1) */
+    unsigned long long rf_seed; /* seed of their noise (rf = 1) */
 } eva_cache;
 
 /*
@@ -160,13 +173,29 @@ int eva_build_summaries(const void* K, const void* V, void* Ksum, void* Vsum,
  *   eps  device fp32 [B][H_kv][L / C][d], 16-byte aligned: the standard
  *        normal draws, one vector per chunk, supplied by the caller.
  * The prefill kernel takes these summaries as it takes any
- * (eva_prefill_attention).  The decode cache builds deterministic summaries
- * for chunks completed during decode.
+ * (eva_prefill_attention).  With eps from eva_rf_noise, a decode cache with
+ * rf = 1 and the same seed and lambda builds the chunks its appends complete
+ * the same way, with the same draws.
  * Errors: as eva_build_summaries; INVALID for a null or misaligned eps or a
  * negative, NaN or infinite lambda.
  */
 int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float lambda, void* Ksum, void* Vsum,
                            int B, int H_kv, int L, int d, int C, int dtype, void* stream);
+
+/*
+ * Counter-based noise for the stochastic summaries: eps [B][H_kv][n_chunks][d]
+ * (fp32, device, 16-byte aligned) receives standard normal draws, the draw
+ * of chunk c of (b, g) depending only on (seed, b * H_kv + g, c): features
+ * 4i .. 4i+3 come from one Philox4x32-10 block (Salmon et al., SC 2011;
+ * counter (i, c, b * H_kv + g, 0), key = the seed's low and high words), each
+ * word pair (x, y) giving two normals by the Box-Muller transform on the
+ * 24-bit uniforms u = ((x >> 8) + 1/2) 2^-24, v = ((y >> 8) + 1/2) 2^-24:
+ * sqrt(-2 ln u) cos(2 pi v) and sqrt(-2 ln u) sin(2 pi v).  The decode cache
+ * draws the same noise for the chunks its appends complete (rf = 1).
+ * Errors: INVALID (B, H_kv < 1, n_chunks < 0, null or misaligned eps),
+ * UNSUPPORTED (d not 64 or 128, sizes).
+ */
+int eva_rf_noise(float* eps, int B, int H_kv, int n_chunks, int d, unsigned long long seed, void* stream);
 
 /*
  * EVA prefill (section "FlashEVA"): O = one softmax per row over the window
@@ -176,7 +205,8 @@ int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float
  * window + summary attention kernel.  If `cache` is not NULL it must describe
  * the same B, H, H_kv, d, W, C and dtype with S_max >= L / C; the call then
  * also writes the last min(L, R) keys/values into the ring, all L / C
- * summaries into the cache, and sets cache->n_tok = L.
+ * summaries into the cache, and sets cache->n_tok = L.  (A cache with rf = 1
+ * is INVALID here: this call builds deterministic summaries.)
  * Errors: INVALID (shapes, W < 1, C < 1, H % H_kv != 0, null pointers,
  * cache mismatch), CAPACITY (cache too small), UNSUPPORTED (d, dtype).
  */
@@ -368,6 +398,9 @@ typedef struct eva_rcache {
     void* vt_ring;
     void* k_sum;
     void* vt_sum;
+    int rf;           /* as in eva_cache */
+    float rf_lambda;
+    unsigned long long rf_seed;
 } eva_rcache;
 
 /*

@@ -55,6 +55,11 @@ def _load():
     lib.eva_ref_backward_terms.restype = None
     lib.eva_ref_backward_terms.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
                                            ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
+    lib.eva_ref_philox4x32_10.restype = None
+    lib.eva_ref_philox4x32_10.argtypes = [ctypes.POINTER(ctypes.c_uint), ctypes.POINTER(ctypes.c_uint),
+                                          ctypes.POINTER(ctypes.c_uint)]
+    lib.eva_ref_rf_noise.restype = None
+    lib.eva_ref_rf_noise.argtypes = [_dp, ctypes.c_long, ctypes.c_long, ctypes.c_int, ctypes.c_ulonglong]
     lib.eva_ref_num_threads.restype = ctypes.c_int
     lib.eva_ref_num_threads.argtypes = []
     lib.eva_ref_set_num_threads.restype = None
@@ -235,3 +240,21 @@ def backward_terms(Q, K, V, dO, W: int, C: int):
             Tk[b, g] = tk
             Tv[b, g] = tv
     return Tq, Tk, Tv
+
+
+def philox4x32_10(counter, key):
+    """One Philox4x32-10 block: counter (4 words), key (2 words) -> 4 words."""
+    c = (ctypes.c_uint * 4)(*[int(x) & 0xffffffff for x in counter])
+    k = (ctypes.c_uint * 2)(*[int(x) & 0xffffffff for x in key])
+    out = (ctypes.c_uint * 4)()
+    _load().eva_ref_philox4x32_10(c, k, out)
+    return [int(x) for x in out]
+
+
+def rf_noise(n_seq: int, n_chunks: int, d: int, seed: int):
+    """Counter-based standard normal draws [n_seq, n_chunks, d] (see
+    eva_ref_rf_noise): the noise of chunk c of sequence-head s = b * H_kv + g."""
+    eps = np.zeros((n_seq, n_chunks, d))
+    if eps.size:
+        _load().eva_ref_rf_noise(_ptr(eps), n_seq, n_chunks, d, int(seed) & 0xffffffffffffffff)
+    return eps

@@ -153,6 +153,67 @@ void eva_ref_summaries_rf(const double* K, const double* V, const double* eps, l
     free(omega);
 }
 
+/* Counter-based normal draws for the stochastic summaries (test
+ * infrastructure for the paper's single-sample estimator: the draw of chunk
+ * c of sequence-head s must be reproducible wherever the chunk's summary is
+ * built, at prefill or when decode completes the chunk).
+ *
+ * Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC 2011): a 128-bit counter and a 64-bit key; each of ten
+ * rounds multiplies counter words 0 and 2 by 0xD2511F53 and 0xCD9E8D57 into
+ * 64-bit products (hi, lo) and produces
+ *     (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)),
+ * the key advancing by (0x9E3779B9, 0xBB67AE85) between rounds. */
+void eva_ref_philox4x32_10(const unsigned* ctr, const unsigned* key, unsigned* out)
+{
+    unsigned c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+    unsigned k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        unsigned long long p0 = (unsigned long long)0xD2511F53u * c[0];
+        unsigned long long p1 = (unsigned long long)0xCD9E8D57u * c[2];
+        unsigned hi0 = (unsigned)(p0 >> 32), lo0 = (unsigned)p0;
+        unsigned hi1 = (unsigned)(p1 >> 32), lo1 = (unsigned)p1;
+        unsigned n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+    for (int i = 0; i < 4; ++i) out[i] = c[i];
+}
+
+/* eps[s][c][f] for s < n_seq, c < n_chunks, f < d (d a multiple of 4):
+ * standard normal draws.  Features 4i .. 4i+3 of (s, c) come from one Philox
+ * block, counter (i, c, s, 0), key (seed low word, seed high word); the
+ * Box-Muller transform (G. E. P. Box and M. E. Muller, 1958) turns each pair of
+ * its words (x, y) into two normals: with u = (x >> 8) + 1/2 and
+ * v = (y >> 8) + 1/2 scaled by 2^-24 (24-bit uniforms on (0, 1)),
+ * sqrt(-2 ln u) cos(2 pi v) and sqrt(-2 ln u) sin(2 pi v). */
+void eva_ref_rf_noise(double* eps, long n_seq, long n_chunks, int d, unsigned long long seed)
+{
+    const unsigned key[2] = {(unsigned)seed, (unsigned)(seed >> 32)};
+    const double two_pi = 6.283185307179586476925286766559;
+    for (long s = 0; s < n_seq; ++s)
+        for (long c = 0; c < n_chunks; ++c)
+            for (int i = 0; i < d / 4; ++i) {
+                const unsigned ctr[4] = {(unsigned)i, (unsigned)c, (unsigned)s, 0u};
+                unsigned x[4];
+                eva_ref_philox4x32_10(ctr, key, x);
+                double* e = eps + ((size_t)s * n_chunks + c) * d + 4 * i;
+                for (int h = 0; h < 2; ++h) {
+                    double u = ((double)(x[2 * h] >> 8) + 0.5) / 16777216.0;
+                    double v = ((double)(x[2 * h + 1] >> 8) + 0.5) / 16777216.0;
+                    double r = sqrt(-2.0 * log(u));
+                    e[2 * h] = r * cos(two_pi * v);
+                    e[2 * h + 1] = r * sin(two_pi * v);
+                }
+            }
+}
+
 /* One attention row: query q at position n against the exact keys of its
  * window and the visible chunk summaries. */
 void eva_ref_attend_row(const double* q, const double* K, const double* V,

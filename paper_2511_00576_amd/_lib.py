@@ -25,6 +25,7 @@ EVA_WINDOW_NONCAUSAL = 3
 SYMBOLS = (
     "eva_build_summaries",
     "eva_build_summaries_rf",
+    "eva_rf_noise",
     "eva_prefill",
     "eva_prefill_attention",
     "eva_prefill_attention_ex",
@@ -55,6 +56,7 @@ class EvaCacheStruct(ctypes.Structure):
         ("R", ctypes.c_int), ("S_max", ctypes.c_int), ("n_tok", ctypes.c_longlong),
         ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
         ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
+        ("rf", ctypes.c_int), ("rf_lambda", ctypes.c_float), ("rf_seed", ctypes.c_ulonglong),
     ]
 
 
@@ -66,6 +68,7 @@ class EvaRCacheStruct(ctypes.Structure):
         ("n_tok", ctypes.c_void_p), ("arrive", ctypes.c_void_p),
         ("k_ring", ctypes.c_void_p), ("vt_ring", ctypes.c_void_p),
         ("k_sum", ctypes.c_void_p), ("vt_sum", ctypes.c_void_p),
+        ("rf", ctypes.c_int), ("rf_lambda", ctypes.c_float), ("rf_seed", ctypes.c_ulonglong),
     ]
 
 
@@ -87,6 +90,8 @@ def load():
     lib.eva_build_summaries.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
     lib.eva_build_summaries_rf.restype = i
     lib.eva_build_summaries_rf.argtypes = [vp, vp, vp, ctypes.c_float, vp, vp, i, i, i, i, i, i, vp]
+    lib.eva_rf_noise.restype = i
+    lib.eva_rf_noise.argtypes = [vp, i, i, i, i, ctypes.c_ulonglong, vp]
     lib.eva_prefill.restype = i
     lib.eva_prefill.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_prefill_attention.restype = i

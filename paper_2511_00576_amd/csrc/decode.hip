@@ -140,7 +140,16 @@ __device__ void append_token(const CacheView& c, size_t bg, int p, const T* __re
     if (s_new >= 0 && s_new < c.S_max) {
         RingChunkPlusNew<D, T> src{{kr, vr, (long long)s_new * c.C, c.R}, kn, vn, c.C - 1};
         float kh[8], vh[8];
-        chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
+        if (c.rf) {
+            // this thread's 8 features of the chunk's counter-based draw
+            const int cc = threadIdx.x % (D / 8);
+            float e[8];
+            rf_normals4(c.rf_seed, (uint32_t)(2 * cc), (uint32_t)s_new, (uint32_t)bg, e);
+            rf_normals4(c.rf_seed, (uint32_t)(2 * cc + 1), (uint32_t)s_new, (uint32_t)bg, e + 4);
+            chunk_summary<D, true>(src, c.C, smem, smem + c.C, kh, vh, RfNoise{e, c.rf_scale});
+        } else {
+            chunk_summary<D>(src, c.C, smem, smem + c.C, kh, vh);
+        }
         const int t = threadIdx.x;
         if (t < D / 8) {
             T* ks = static_cast<T*>(c.k_sum) + bg * (size_t)c.S_max * D;

@@ -78,8 +78,13 @@ int check_cache(const eva_cache* c) {
     if (c->R < 32 || c->R % 32 != 0 || c->S_max < 32 || c->S_max % 32 != 0) return EVA_ERR_INVALID;
     if ((long long)c->R < (long long)c->W + c->C - 1) return EVA_ERR_CAPACITY;
     if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (c->rf != 0 && c->rf != 1) return EVA_ERR_INVALID;
+    if (c->rf && (!(c->rf_lambda >= 0.f) || c->rf_lambda > 1e30f)) return EVA_ERR_INVALID;
     return EVA_OK;
 }
+
+// lambda * d^(1/4): the noise's weight in the summaries' logit vectors
+float rf_scale_of(int rf, float lambda, int d) { return rf ? (float)(lambda * sqrt(sqrt((double)d))) : 0.f; }
 
 eva::CacheView view_of(const eva_cache* c) {
     eva::CacheView v;
@@ -96,6 +101,9 @@ eva::CacheView view_of(const eva_cache* c) {
     v.vt_ring = c->vt_ring;
     v.k_sum = c->k_sum;
     v.vt_sum = c->vt_sum;
+    v.rf = c->rf;
+    v.rf_scale = rf_scale_of(c->rf, c->rf_lambda, c->d);
+    v.rf_seed = c->rf_seed;
     return v;
 }
 
@@ -135,6 +143,8 @@ int check_rcache(const eva_rcache* c) {
     // summaries are built as chunks complete: up to max_tok / C of them
     if (c->max_tok / c->C > c->S_max) return EVA_ERR_CAPACITY;
     if ((long long)c->B * c->H_kv > 65535) return EVA_ERR_UNSUPPORTED;
+    if (c->rf != 0 && c->rf != 1) return EVA_ERR_INVALID;
+    if (c->rf && (!(c->rf_lambda >= 0.f) || c->rf_lambda > 1e30f)) return EVA_ERR_INVALID;
     return EVA_OK;
 }
 
@@ -153,6 +163,9 @@ eva::CacheView rview_of(const eva_rcache* c) {
     v.vt_ring = c->vt_ring;
     v.k_sum = c->k_sum;
     v.vt_sum = c->vt_sum;
+    v.rf = c->rf;
+    v.rf_scale = rf_scale_of(c->rf, c->rf_lambda, c->d);
+    v.rf_seed = c->rf_seed;
     return v;
 }
 
@@ -237,6 +250,17 @@ int eva_build_summaries_rf(const void* K, const void* V, const float* eps, float
         return eva::launch_summaries<decltype(dd)::value, decltype(t)>(K, V, Ksum, Vsum, B * H_kv, L, C, eps,
                                                                        rf_scale, s);
     }));
+}
+
+int eva_rf_noise(float* eps, int B, int H_kv, int n_chunks, int d, unsigned long long seed, void* stream) {
+    if (B < 1 || H_kv < 1 || n_chunks < 0) return EVA_ERR_INVALID;
+    if (d != 64 && d != 128) return EVA_ERR_UNSUPPORTED;
+    if ((long long)B * H_kv > 65535 || n_chunks > kMaxLen) return EVA_ERR_UNSUPPORTED;
+    if (n_chunks == 0) return EVA_OK;
+    if (!eps || !aligned16(eps)) return EVA_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(d == 64 ? eva::launch_rf_noise<64>(eps, B * H_kv, n_chunks, seed, s)
+                              : eva::launch_rf_noise<128>(eps, B * H_kv, n_chunks, seed, s));
 }
 
 int eva_prefill_attention(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
@@ -385,6 +409,9 @@ int eva_prefill_ex(const void* Q, const void* K, const void* V, void* O, int B, 
         if (cache->B != B || cache->H != H || cache->H_kv != H_kv || cache->d != d || cache->W != W ||
             cache->C != C || cache->dtype != dtype || cache->window != window)
             return EVA_ERR_INVALID;
+        // this call builds deterministic summaries: a cache of stochastic
+        // ones is filled by eva_cache_fill from eva_build_summaries_rf
+        if (cache->rf) return EVA_ERR_INVALID;
         if (cache->S_max < n_chunks) return EVA_ERR_CAPACITY;
     }
     st = eva_build_summaries(K, V, Ksum, Vsum, B, H_kv, L, d, C, dtype, stream);

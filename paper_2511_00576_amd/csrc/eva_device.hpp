@@ -104,6 +104,49 @@ __host__ __device__ __forceinline__ size_t vt_index(int f, int r) {
     return (size_t)(r >> 3) * (kVtTile * D) + (size_t)f * kVtTile + (r & 7);
 }
 
+// Counter-based normal draws for the stochastic summaries, so that the draw
+// of chunk c of sequence-head s is the same wherever its summary is built.
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds over a
+// 128-bit counter with a 64-bit key; a round takes the 64-bit products of
+// counter words 0 and 2 with two fixed multipliers, swaps their halves in and
+// mixes in the key, which advances by two fixed increments between rounds.
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t m0 = 0xD2511F53u, m1 = 0xCD9E8D57u;
+        const uint32_t hi0 = __umulhi(m0, c[0]), lo0 = m0 * c[0];
+        const uint32_t hi1 = __umulhi(m1, c[2]), lo1 = m1 * c[2];
+        const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+}
+
+// Normals for features 4i .. 4i+3 of chunk `chunk` of sequence-head `seq`:
+// Philox block at counter (i, chunk, seq, 0), key = the seed's two words;
+// each word pair (x, y) gives two normals by the Box-Muller transform on the
+// 24-bit uniforms u = ((x >> 8) + 1/2) 2^-24, v = ((y >> 8) + 1/2) 2^-24:
+// sqrt(-2 ln u) (cos 2 pi v, sin 2 pi v).
+__device__ __forceinline__ void rf_normals4(unsigned long long seed, uint32_t i, uint32_t chunk, uint32_t seq,
+                                            float out[4]) {
+    uint32_t c[4] = {i, chunk, seq, 0u};
+    philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const float u = ((float)(c[2 * h] >> 8) + 0.5f) * 5.9604644775390625e-8f;  // 2^-24
+        const float v = ((float)(c[2 * h + 1] >> 8) + 0.5f) * 5.9604644775390625e-8f;
+        const float r = sqrtf(-2.f * logf(u));
+        float sn, cs;
+        sincosf(6.283185307179586f * v, &sn, &cs);
+        out[2 * h] = r * cs;
+        out[2 * h + 1] = r * sn;
+    }
+}
+
 __device__ __forceinline__ int visible_summaries(int n, int W, int C) {
     int start = n - W + 1;
     return start > 0 ? start / C : 0;

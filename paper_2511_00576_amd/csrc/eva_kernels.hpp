@@ -99,9 +99,20 @@ template <int D, typename T>
 hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
                             const float* eps, float rf_scale, hipStream_t stream);
 
+// eps [n_seq][n_chunks][D]: the counter-based normal draws (rf_normals4) of
+// every chunk of every sequence-head.
+template <int D>
+hipError_t launch_rf_noise(float* eps, int n_seq, int n_chunks, unsigned long long seed, hipStream_t stream);
+
 struct CacheView {
     int B, H, Hkv, W, C, R, S_max;
     int window;  // causal window variant (kWinSliding / kWinChunkAligned / kWinBlocked)
+    // summaries built during decode: stochastic random-feature ones (rf != 0,
+    // rf_scale = lambda * d^(1/4), noise from rf_normals4 with rf_seed) or
+    // the deterministic ones
+    int rf;
+    float rf_scale;
+    unsigned long long rf_seed;
     long long n_tok;
     void* k_ring;
     void* vt_ring;

@@ -323,6 +323,32 @@ hipError_t launch_summaries_impl(const void* K, const void* V, void* Ks, void* V
 
 }  // namespace
 
+template <int D>
+__global__ __launch_bounds__(256) void rf_noise_kernel(float* __restrict__ eps, long long n_blocks,
+                                                       int n_chunks, unsigned long long seed) {
+    // one thread per block of 4 features: (seq, chunk, i)
+    const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n_blocks) return;
+    const int i = (int)(t % (D / 4));
+    const long long sc = t / (D / 4);
+    const int chunk = (int)(sc % n_chunks);
+    const int seq = (int)(sc / n_chunks);
+    float e[4];
+    rf_normals4(seed, (uint32_t)i, (uint32_t)chunk, (uint32_t)seq, e);
+    *reinterpret_cast<floatx4*>(eps + t * 4) = floatx4{e[0], e[1], e[2], e[3]};
+}
+
+template <int D>
+hipError_t launch_rf_noise(float* eps, int n_seq, int n_chunks, unsigned long long seed, hipStream_t stream) {
+    const long long n_blocks = (long long)n_seq * n_chunks * (D / 4);
+    if (n_blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL((rf_noise_kernel<D>), dim3((unsigned)((n_blocks + 255) / 256)), dim3(256), 0, stream, eps,
+                       n_blocks, n_chunks, seed);
+    return hipGetLastError();
+}
+template hipError_t launch_rf_noise<64>(float*, int, int, unsigned long long, hipStream_t);
+template hipError_t launch_rf_noise<128>(float*, int, int, unsigned long long, hipStream_t);
+
 template <int D, typename T>
 hipError_t launch_summaries(const void* K, const void* V, void* Ks, void* Vs, int BH, int L, int C,
                             const float* eps, float rf_scale, hipStream_t stream) {

@@ -74,6 +74,17 @@ def build_summaries_rf(K: torch.Tensor, V: torch.Tensor, eps: torch.Tensor, C: i
     return Ks, Vs
 
 
+def rf_noise(B, Hkv, n_chunks, d, seed, device="cuda"):
+    """Counter-based standard normal draws for the stochastic summaries:
+    fp32 [B, Hkv, n_chunks, d], chunk c of (b, g) depending only on
+    (seed, b * Hkv + g, c) (eva_rf_noise); the draws a cache with the same
+    seed uses for the chunks its appends complete."""
+    eps = torch.empty(B, Hkv, n_chunks, d, dtype=torch.float32, device=device)
+    _require_device(eps)
+    _lib.check("eva_rf_noise", _lib.load().eva_rf_noise(_ptr(eps), B, Hkv, n_chunks, d, int(seed), _stream()))
+    return eps
+
+
 class Cache:
     """Window + summary decode cache in device memory (see eva_cache in eva.h).
 
@@ -85,7 +96,7 @@ class Cache:
     """
 
     def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None,
-                 fill=None, window=_lib.EVA_WINDOW_SLIDING):
+                 fill=None, window=_lib.EVA_WINDOW_SLIDING, rf_lambda=None, rf_seed=0):
         if R is None:
             R = -(-(W + C - 1) // 32) * 32
         S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
@@ -99,7 +110,8 @@ class Cache:
         self.struct = _lib.EvaCacheStruct(B=B, H=H, H_kv=Hkv, d=d, W=W, C=C, dtype=_DTYPES[dtype], window=window,
                                           R=R, S_max=S_max, n_tok=0, k_ring=self.k_ring.data_ptr(),
                                           vt_ring=self.vt_ring.data_ptr(), k_sum=self.k_sum.data_ptr(),
-                                          vt_sum=self.vt_sum.data_ptr())
+                                          vt_sum=self.vt_sum.data_ptr(), rf=int(rf_lambda is not None),
+                                          rf_lambda=float(rf_lambda or 0.0), rf_seed=int(rf_seed))
         self._ws = None
 
     @property
@@ -256,7 +268,7 @@ class RaggedCache:
     so steps need no host-side state.  `max_tokens` bounds every sequence."""
 
     def __init__(self, B, H, Hkv, d, W, C, max_tokens, dtype=torch.bfloat16, device="cuda", R=None, fill=None,
-                 window=_lib.EVA_WINDOW_SLIDING):
+                 window=_lib.EVA_WINDOW_SLIDING, rf_lambda=None, rf_seed=0):
         if R is None:
             R = -(-(W + C - 1) // 32) * 32
         S_max = max(32, -(-(max_tokens // C + 1) // 32) * 32)
@@ -273,7 +285,8 @@ class RaggedCache:
                                            R=R, S_max=S_max, max_tok=max_tokens, n_tok=self.n_tok.data_ptr(),
                                            arrive=self.arrive.data_ptr(), k_ring=self.k_ring.data_ptr(),
                                            vt_ring=self.vt_ring.data_ptr(), k_sum=self.k_sum.data_ptr(),
-                                           vt_sum=self.vt_sum.data_ptr())
+                                           vt_sum=self.vt_sum.data_ptr(), rf=int(rf_lambda is not None),
+                                           rf_lambda=float(rf_lambda or 0.0), rf_seed=int(rf_seed))
         n = _lib.load().eva_rdecode_workspace_bytes(ctypes.byref(self.struct))
         self.ws = torch.empty((n + 3) // 4, dtype=torch.float32, device=device) if n else None
 

@@ -88,6 +88,9 @@ def make_cache(**kw):
     (dict(vt_sum=0x40004), _lib.EVA_ERR_INVALID),  # misaligned
     (dict(H=3), _lib.EVA_ERR_INVALID),
     (dict(d=80), _lib.EVA_ERR_UNSUPPORTED),
+    (dict(rf=2), _lib.EVA_ERR_INVALID),           # rf is 0 or 1
+    (dict(rf=1, rf_lambda=float("nan")), _lib.EVA_ERR_INVALID),
+    (dict(rf=1, rf_lambda=-0.1), _lib.EVA_ERR_INVALID),
 ])
 def test_cache_validation(lib, kw, code):
     c = make_cache(**kw)
@@ -191,6 +194,8 @@ def make_rcache(**kw):
     (dict(max_tok=132), _lib.EVA_ERR_CAPACITY),
     (dict(H=5), _lib.EVA_ERR_INVALID),
     (dict(d=96), _lib.EVA_ERR_UNSUPPORTED),
+    (dict(rf=3), _lib.EVA_ERR_INVALID),
+    (dict(rf=1, rf_lambda=float("inf")), _lib.EVA_ERR_INVALID),
 ])
 def test_rcache_validation(lib, kw, code):
     c = make_rcache(**kw)
@@ -282,3 +287,17 @@ def test_noncausal_takes_no_cache(lib):
                               ctypes.byref(c), None) == _lib.EVA_ERR_INVALID
     r = make_rcache(window=_lib.EVA_WINDOW_NONCAUSAL)
     assert lib.eva_rcache_append(ctypes.byref(r), FAKE, FAKE, None, None) == _lib.EVA_ERR_INVALID
+
+
+def test_rf_noise_and_rf_cache_validation(lib):
+    f = lib.eva_rf_noise
+    assert f(FAKE, 0, 2, 4, 64, 1, None) == _lib.EVA_ERR_INVALID
+    assert f(FAKE, 1, 2, -1, 64, 1, None) == _lib.EVA_ERR_INVALID
+    assert f(FAKE, 1, 2, 4, 96, 1, None) == _lib.EVA_ERR_UNSUPPORTED
+    assert f(None, 1, 2, 4, 64, 1, None) == _lib.EVA_ERR_INVALID
+    assert f(ctypes.c_void_p(0x10004), 1, 2, 4, 64, 1, None) == _lib.EVA_ERR_INVALID
+    assert f(None, 1, 2, 0, 64, 1, None) == _lib.EVA_OK  # nothing to draw
+    # eva_prefill builds deterministic summaries: a cache of stochastic ones is refused
+    c = make_cache(rf=1, rf_lambda=0.1, rf_seed=5)
+    assert prefill_call(lib, cache=ctypes.byref(c)) == _lib.EVA_ERR_INVALID
+    assert c.n_tok == 0

@@ -255,3 +255,66 @@ def test_noalloc_fp32_cache():
         outs.append(eva.append_decode_noalloc(cache, qn, kn, vn) if noalloc else eva.append_decode(cache, qn, kn, vn))
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1])
+
+
+# ---- stochastic (random-feature) summaries through decode: the cache
+# builds, for every chunk an append completes, the paper's single-sample
+# summary with the counter-based draw eva_rf_noise gives that chunk, so the
+# decoded rows equal the oracle's rows over summaries_rf of the whole history
+# with the oracle's own draws (same counters, computed independently)
+def test_rf_noise_matches_oracle_generator():
+    for d in (64, 128):
+        eps = eva.rf_noise(3, 5, 37, d, seed=2 ** 40 + 7)
+        torch.cuda.synchronize()
+        ref = oracle.rf_noise(15, 37, d, seed=2 ** 40 + 7).reshape(3, 5, 37, d)
+        assert_parity(to64(eps), ref, torch.float32, f"rf noise d{d}")
+
+
+def rf_oracle_row(qrow, K, V, p, W, C, lam, seed, seq):
+    """Oracle row at position p over the stochastic summaries of positions 0..p
+    of sequence-head `seq` (its draws from the counter-based generator)."""
+    n_chunks = (p + 1) // C
+    eps = oracle.rf_noise(seq + 1, max(n_chunks, 1), K.shape[1], seed)[seq, :n_chunks]
+    Ks, Vs = oracle.summaries_rf(K[: p + 1], V[: p + 1], eps, C, lam)
+    return oracle.attend_rows(qrow[None], np.array([p]), K[: p + 1], V[: p + 1], Ks, Vs, W, C)[0]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_rf_summaries(fused, dtype):
+    B, H, Hkv, d, W, C, L0, steps, lam, seed = 2, 8, 2, 128, 48, 16, 150, 90, 0.3, 1234567
+    print(f"rf decode fused={fused} {dtype}", flush=True)
+    q, k, v = inputs.qkv(B, H, Hkv, L0 + steps, d, dtype, seed=36)
+    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L0 + steps, dtype=dtype, fill=float("nan"), rf_lambda=lam,
+                      rf_seed=seed)
+    kp, vp = k[:, :, :L0].contiguous().cuda(), v[:, :, :L0].contiguous().cuda()
+    eps = eva.rf_noise(B, Hkv, L0 // C, d, seed)
+    Ks, Vs = eva.build_summaries_rf(kp, vp, eps, C, lam=lam)
+    eva.cache_fill(cache, kp, vp, Ks, Vs)
+    k64, v64 = to64(k), to64(v)
+    for t in range(steps):
+        p = L0 + t
+        kn, vn, qn = (x[:, :, p].contiguous().cuda() for x in (k, v, q))
+        if fused:
+            o = eva.append_decode(cache, qn, kn, vn)
+        else:
+            eva.cache_append(cache, kn, vn)
+            o = eva.decode_step(cache, qn)
+        if t % 11 and t != steps - 1:
+            continue
+        torch.cuda.synchronize()
+        got = to64(o)
+        for b in range(B):
+            for h in (0, H - 1):
+                g = h // (H // Hkv)
+                ref = rf_oracle_row(to64(q[b, h, p]), k64[b, g], v64[b, g], p, W, C, lam, seed, b * Hkv + g)
+                assert_parity(got[b, h][None], ref[None], dtype, f"p={p} b{b} h{h}")
+    # every summary the cache holds is the stochastic one of its chunk
+    n = (L0 + steps) // C
+    for b in range(B):
+        for g in range(Hkv):
+            eps_o = oracle.rf_noise(b * Hkv + g + 1, n, d, seed)[b * Hkv + g]
+            rK, rV = oracle.summaries_rf(k64[b, g, : n * C], v64[b, g, : n * C], eps_o, C, lam)
+            got_v = to64(cache.vt_sum[b, g].permute(0, 2, 1).reshape(-1, d)[:n])
+            assert_parity(to64(cache.k_sum[b, g, :n]), rK, dtype, "k_sum")
+            assert_parity(got_v, rV, dtype, "vt_sum")

@@ -285,3 +285,45 @@ def test_ragged_generation_fp32(fused):
               active_fn=active, dtype=torch.float32)
     run_steps(3, 4, 2, 64, 40, 8, lens=[0, 77, 9], steps=50, seed=46, fill=float("nan"), check_every=5,
               fused=fused, max_tokens=110, dtype=torch.float32)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_ragged_generation_rf_summaries(dtype):
+    # ragged cache of stochastic summaries: prompts loaded from
+    # eva_build_summaries_rf with the counter-based draws, every chunk the
+    # generation completes summarized with its own draw; rows against the
+    # oracle over summaries_rf of each sequence's tokens
+    B, H, Hkv, d, W, C, steps, lam, seed = 3, 8, 2, 128, 48, 16, 60, 0.3, 99
+    lens = [60, 130, 7]
+    total = max(lens) + steps
+    print(f"ragged rf generation {dtype}", flush=True)
+    q, k, v = inputs.qkv(B, H, Hkv, total, d, dtype, seed=51)
+    Qp, Kp, Vp = (t.cuda() for t in padded_prefill_inputs(q, k, v, lens, 51))
+    cache = eva.RaggedCache(B, H, Hkv, d, W, C, max_tokens=total, dtype=dtype, fill=float("nan"), rf_lambda=lam,
+                            rf_seed=seed)
+    L = Kp.shape[2]
+    eps = eva.rf_noise(B, Hkv, L // C, d, seed)
+    Ks, Vs = eva.build_summaries_rf(Kp, Vp, eps, C, lam=lam)
+    eva.rcache_fill(cache, Kp, Vp, Ks, Vs, torch.tensor(lens, dtype=torch.int32, device="cuda"))
+    k64, v64 = to64(k), to64(v)
+    n = list(lens)
+    for t in range(steps):
+        pos = list(n)
+        qs, ks, vs = (x.cuda() for x in step_inputs(q, k, v, pos))
+        o = eva.rappend_decode(cache, qs, ks, vs)
+        n = [x + 1 for x in n]
+        if t % 9 and t != steps - 1:
+            continue
+        torch.cuda.synchronize()
+        got = to64(o)
+        for b in range(B):
+            p = n[b] - 1
+            nc = (p + 1) // C
+            for h in (0, H - 1):
+                g = h // (H // Hkv)
+                seq = b * Hkv + g
+                e = oracle.rf_noise(seq + 1, max(nc, 1), d, seed)[seq, :nc]
+                rK, rV = oracle.summaries_rf(k64[b, g, : p + 1], v64[b, g, : p + 1], e, C, lam)
+                ref = oracle.attend_rows(to64(qs[b, h])[None], np.array([p]), k64[b, g, : p + 1], v64[b, g, : p + 1],
+                                         rK, rV, W, C)
+                assert_parity(got[b, h][None], ref, dtype, f"step {t} b{b} h{h} p={p}")

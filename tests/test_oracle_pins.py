@@ -561,3 +561,42 @@ def test_backward_terms_scale_with_the_output_gradient():
     R = rand((B, H, L, d), 105)
     for t1, t2 in zip(oracle.backward_terms(q, k, v, R, W, C), oracle.backward_terms(q, k, v, -2.5 * R, W, C)):
         np.testing.assert_allclose(t2, 2.5 * t1, rtol=1e-12, atol=0)
+
+
+# ---------------------------------------------------------------------------
+# Counter-based noise for the stochastic summaries (so that a chunk's draw
+# is the same whether its summary is built at prefill or during decode)
+# ---------------------------------------------------------------------------
+
+def test_philox_known_answers():
+    # Philox4x32-10 known-answer vectors of its authors' reference suite
+    # (Salmon et al., SC 2011): counter, key -> output
+    cases = [
+        ([0, 0, 0, 0], [0, 0], [0x6627e8d5, 0xe169c58d, 0xbc57ac4c, 0x9b00dbd8]),
+        ([0xffffffff] * 4, [0xffffffff] * 2, [0x408f276d, 0x41c83b0e, 0xa20bc7c6, 0x6d5451fd]),
+        ([0x243f6a88, 0x85a308d3, 0x13198a2e, 0x03707344], [0xa4093822, 0x299f31d0],
+         [0xd16cfe09, 0x94fdcceb, 0x5001e420, 0x24126ea1]),
+    ]
+    for ctr, key, want in cases:
+        assert oracle.philox4x32_10(ctr, key) == want
+
+
+def test_rf_noise_is_standard_normal():
+    from scipy import stats
+    eps = oracle.rf_noise(64, 64, 128, seed=12345).ravel()
+    assert abs(eps.mean()) < 5e-3 and abs(eps.var() - 1.0) < 1e-2
+    assert stats.kstest(eps, "norm").pvalue > 1e-3
+    # pairs from one Box-Muller draw, and neighbouring blocks, are uncorrelated
+    e = eps.reshape(-1, 4)
+    for i, j in ((0, 1), (2, 3), (1, 2)):
+        assert abs(np.corrcoef(e[:, i], e[:, j])[0, 1]) < 1e-2
+
+
+def test_rf_noise_depends_on_counter_and_seed_only():
+    big = oracle.rf_noise(5, 7, 64, seed=99)
+    small = oracle.rf_noise(2, 3, 64, seed=99)
+    np.testing.assert_array_equal(small, big[:2, :3])
+    other = oracle.rf_noise(2, 3, 64, seed=100)
+    assert np.abs(other - small).max() > 0.5
+    # seed words go to the key: the high word matters too
+    assert np.abs(oracle.rf_noise(1, 1, 64, seed=99 + (1 << 32)) - small[:1, :1]).max() > 0.5
