@@ -52,6 +52,12 @@ def _load():
     lib.eva_ref_backward_group.restype = None
     lib.eva_ref_backward_group.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
                                            ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
+    lib.eva_ref_backward_group_variant.restype = None
+    lib.eva_ref_backward_group_variant.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
+                                                   ctypes.c_long, ctypes.c_long, ctypes.c_int, _dp, _dp, _dp]
+    lib.eva_ref_backward_terms_variant.restype = None
+    lib.eva_ref_backward_terms_variant.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
+                                                   ctypes.c_long, ctypes.c_long, ctypes.c_int, _dp, _dp, _dp]
     lib.eva_ref_backward_terms.restype = None
     lib.eva_ref_backward_terms.argtypes = [_dp, _dp, _dp, _dp, ctypes.c_int, ctypes.c_long, ctypes.c_int,
                                            ctypes.c_long, ctypes.c_long, _dp, _dp, _dp]
@@ -186,10 +192,10 @@ def prefill_variant(Q, K, V, W: int, C: int, variant: int):
     return O
 
 
-def backward(Q, K, V, dO, W: int, C: int):
-    """Gradients of the EVA prefill (sliding window): Q, dO [B, H, L, d];
-    K, V [B, Hkv, L, d] -> (dQ, dK, dV) in fp64, for the loss whose gradient
-    with respect to O is dO."""
+def backward(Q, K, V, dO, W: int, C: int, variant: int = SLIDING):
+    """Gradients of the EVA prefill (window variant `variant`, default the
+    sliding window): Q, dO [B, H, L, d]; K, V [B, Hkv, L, d] -> (dQ, dK, dV)
+    in fp64, for the loss whose gradient with respect to O is dO."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
@@ -205,15 +211,16 @@ def backward(Q, K, V, dO, W: int, C: int):
             dq = np.zeros_like(q)
             dk = np.zeros((L, d))
             dv = np.zeros((L, d))
-            lib.eva_ref_backward_group(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])), _ptr(np.ascontiguousarray(V[b, g])),
-                                       _ptr(go), G, L, d, W, C, _ptr(dq), _ptr(dk), _ptr(dv))
+            lib.eva_ref_backward_group_variant(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])),
+                                               _ptr(np.ascontiguousarray(V[b, g])), _ptr(go), G, L, d, W, C,
+                                               int(variant), _ptr(dq), _ptr(dk), _ptr(dv))
             dQ[b, g * G:(g + 1) * G] = dq
             dK[b, g] = dk
             dV[b, g] = dv
     return dQ, dK, dV
 
 
-def backward_terms(Q, K, V, dO, W: int, C: int):
+def backward_terms(Q, K, V, dO, W: int, C: int, variant: int = SLIDING):
     """Term magnitudes of backward() (rounding-error scales, not part of the
     method): for every gradient entry the sum of the absolute values of the
     terms it sums, carried through the same steps.  Same shapes as
@@ -233,9 +240,9 @@ def backward_terms(Q, K, V, dO, W: int, C: int):
             tq = np.zeros_like(q)
             tk = np.zeros((L, d))
             tv = np.zeros((L, d))
-            lib.eva_ref_backward_terms(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])),
-                                       _ptr(np.ascontiguousarray(V[b, g])), _ptr(go), G, L, d, W, C, _ptr(tq),
-                                       _ptr(tk), _ptr(tv))
+            lib.eva_ref_backward_terms_variant(_ptr(q), _ptr(np.ascontiguousarray(K[b, g])),
+                                               _ptr(np.ascontiguousarray(V[b, g])), _ptr(go), G, L, d, W, C,
+                                               int(variant), _ptr(tq), _ptr(tk), _ptr(tv))
             Tq[b, g * G:(g + 1) * G] = tq
             Tk[b, g] = tk
             Tv[b, g] = tv

@@ -410,6 +410,32 @@ void eva_ref_prefill(const double* Q, const double* K, const double* V, double* 
     }
 }
 
+/* The items row n attends under a window variant (see
+ * eva_ref_attend_row_variant): exact keys [*lo, *hi], then the summaries
+ * listed in sum_idx (ascending); returns how many summaries. */
+static long variant_row_items(long n, long L, long W, long C, int variant, long* lo, long* hi, long* sum_idx)
+{
+    long n_chunks = L / C;
+    if (variant == 0) {
+        *lo = n - W + 1 < 0 ? 0 : n - W + 1;
+        *hi = n;
+    } else if (variant == 1) {
+        long start = n - W + 1 < 0 ? 0 : n - W + 1;
+        *lo = (start / C) * C;
+        *hi = n;
+    } else if (variant == 2) {
+        *lo = (n / W) * W;
+        *hi = n;
+    } else {
+        *lo = (n / W) * W;
+        *hi = *lo + W - 1 < L - 1 ? *lo + W - 1 : L - 1;
+    }
+    long ns = 0;
+    for (long c = 0; c < n_chunks; ++c)
+        if ((c + 1) * C <= *lo || (variant == 3 && c * C > *hi)) sum_idx[ns++] = c;
+    return ns;
+}
+
 /* Threads the OpenMP runtime will use (1 when built without OpenMP). */
 /* Backward pass of the EVA prefill for one kv group: G query heads sharing
  * K, V.  Given dO (the gradient of a loss with respect to O), returns dQ,
@@ -426,9 +452,9 @@ void eva_ref_prefill(const double* Q, const double* K, const double* V, double* 
  *   dkhat = dkey_c + sum_j da_j k_j / sqrt(d),
  *   dk_j += da_j khat / sqrt(d) + dkhat / C.
  * The + ln C logit offset is a constant. */
-void eva_ref_backward_group(const double* Q, const double* K, const double* V, const double* dO,
-                            int G, long L, int d, long W, long C,
-                            double* dQ, double* dK, double* dV)
+void eva_ref_backward_group_variant(const double* Q, const double* K, const double* V, const double* dO,
+                                    int G, long L, int d, long W, long C, int variant,
+                                    double* dQ, double* dK, double* dV)
 {
     double inv_sqrt_d = 1.0 / sqrt((double)d);
     long n_chunks = L / C;
@@ -441,22 +467,23 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
     memset(dK, 0, (size_t)L * d * sizeof(double));
     memset(dV, 0, (size_t)L * d * sizeof(double));
 
-    double* logit = (double*)malloc((size_t)(W + nc1) * sizeof(double));
-    double* p = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    long* sidx = (long*)malloc(nc1 * sizeof(long));
+    double* logit = (double*)malloc((size_t)(L + nc1) * sizeof(double));
+    double* p = (double*)malloc((size_t)(L + nc1) * sizeof(double));
     double* o = (double*)malloc((size_t)d * sizeof(double));
     for (int h = 0; h < G; ++h) {
         for (long n = 0; n < L; ++n) {
             const double* q = Q + ((size_t)h * L + n) * d;
             const double* g = dO + ((size_t)h * L + n) * d;
             double* dq = dQ + ((size_t)h * L + n) * d;
-            long lo = n - W + 1 < 0 ? 0 : n - W + 1;
-            long n_win = n - lo + 1;
-            long n_sum = eva_ref_visible_summaries(n, W, C);
+            long lo, hi;
+            long n_sum = variant_row_items(n, L, W, C, variant, &lo, &hi, sidx);
+            long n_win = hi - lo + 1;
             long count = n_win + n_sum;
             /* forward of the row: items 0..n_win-1 are keys lo..n, then summaries */
             double lmax = -INFINITY;
             for (long i = 0; i < count; ++i) {
-                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)sidx[i - n_win] * d;
                 double s = 0.0;
                 for (int e = 0; e < d; ++e) s += q[e] * key[e];
                 logit[i] = s * inv_sqrt_d + (i < n_win ? 0.0 : log((double)C));
@@ -471,7 +498,7 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
             for (int e = 0; e < d; ++e) {
                 double acc = 0.0;
                 for (long i = 0; i < count; ++i) {
-                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)sidx[i - n_win] * d;
                     acc += p[i] * val[e];
                 }
                 o[e] = acc;
@@ -482,10 +509,10 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
             for (int e = 0; e < d; ++e) dq[e] = 0.0;
             for (long i = 0; i < count; ++i) {
                 const int win = i < n_win;
-                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
-                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
-                double* dkey = win ? dK + (size_t)(lo + i) * d : dKs + (size_t)(i - n_win) * d;
-                double* dval = win ? dV + (size_t)(lo + i) * d : dVs + (size_t)(i - n_win) * d;
+                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)sidx[i - n_win] * d;
+                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)sidx[i - n_win] * d;
+                double* dkey = win ? dK + (size_t)(lo + i) * d : dKs + (size_t)sidx[i - n_win] * d;
+                double* dval = win ? dV + (size_t)(lo + i) * d : dVs + (size_t)sidx[i - n_win] * d;
                 double gv = 0.0;
                 for (int e = 0; e < d; ++e) gv += g[e] * val[e];
                 const double dl = p[i] * (gv - D);
@@ -540,6 +567,7 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
     free(a);
     free(b);
     free(dkh);
+    free(sidx);
     free(logit);
     free(p);
     free(o);
@@ -547,6 +575,14 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
     free(Vs);
     free(dKs);
     free(dVs);
+}
+
+/* The sliding window (variant 0). */
+void eva_ref_backward_group(const double* Q, const double* K, const double* V, const double* dO,
+                            int G, long L, int d, long W, long C,
+                            double* dQ, double* dK, double* dV)
+{
+    eva_ref_backward_group_variant(Q, K, V, dO, G, L, d, W, C, 0, dQ, dK, dV);
 }
 
 /* Term magnitudes of eva_ref_backward_group, for rounding-error bounds (test
@@ -558,9 +594,9 @@ void eva_ref_backward_group(const double* Q, const double* K, const double* V, c
  * term to relative precision u is then off by at most about u times this
  * magnitude, however much the terms cancel.  Same arguments and layouts as
  * eva_ref_backward_group; Tq, Tk, Tv take the places of dQ, dK, dV. */
-void eva_ref_backward_terms(const double* Q, const double* K, const double* V, const double* dO,
-                            int G, long L, int d, long W, long C,
-                            double* Tq, double* Tk, double* Tv)
+void eva_ref_backward_terms_variant(const double* Q, const double* K, const double* V, const double* dO,
+                                    int G, long L, int d, long W, long C, int variant,
+                                    double* Tq, double* Tk, double* Tv)
 {
     double inv_sqrt_d = 1.0 / sqrt((double)d);
     long n_chunks = L / C;
@@ -573,20 +609,22 @@ void eva_ref_backward_terms(const double* Q, const double* K, const double* V, c
     memset(Tk, 0, (size_t)L * d * sizeof(double));
     memset(Tv, 0, (size_t)L * d * sizeof(double));
 
-    double* logit = (double*)malloc((size_t)(W + nc1) * sizeof(double));
-    double* p = (double*)malloc((size_t)(W + nc1) * sizeof(double));
+    long* sidx = (long*)malloc(nc1 * sizeof(long));
+    double* logit = (double*)malloc((size_t)(L + nc1) * sizeof(double));
+    double* p = (double*)malloc((size_t)(L + nc1) * sizeof(double));
     double* o = (double*)malloc((size_t)d * sizeof(double));
     for (int h = 0; h < G; ++h) {
         for (long n = 0; n < L; ++n) {
             const double* q = Q + ((size_t)h * L + n) * d;
             const double* g = dO + ((size_t)h * L + n) * d;
             double* tq = Tq + ((size_t)h * L + n) * d;
-            long lo = n - W + 1 < 0 ? 0 : n - W + 1;
-            long n_win = n - lo + 1;
-            long count = n_win + eva_ref_visible_summaries(n, W, C);
+            long lo, hi;
+            long n_sum = variant_row_items(n, L, W, C, variant, &lo, &hi, sidx);
+            long n_win = hi - lo + 1;
+            long count = n_win + n_sum;
             double lmax = -INFINITY;
             for (long i = 0; i < count; ++i) {
-                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
+                const double* key = i < n_win ? K + (size_t)(lo + i) * d : Ks + (size_t)sidx[i - n_win] * d;
                 double s = 0.0;
                 for (int e = 0; e < d; ++e) s += q[e] * key[e];
                 logit[i] = s * inv_sqrt_d + (i < n_win ? 0.0 : log((double)C));
@@ -601,7 +639,7 @@ void eva_ref_backward_terms(const double* Q, const double* K, const double* V, c
             for (int e = 0; e < d; ++e) {
                 double acc = 0.0;
                 for (long i = 0; i < count; ++i) {
-                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
+                    const double* val = i < n_win ? V + (size_t)(lo + i) * d : Vs + (size_t)sidx[i - n_win] * d;
                     acc += p[i] * val[e];
                 }
                 o[e] = acc;
@@ -611,10 +649,10 @@ void eva_ref_backward_terms(const double* Q, const double* K, const double* V, c
             for (int e = 0; e < d; ++e) tq[e] = 0.0;
             for (long i = 0; i < count; ++i) {
                 const int win = i < n_win;
-                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)(i - n_win) * d;
-                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)(i - n_win) * d;
-                double* tkey = win ? Tk + (size_t)(lo + i) * d : Tks + (size_t)(i - n_win) * d;
-                double* tval = win ? Tv + (size_t)(lo + i) * d : Tvs + (size_t)(i - n_win) * d;
+                const double* key = win ? K + (size_t)(lo + i) * d : Ks + (size_t)sidx[i - n_win] * d;
+                const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)sidx[i - n_win] * d;
+                double* tkey = win ? Tk + (size_t)(lo + i) * d : Tks + (size_t)sidx[i - n_win] * d;
+                double* tval = win ? Tv + (size_t)(lo + i) * d : Tvs + (size_t)sidx[i - n_win] * d;
                 double gv = 0.0;
                 for (int e = 0; e < d; ++e) gv += g[e] * val[e];
                 const double dl = fabs(p[i] * (gv - D));
@@ -670,6 +708,7 @@ void eva_ref_backward_terms(const double* Q, const double* K, const double* V, c
     free(a);
     free(b);
     free(tkh);
+    free(sidx);
     free(logit);
     free(p);
     free(o);
@@ -677,6 +716,14 @@ void eva_ref_backward_terms(const double* Q, const double* K, const double* V, c
     free(Vs);
     free(Tks);
     free(Tvs);
+}
+
+/* The sliding window (variant 0). */
+void eva_ref_backward_terms(const double* Q, const double* K, const double* V, const double* dO,
+                            int G, long L, int d, long W, long C,
+                            double* Tq, double* Tk, double* Tv)
+{
+    eva_ref_backward_terms_variant(Q, K, V, dO, G, L, d, W, C, 0, Tq, Tk, Tv);
 }
 
 int eva_ref_num_threads(void)

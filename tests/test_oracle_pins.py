@@ -600,3 +600,37 @@ def test_rf_noise_depends_on_counter_and_seed_only():
     assert np.abs(other - small).max() > 0.5
     # seed words go to the key: the high word matters too
     assert np.abs(oracle.rf_noise(1, 1, 64, seed=99 + (1 << 32)) - small[:1, :1]).max() > 0.5
+
+
+# Backward under the window variants: the same chain rule over each row's
+# variant item set
+@pytest.mark.parametrize("variant", [oracle.CHUNK_ALIGNED, oracle.BLOCKED, oracle.NONCAUSAL])
+@pytest.mark.parametrize("L,W,C", [(13, 4, 2), (14, 5, 3), (12, 20, 3)])
+def test_backward_variant_matches_finite_differences(variant, L, W, C):
+    B, H, Hkv, d = 1, 2, 1, 3
+    q, k, v = rand((B, H, L, d), 110), rand((B, Hkv, L, d), 111), rand((B, Hkv, L, d), 112)
+    R = rand((B, H, L, d), 113)
+    loss = lambda: float((oracle.prefill_variant(q, k, v, W, C, variant) * R).sum())
+    dq, dk, dv = oracle.backward(q, k, v, R, W, C, variant)
+    for x, g in ((q, dq), (k, dk), (v, dv)):
+        np.testing.assert_allclose(g, numeric_grad(loss, x), rtol=1e-6, atol=1e-8)
+    for g, t in zip((dq, dk, dv), oracle.backward_terms(q, k, v, R, W, C, variant)):
+        assert np.all(t >= np.abs(g) * (1 - 1e-12))
+
+
+def test_backward_variants_reduce_to_exact_attention():
+    # C = 1 with a window covering the sequence: every causal variant is exact
+    # causal attention and the non-causal one full attention, so the
+    # gradients are the library's (torch autograd through SDPA, fp64)
+    B, H, Hkv, L, d = 1, 2, 1, 16, 4
+    q, k, v = rand((B, H, L, d), 114), rand((B, Hkv, L, d), 115), rand((B, Hkv, L, d), 116)
+    R = rand((B, H, L, d), 117)
+    for variant, causal in ((oracle.CHUNK_ALIGNED, True), (oracle.BLOCKED, True), (oracle.NONCAUSAL, False)):
+        tq, tk, tv = (torch.from_numpy(x.copy()).requires_grad_() for x in (q, k, v))
+        o = torch.nn.functional.scaled_dot_product_attention(tq, tk.repeat_interleave(H // Hkv, 1),
+                                                             tv.repeat_interleave(H // Hkv, 1), is_causal=causal)
+        (o * torch.from_numpy(R)).sum().backward()
+        dq, dk, dv = oracle.backward(q, k, v, R, L, 1, variant)
+        np.testing.assert_allclose(dq, tq.grad.numpy(), rtol=1e-10, atol=1e-11)
+        np.testing.assert_allclose(dk, tk.grad.numpy(), rtol=1e-10, atol=1e-11)
+        np.testing.assert_allclose(dv, tv.grad.numpy(), rtol=1e-10, atol=1e-11)
