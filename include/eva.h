@@ -257,8 +257,16 @@ int eva_prefill_forward(const void* Q, const void* K, const void* V, const void*
                         float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                         void* stream);
 
+/* eva_prefill_forward under a window variant (eva_window), for the backward
+ * of the same variant.  Errors: as eva_prefill_forward; INVALID for an
+ * unknown window. */
+int eva_prefill_forward_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                           float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                           int window, void* stream);
+
 /*
- * Backward of the EVA prefill (sliding window, bf16): given dO [B][H][L][d],
+ * Backward of the EVA prefill (sliding window, bf16; eva_prefill_backward_ex
+ * takes the other window variants): given dO [B][H][L][d],
  * the gradient of a loss with respect to O, writes dQ [B][H][L][d] and
  * dK, dV [B][H_kv][L][d] of that loss — through the window keys and values,
  * the summary keys and values, and the summaries' own dependence on K and V
@@ -278,6 +286,20 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
                          const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK,
                          void* dV, void* ws, size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C,
                          int dtype, void* stream);
+
+/*
+ * eva_prefill_backward under a window variant (eva_window; the ablation
+ * "EVA Local Window Attention Variants" trains with blocked local windows as
+ * well as sliding ones): the gradients of the attention whose row n attends
+ * the exact keys [lo(n), hi(n)] and the summaries of the chunks wholly
+ * outside them (before, and for EVA_WINDOW_NONCAUSAL after), given the
+ * forward of the same variant (eva_prefill_forward_ex).
+ * Errors: as eva_prefill_backward; INVALID for an unknown window.
+ */
+int eva_prefill_backward_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                            const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK,
+                            void* dV, void* ws, size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C,
+                            int dtype, int window, void* stream);
 
 /* Workspace eva_prefill_backward needs (0 for invalid sizes). */
 size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d, int C);

@@ -31,7 +31,9 @@ SYMBOLS = (
     "eva_prefill_attention_ex",
     "eva_prefill_ex",
     "eva_prefill_forward",
+    "eva_prefill_forward_ex",
     "eva_prefill_backward",
+    "eva_prefill_backward_ex",
     "eva_prefill_backward_workspace_bytes",
     "eva_cache_fill",
     "eva_cache_append",
@@ -102,9 +104,14 @@ def load():
     lib.eva_prefill_ex.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp, vp, cp, vp]
     lib.eva_prefill_forward.restype = i
     lib.eva_prefill_forward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    lib.eva_prefill_forward_ex.restype = i
+    lib.eva_prefill_forward_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp]
     lib.eva_prefill_backward.restype = i
     lib.eva_prefill_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i, i,
                                          i, vp]
+    lib.eva_prefill_backward_ex.restype = i
+    lib.eva_prefill_backward_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i,
+                                            i, i, i, vp]
     lib.eva_prefill_backward_workspace_bytes.restype = sz
     lib.eva_prefill_backward_workspace_bytes.argtypes = [i, i, i, i, i, i]
     lib.eva_cache_fill.restype = i

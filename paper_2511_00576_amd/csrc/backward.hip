@@ -1,4 +1,4 @@
-// Backward pass of the fused EVA prefill (bf16, sliding window): dQ, dK, dV
+// Backward pass of the fused EVA prefill (bf16, every window variant): dQ, dK, dV
 // of a loss given dO, through the window keys/values, the summary keys and
 // values, and the summaries' own dependence on K and V.
 //
@@ -167,7 +167,7 @@ __device__ __forceinline__ bf16x8 pair_to_b(const floatx4& t0, const floatx4& t1
 // ---------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------
-template <int D, int NCB, int NS, int WPE>
+template <int D, int NCB, int NS, int WPE, int VAR>
 __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void bwd_dq_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
@@ -195,11 +195,21 @@ void bwd_dq_kernel(BwdParams a) {
     const bool w_active = p0 < L;
     const int wp_last = min(p0 + CW - 1, L - 1);
 
-    // block plan as in the forward: summaries [0, s(n_hi)), then the window band
-    const int nsb = (visible_summaries(n_hi, W, C) + kBwdBN - 1) / kBwdBN;
-    const int kb0 = max(0, n0 - W + 1) / kBwdBN;
-    const int nb = nsb + (n_hi / kBwdBN - kb0 + 1);
-    const int ws_hi = w_active ? visible_summaries(wp_last, W, C) : 0;
+    // block plan as in the forward: summaries [0, sum_lo(n_hi)) (non-causal:
+    // all), then the window band [win_lo(n0), win_hi(n_hi)]
+    constexpr bool NC = VAR == kWinNonCausal;
+    const int nsb = ((NC ? a.n_chunks : sum_lo<VAR>(n_hi, W, C)) + kBwdBN - 1) / kBwdBN;
+    const int kb0 = win_lo<VAR>(n0, W, C) / kBwdBN;
+    const int nb = nsb + (win_hi<VAR>(n_hi, W, L) / kBwdBN - kb0 + 1);
+    // what this wave needs: prefix summaries c < ws_hi (all columns: c < ws_lo),
+    // non-causal suffix summaries c >= wsx_lo (all columns: c >= wsx_hi), and
+    // window keys in [wlo_min, whi_max] (all columns: [wlo_max, whi_min])
+    const int ws_hi = w_active ? sum_lo<VAR>(wp_last, W, C) : 0;
+    const int ws_lo = sum_lo<VAR>(p0, W, C);
+    const int wsx_lo = NC ? sum_hi<VAR>(p0, W, C, L) : 0;
+    const int wsx_hi = NC ? sum_hi<VAR>(wp_last, W, C, L) : 0;
+    const int wlo_min = win_lo<VAR>(p0, W, C), wlo_max = win_lo<VAR>(wp_last, W, C);
+    const int whi_min = win_hi<VAR>(p0, W, L), whi_max = win_hi<VAR>(wp_last, W, L);
 
     const bf16* Kbg = static_cast<const bf16*>(a.K) + bg * (size_t)L * D;
     const bf16* Vbg = static_cast<const bf16*>(a.V) + bg * (size_t)L * D;
@@ -210,12 +220,15 @@ void bwd_dq_kernel(BwdParams a) {
     const size_t row0 = (size_t)bh * L;
     bf16x8 qf[NCB][NDC], gf[NCB][NDC];
     float lse2[NCB], dcol[NCB];
-    int col_n[NCB], col_s[NCB];
+    int col_n[NCB], col_s[NCB], col_sx[NCB], col_lo[NCB], col_span[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
         col_n[cb] = p0 + cb * 16 + c16;
         const int n = min(col_n[cb], L - 1);
-        col_s[cb] = visible_summaries(n, W, C);
+        col_s[cb] = sum_lo<VAR>(n, W, C);
+        col_sx[cb] = NC ? sum_hi<VAR>(n, W, C, L) : a.n_chunks;
+        col_lo[cb] = win_lo<VAR>(n, W, C);
+        col_span[cb] = win_hi<VAR>(n, W, L) - col_lo[cb];
         const bf16* qrow = static_cast<const bf16*>(a.Q) + (row0 + n) * D;
         const bf16* grow = static_cast<const bf16*>(a.dO) + (row0 + n) * D;
         const bf16* orow = static_cast<const bf16*>(a.O) + (row0 + n) * D;
@@ -274,8 +287,10 @@ void bwd_dq_kernel(BwdParams a) {
         stage(j + AHEAD);
         const bool sum = j < nsb;
         const int base = sum ? j * kBwdBN : (kb0 + j - nsb) * kBwdBN;
+        const int last = base + kBwdBN - 1;
         const bool needed =
-            w_active && (sum ? base < ws_hi : (base <= wp_last && base + kBwdBN - 1 >= p0 - W + 1));
+            w_active && (sum ? base < ws_hi || (NC && last >= wsx_lo && base < a.n_chunks)
+                             : base <= whi_max && last >= wlo_min);
         if (!needed) return;
         const unsigned char* ks = lds[PH][0];
         const unsigned char* vs = lds[PH][1];
@@ -301,8 +316,8 @@ void bwd_dq_kernel(BwdParams a) {
         // visible to this wave's columns skips the per-element test
         const float bias = sum ? a.log2C : 0.f;
         const bool full = wp_last == p0 + CW - 1 &&
-                          (sum ? base + kBwdBN <= visible_summaries(p0, W, C)
-                               : base + kBwdBN - 1 <= p0 && wp_last - base < W);
+                          (sum ? last < ws_lo || (NC && base >= wsx_hi && last < a.n_chunks)
+                               : base >= wlo_max && last <= whi_min);
         if (full) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
@@ -322,7 +337,9 @@ void bwd_dq_kernel(BwdParams a) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int key = base + kb * 16 + g * 4 + i;
-                        const bool ok = n < L && (sum ? key < col_s[cb] : (unsigned)(n - key) < (unsigned)W);
+                        const bool ok = n < L && (sum ? key < col_s[cb] || (NC && key >= col_sx[cb] &&
+                                                                            key < a.n_chunks)
+                                                      : (unsigned)(key - col_lo[cb]) <= (unsigned)col_span[cb]);
                         const float p = ok ? fast_exp2(fmaf(s[kb][cb][i], a.scale_log2, bias - lse2[cb])) : 0.f;
                         s[kb][cb][i] = p * (dp[kb][cb][i] - dcol[cb]);  // dS^T
                     }
@@ -374,7 +391,29 @@ void bwd_dq_kernel(BwdParams a) {
 // ---------------------------------------------------------------------------
 // dK, dV of window keys and of summaries
 // ---------------------------------------------------------------------------
-template <int D, bool SUM>
+// Rows that see window key m: [kv_rows_lo(m), kv_rows_hi(m)] (the inverse
+// of [win_lo(n), win_hi(n)], both non-decreasing); rows that see summary c
+// from the prefix side: n >= sum_rows_lo(c) (win_lo(n) >= (c + 1) C).
+// Non-causal summaries are also seen by the rows of the blocks wholly before
+// them: their tiles stream every row, masked per element.
+template <int VAR>
+__device__ __forceinline__ int kv_rows_lo(int m, int W) {
+    return VAR == kWinNonCausal ? (m / W) * W : m;
+}
+template <int VAR>
+__device__ __forceinline__ long long kv_rows_hi(int m, int W, int C) {
+    if constexpr (VAR == kWinSliding) return (long long)m + W - 1;
+    if constexpr (VAR == kWinChunkAligned) return ((long long)(m / C) + 1) * C + W - 2;
+    return (long long)(m / W) * W + W - 1;
+}
+template <int VAR>
+__device__ __forceinline__ long long sum_rows_lo(int c, int W, int C) {
+    if constexpr (VAR == kWinSliding || VAR == kWinChunkAligned) return ((long long)c + 1) * C + W - 1;
+    if constexpr (VAR == kWinBlocked) return (((long long)c + 1) * C + W - 1) / W * W;
+    return 0;
+}
+
+template <int D, bool SUM, int VAR>
 __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(3, 3))) void bwd_dkdv_kernel(BwdParams a) {
     typedef BCfg<D> Cfg;
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
@@ -414,19 +453,19 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
         vf[dc] = *reinterpret_cast<const bf16x8*>(Vr + dc * 32 + g * 8);
     }
 
-    // query rows that can see some key of the tile: window keys k are seen by
-    // rows [k, k + W - 1]; summary c by rows n with s(n) > c, i.e.
-    // n >= (c + 1) C + W - 1
+    // query rows that can see some key of the tile (and of this wave's keys
+    // [wk0, wk1]): window key k is seen by rows [kv_rows_lo(k), kv_rows_hi(k)],
+    // summary c by rows from sum_rows_lo(c) on (non-causal: by any row)
+    constexpr bool NC = VAR == kWinNonCausal;
     const int k_last = min(k0 + KT, lim) - 1;
-    const int r_lo = sum ? (int)min((long long)L, (long long)(k0 + 1) * C + W - 1) : k0;
-    const int r_hi = sum ? L - 1 : min(L - 1, k_last + W - 1);
+    const int r_lo = sum ? (int)min((long long)L, sum_rows_lo<VAR>(k0, W, C)) : kv_rows_lo<VAR>(k0, W);
+    const int r_hi = sum ? L - 1 : (int)min((long long)L - 1, kv_rows_hi<VAR>(k_last, W, C));
     const int qb0 = r_lo / kBwdBN;
     const int nqb = r_lo <= r_hi ? r_hi / kBwdBN - qb0 + 1 : 0;
-    // this wave's keys [wk0, wk1]
     const int wk0 = k0 + wave * 16, wk1 = min(wk0 + 15, lim - 1);
     const bool w_active = wk0 < lim;
-    const int wr_lo = sum ? (int)min((long long)L, (long long)(wk0 + 1) * C + W - 1) : wk0;
-    const int wr_hi = sum ? L - 1 : min(L - 1, wk1 + W - 1);
+    const int wr_lo = sum ? (int)min((long long)L, sum_rows_lo<VAR>(wk0, W, C)) : kv_rows_lo<VAR>(wk0, W);
+    const int wr_hi = sum ? L - 1 : (int)min((long long)L - 1, kv_rows_hi<VAR>(wk1, W, C));
 
     floatx4 dk[NDB], dv[NDB];
 #pragma unroll
@@ -503,9 +542,11 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
         floatx4 p[2];
         // a step every pair of which is visible (the wave's 16 keys, the
         // block's 32 rows: most window steps) skips the per-element test
-        const bool full = wk0 + 15 < lim && r0 + kBwdBN - 1 < L &&
-                          (sum ? wk0 + 16 <= visible_summaries(r0, W, C)
-                               : wk0 + 15 <= r0 && r0 + kBwdBN - 1 - wk0 < W);
+        const int r1 = r0 + kBwdBN - 1;
+        const bool full = wk0 + 15 < lim && r1 < L &&
+                          (sum ? wk0 + 16 <= sum_lo<VAR>(r0, W, C) ||
+                                     (NC && wk0 >= sum_hi<VAR>(r1, W, C, L))
+                               : win_lo<VAR>(r1, W, C) <= wk0 && wk0 + 15 <= win_hi<VAR>(r0, W, L));
         if (full) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -520,8 +561,10 @@ __global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int n = r0 + kb * 16 + g * 4 + i;
+                    const int nc = min(n, L - 1);
                     const bool ok = key < lim && n < L &&
-                                    (sum ? key < visible_summaries(n, W, C) : (unsigned)(n - key) < (unsigned)W);
+                                    (sum ? key < sum_lo<VAR>(nc, W, C) || (NC && key >= sum_hi<VAR>(nc, W, C, L))
+                                         : win_lo<VAR>(nc, W, C) <= key && key <= win_hi<VAR>(nc, W, L));
                     p[kb][i] = ok ? fast_exp2(fmaf(s[kb][i], a.scale_log2, bias - lse2[kb][i])) : 0.f;
                     s[kb][i] = p[kb][i] * (dp[kb][i] - dq[kb][i]);  // dS
                 }
@@ -862,20 +905,21 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
 
 }  // namespace
 
-template <int D>
-hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
+template <int D, int VAR>
+hipError_t launch_backward_var(const BwdParams& p, hipStream_t stream) {
     // dQ, and the row dots D = dO . O the dK/dV kernels read
     constexpr int POS = kBwdWaves * 16 * kDqColBlocks;
     const int n_pt = (p.L + POS - 1) / POS;
-    hipLaunchKernelGGL((bwd_dq_kernel<D, kDqColBlocks, kDqNS, kDqWpe>), dim3(p.B * p.H * n_pt), dim3(kBwdWaves * 64),
-                       0, stream, p);
+    hipLaunchKernelGGL((bwd_dq_kernel<D, kDqColBlocks, kDqNS, kDqWpe, VAR>), dim3(p.B * p.H * n_pt),
+                       dim3(kBwdWaves * 64), 0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     constexpr int KT = kBwdWaves * 16;
     if (p.n_chunks > 0) {
         // summary gradients, then their per-chunk and per-key factors
         const int st = (p.n_chunks + KT - 1) / KT * p.n_split;
-        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(p.B * p.Hkv * st), dim3(kBwdWaves * 64), 0, stream, p);
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, true, VAR>), dim3(p.B * p.Hkv * st), dim3(kBwdWaves * 64), 0, stream,
+                           p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         constexpr int RPS = 256 / (D / 8);
         const dim3 grid(p.n_chunks, p.B * p.Hkv);
@@ -892,8 +936,18 @@ hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const int wt = (p.L + KT - 1) / KT;
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(p.B * p.Hkv * wt), dim3(kBwdWaves * 64), 0, stream, p);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, false, VAR>), dim3(p.B * p.Hkv * wt), dim3(kBwdWaves * 64), 0, stream, p);
     return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_backward(const BwdParams& p, hipStream_t stream) {
+    switch (p.window) {
+        case kWinChunkAligned: return launch_backward_var<D, kWinChunkAligned>(p, stream);
+        case kWinBlocked: return launch_backward_var<D, kWinBlocked>(p, stream);
+        case kWinNonCausal: return launch_backward_var<D, kWinNonCausal>(p, stream);
+        default: return launch_backward_var<D, kWinSliding>(p, stream);
+    }
 }
 
 template hipError_t launch_backward<64>(const BwdParams&, hipStream_t);

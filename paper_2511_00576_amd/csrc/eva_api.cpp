@@ -301,12 +301,18 @@ int eva_prefill_attention_ex(const void* Q, const void* K, const void* V, const 
                                   stream);
 }
 
+int eva_prefill_forward_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
+                           float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                           int window, void* stream) {
+    if (!lse) return EVA_ERR_INVALID;
+    if (O_lo && (dtype != EVA_BF16 || !aligned16(O_lo))) return EVA_ERR_INVALID;
+    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, lse, O_lo, B, H, H_kv, L, d, W, C, dtype, window, stream);
+}
+
 int eva_prefill_forward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum, void* O,
                         float* lse, void* O_lo, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
                         void* stream) {
-    if (!lse) return EVA_ERR_INVALID;
-    if (O_lo && (dtype != EVA_BF16 || !aligned16(O_lo))) return EVA_ERR_INVALID;
-    return prefill_attention_impl(Q, K, V, Ksum, Vsum, O, lse, O_lo, B, H, H_kv, L, d, W, C, dtype,
+    return eva_prefill_forward_ex(Q, K, V, Ksum, Vsum, O, lse, O_lo, B, H, H_kv, L, d, W, C, dtype,
                                   EVA_WINDOW_SLIDING, stream);
 }
 
@@ -573,12 +579,12 @@ size_t eva_prefill_backward_workspace_bytes(int B, int H, int H_kv, int L, int d
     return bwd_layout(B, H, H_kv, L, d, C).total;
 }
 
-int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
-                         const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK, void* dV,
-                         void* ws,
-                         size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
-                         void* stream) {
+int eva_prefill_backward_ex(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                            const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK,
+                            void* dV, void* ws, size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C,
+                            int dtype, int window, void* stream) {
     if (B < 1 || H < 1 || H_kv < 1 || L < 1 || W < 1 || C < 1 || H % H_kv != 0) return EVA_ERR_INVALID;
+    if (!valid_window(window)) return EVA_ERR_INVALID;
     if (L > kMaxLen) return EVA_ERR_UNSUPPORTED;
     int st = supported(d, dtype);
     if (st != EVA_OK) return st;
@@ -623,11 +629,20 @@ int eva_prefill_backward(const void* Q, const void* K, const void* V, const void
     p.C = C;
     p.n_chunks = n_chunks;
     p.n_split = eva::bwd_summary_splits(B, H_kv, L, C, H / H_kv);
+    p.window = window;
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
     p.log2C = (float)log2((double)C);
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = d == 64 ? eva::launch_backward<64>(p, s) : eva::launch_backward<128>(p, s);
     return hip_status(e);
+}
+
+int eva_prefill_backward(const void* Q, const void* K, const void* V, const void* Ksum, const void* Vsum,
+                         const void* O, const void* O_lo, const void* dO, const float* lse, void* dQ, void* dK, void* dV,
+                         void* ws, size_t ws_bytes, int B, int H, int H_kv, int L, int d, int W, int C, int dtype,
+                         void* stream) {
+    return eva_prefill_backward_ex(Q, K, V, Ksum, Vsum, O, O_lo, dO, lse, dQ, dK, dV, ws, ws_bytes, B, H, H_kv, L, d,
+                                   W, C, dtype, EVA_WINDOW_SLIDING, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -46,7 +46,7 @@ struct PrefillParams {
 template <int D, typename T>
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
 
-// Backward of the bf16 prefill (sliding window).  Device pointers; the fp32
+// Backward of the bf16 prefill (any window variant).  Device pointers; the fp32
 // scratch (Dv, dK_w, dV_w, dKs_w, dVs_w) comes from the caller's workspace.
 struct BwdParams {
     const void* Q;
@@ -72,6 +72,7 @@ struct BwdParams {
     int n_split;       // query-range splits of each summary-key tile
     float scale_log2;  // log2(e) / sqrt(d)
     float log2C;
+    int window;        // window variant (kWin* in eva_device.hpp)
 };
 
 // Splits of the query range of each summary-key tile of the backward (a

@@ -680,9 +680,13 @@ void launch_prefill_mfma_var(const PrefillParams& p, hipStream_t stream) {
 template <int D>
 hipError_t launch_prefill_mfma(const PrefillParams& p, hipStream_t stream) {
     if (p.O_lo) {
-        // the training forward (sliding window only)
-        if (p.window != kWinSliding) return hipErrorInvalidValue;
-        launch_prefill_mfma_var<D, kWinSliding, true>(p, stream);
+        // the training forward, keeping the output's rounding residual
+        switch (p.window) {
+            case kWinChunkAligned: launch_prefill_mfma_var<D, kWinChunkAligned, true>(p, stream); break;
+            case kWinBlocked: launch_prefill_mfma_var<D, kWinBlocked, true>(p, stream); break;
+            case kWinNonCausal: launch_prefill_mfma_var<D, kWinNonCausal, true>(p, stream); break;
+            default: launch_prefill_mfma_var<D, kWinSliding, true>(p, stream); break;
+        }
         return hipGetLastError();
     }
     switch (p.window) {

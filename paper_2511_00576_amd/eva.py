@@ -388,11 +388,11 @@ def generate(cache: RaggedCache, q, k, v, active=None, out=None, use_workspace=T
     return o
 
 
-def prefill_forward(Q, K, V, W: int, C: int, residual: bool = False):
-    """Training forward (sliding window): summaries, O and the per-row
-    log-sum-exp.  Returns (O, lse, Ks, Vs); lse is fp32 [B, H, L].  With
-    `residual` (bf16) also the output's rounding residual O_lo:
-    (O, lse, Ks, Vs, O_lo)."""
+def prefill_forward(Q, K, V, W: int, C: int, residual: bool = False, window: int = _lib.EVA_WINDOW_SLIDING):
+    """Training forward under window variant `window` (EVA_WINDOW_*):
+    summaries, O and the per-row log-sum-exp.  Returns (O, lse, Ks, Vs); lse
+    is fp32 [B, H, L].  With `residual` (bf16) also the output's rounding
+    residual O_lo: (O, lse, Ks, Vs, O_lo)."""
     _require_device(Q, K, V)
     B, H, L, d = Q.shape
     Hkv = K.shape[1]
@@ -401,19 +401,21 @@ def prefill_forward(Q, K, V, W: int, C: int, residual: bool = False):
     O_lo = torch.empty_like(Q) if residual else None
     lse = torch.empty(B, H, L, dtype=torch.float32, device=Q.device)
     n_chunks = L // C
-    _lib.check("eva_prefill_forward",
-               _lib.load().eva_prefill_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
-                                               _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(lse), _ptr(O_lo), B, H,
-                                               Hkv, L, d, W, C, _dtype_code(Q), _stream()))
+    _lib.check("eva_prefill_forward_ex",
+               _lib.load().eva_prefill_forward_ex(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
+                                                  _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(lse), _ptr(O_lo), B, H,
+                                                  Hkv, L, d, W, C, _dtype_code(Q), window, _stream()))
     if residual:
         return O, lse, Ks, Vs, O_lo
     return O, lse, Ks, Vs
 
 
-def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None, O_lo=None):
+def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None, O_lo=None,
+                     window: int = _lib.EVA_WINDOW_SLIDING):
     """Gradients (dQ, dK, dV) of the EVA prefill for the output gradient dO
-    (bf16, sliding window), from the training forward's O, lse and summaries
-    (and, if it kept one, its output residual O_lo)."""
+    (bf16, window variant `window`), from the training forward's O, lse and
+    summaries under the same variant (and, if it kept one, its output
+    residual O_lo)."""
     _require_device(Q, K, V, O, lse, dO)
     if O_lo is not None:
         _require_device(O_lo)
@@ -432,10 +434,9 @@ def prefill_backward(Q, K, V, Ks, Vs, O, lse, dO, W: int, C: int, workspace=None
     dK = torch.empty_like(K)
     dV = torch.empty_like(V)
     n_chunks = L // C
-    _lib.check("eva_prefill_backward",
-               lib.eva_prefill_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
-                                        _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(O_lo), _ptr(dO), _ptr(lse),
-                                        _ptr(dQ),
-                                        _ptr(dK), _ptr(dV), _ptr(ws), ws.numel() * ws.element_size(), B, H, Hkv, L, d,
-                                        W, C, _dtype_code(Q), _stream()))
+    _lib.check("eva_prefill_backward_ex",
+               lib.eva_prefill_backward_ex(_ptr(Q), _ptr(K), _ptr(V), _ptr(Ks) if n_chunks else None,
+                                           _ptr(Vs) if n_chunks else None, _ptr(O), _ptr(O_lo), _ptr(dO), _ptr(lse),
+                                           _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), ws.numel() * ws.element_size(), B,
+                                           H, Hkv, L, d, W, C, _dtype_code(Q), window, _stream()))
     return dQ, dK, dV

@@ -275,6 +275,16 @@ def test_prefill_rejects_unknown_window(lib, window, code):
     assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 64, 64, 8, 4, 0, window, None) == code
 
 
+@pytest.mark.parametrize("window", [4, -1])
+def test_training_calls_reject_unknown_window(lib, window):
+    f = lib.eva_prefill_forward_ex
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 4, 2, 64, 64, 8, 4, 0, window,
+             None) == _lib.EVA_ERR_INVALID
+    g = lib.eva_prefill_backward_ex
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, 1, 4, 2, 64, 64,
+             8, 4, 0, window, None) == _lib.EVA_ERR_INVALID
+
+
 def test_noncausal_takes_no_cache(lib):
     c = make_cache(window=_lib.EVA_WINDOW_NONCAUSAL)
     assert lib.eva_cache_append(ctypes.byref(c), FAKE, FAKE, None) == _lib.EVA_ERR_INVALID

@@ -1,4 +1,4 @@
-"""GPU parity of the EVA prefill backward (bf16, sliding window) against the
+"""GPU parity of the EVA prefill backward (bf16, every window variant) against the
 fp64 oracle's gradients (themselves pinned by finite differences and by
 autograd of exact attention).
 
@@ -26,16 +26,16 @@ def _gpu():
     eva._lib.load()
 
 
-def run_backward(q, k, v, dO, W, C, residual=True):
+def run_backward(q, k, v, dO, W, C, residual=True, window=oracle.SLIDING):
     """Training forward + backward.  With `residual` the forward keeps its
     output's rounding residual and the backward's row dots D = dO . O are
     exact; without it D comes from the bf16 O."""
     qc, kc, vc, gc = (t.cuda() for t in (q, k, v, dO))
     if residual:
-        O, lse, Ks, Vs, O_lo = eva.prefill_forward(qc, kc, vc, W, C, residual=True)
+        O, lse, Ks, Vs, O_lo = eva.prefill_forward(qc, kc, vc, W, C, residual=True, window=window)
     else:
-        (O, lse, Ks, Vs), O_lo = eva.prefill_forward(qc, kc, vc, W, C), None
-    dQ, dK, dV = eva.prefill_backward(qc, kc, vc, Ks, Vs, O, lse, gc, W, C, O_lo=O_lo)
+        (O, lse, Ks, Vs), O_lo = eva.prefill_forward(qc, kc, vc, W, C, window=window), None
+    dQ, dK, dV = eva.prefill_backward(qc, kc, vc, Ks, Vs, O, lse, gc, W, C, O_lo=O_lo, window=window)
     torch.cuda.synchronize()
     return O, lse, dQ, dK, dV
 
@@ -179,3 +179,55 @@ def test_backward_without_output_residual(shape):
     for g, r, name in ((dQ, rq, "dQ"), (dK, rk, "dK")):
         err = float(np.abs(to64(g) - r).max()) / float(np.abs(r).max())
         assert err <= 2e-2, f"{name}: max abs error {err:.3e} x max |ref| > 2e-2"
+
+
+VARIANTS = [oracle.CHUNK_ALIGNED, oracle.BLOCKED, oracle.NONCAUSAL]
+VARIANT_SHAPES = [
+    # B, H, Hkv, L, d, W, C
+    (1, 4, 2, 400, 128, 7, 4),      # small window and chunk: masks matter
+    (2, 8, 2, 517, 128, 64, 24),    # G = 4, ragged tail; chunk not dividing the window
+    (1, 2, 1, 300, 64, 40, 16),     # d = 64
+    (1, 2, 2, 333, 128, 96, 32),    # blocks of 96 rows (three workgroup tiles of keys)
+    (2, 2, 1, 17, 128, 5, 3),       # shorter than one block
+    (1, 2, 2, 120, 64, 200, 16),    # W >= L: one block, no prefix summaries
+]
+
+
+@pytest.mark.parametrize("window", VARIANTS)
+@pytest.mark.parametrize("shape", VARIANT_SHAPES)
+def test_backward_variants_match_oracle(shape, window):
+    # the window variants of the ablation: each row's window and summaries
+    # move (chunk-aligned start, blocks, whole blocks with summaries on both
+    # sides), so the rows that see a key or a summary are different sets
+    B, H, Hkv, L, d, W, C = shape
+    print(f"backward variant {window} B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C}", flush=True)
+    q, k, v = inputs.qkv(B, H, Hkv, L, d, torch.bfloat16, seed=65)
+    dO = inputs.normal((B, H, L, d), 66, torch.bfloat16)
+    O, lse, dQ, dK, dV = run_backward(q, k, v, dO, W, C, window=window)
+    O_inf = eva.prefill(q.cuda(), k.cuda(), v.cuda(), W, C, window=window)
+    assert torch.equal(O, O_inf)
+    rq, rk, rv = oracle.backward(q, k, v, dO, W, C, variant=window)
+    tq, tk, tv = oracle.backward_terms(q, k, v, dO, W, C, variant=window)
+    errs = [assert_grad_parity(to64(g), r, t, name)
+            for g, r, t, name in ((dQ, rq, tq, "dQ"), (dK, rk, tk, "dK"), (dV, rv, tv, "dV"))]
+    print("row-normwise errors dQ %.2e dK %.2e dV %.2e" % tuple(errs), flush=True)
+
+
+@pytest.mark.parametrize("window", VARIANTS)
+def test_backward_variants_spiked_edges(window):
+    # spikes on the keys that bound the windows and chunks of each variant
+    # (alpha 1.2: a spike takes a part of its rows' weight, so a key counted
+    # by the wrong row set moves dQ, dK and dV by O(1))
+    B, H, Hkv, L, d, W, C = 1, 4, 2, 400, 128, 24, 8
+    anchors = [n for n in range(W, L, 17)] + [L - 1]
+    pos = sorted(set(inputs.window_edge_positions(L, W, C, anchors)) |
+                 {m for m in range(0, L, W)} | {min(L - 1, m + W - 1) for m in range(0, L, W)})
+    print(f"backward variant {window} spikes keys {len(pos)}", flush=True)
+    q, k, v = inputs.spike_at_qkv(B, H, Hkv, L, d, pos, (), C, torch.bfloat16, seed=67, alpha=1.2)
+    dO = inputs.normal((B, H, L, d), 68, torch.bfloat16)
+    _, _, dQ, dK, dV = run_backward(q, k, v, dO, W, C, window=window)
+    rq, rk, rv = oracle.backward(q, k, v, dO, W, C, variant=window)
+    tq, tk, tv = oracle.backward_terms(q, k, v, dO, W, C, variant=window)
+    errs = [assert_grad_parity(to64(g), r, t, name)
+            for g, r, t, name in ((dQ, rq, tq, "dQ"), (dK, rk, tk, "dK"), (dV, rv, tv, "dV"))]
+    print("row-normwise errors dQ %.2e dK %.2e dV %.2e" % tuple(errs), flush=True)
