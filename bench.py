@@ -188,6 +188,9 @@ def main():
     # the GPU reaches its steady clocks only after ~0.1 s of load: 200 warmup
     # steps (about 0.1 s) before the timed ones
     ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--warmup-seconds", type=float, default=WARMUP_S,
+                    help="minimum wall-clock length of the warmup (counter runs, which serialise every "
+                         "dispatch, set 0)")
     ap.add_argument("--decode-iters", type=int, default=64, help="graph-captured decode tokens (x4 caches)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
@@ -263,10 +266,11 @@ def main():
 
     # warm-up: at least --warmup steps and at least WARMUP_S seconds of them
     # (the clocks reach their steady state only after ~0.1 s of load)
-    print(f"# warmup >= {args.warmup} steps and >= {WARMUP_S} s, steps {args.steps}", file=sys.stderr, flush=True)
+    print(f"# warmup >= {args.warmup} steps and >= {args.warmup_seconds} s, steps {args.steps}", file=sys.stderr,
+          flush=True)
     w0 = time.perf_counter()
     n_warm = 0
-    while n_warm < args.warmup or time.perf_counter() - w0 < WARMUP_S:
+    while n_warm < args.warmup or time.perf_counter() - w0 < args.warmup_seconds:
         for _ in range(10):
             step()
         n_warm += 10
