@@ -727,6 +727,8 @@ def bench_generate(args, torch, eva, inputs, dev):
     us_layer_step = ms_gen * 1e3 / (T * n_layers)
     print(f"# generation {us_layer_step:.1f} us per layer-step (fused append + decode), decode alone {us_dec:.1f} us "
           f"({dec_gbs:.0f} GB/s) at the final lengths", file=sys.stderr, flush=True)
+    del caches, outs, graphs
+    scaling = ragged_decode_scaling(torch, eva, gw, kh, vh, Ks, Vs, lens, qn, dev)
     return {
         "workload": gw.name,
         "layers": n_layers,
@@ -740,7 +742,61 @@ def bench_generate(args, torch, eva, inputs, dev):
         "alg_bytes_decode_final": nbytes,
         "alg_flops_decode_final": flops,
         "graph_matches_eager": graph_ok,
+        "decode_batch_scaling": scaling,
     }
+
+
+def ragged_decode_scaling(torch, eva, gw, kh, vh, Ks, Vs, lens, qn, dev):
+    """How much of a small ragged decode launch is fixed cost: the decode
+    kernel on the prompts replicated 1, 2 and 4 times along the batch (about
+    400 MB of caches rotated at every size, beyond the Infinity Cache; one
+    captured graph per size, replayed), and
+    a least-squares fit time = fixed + bytes / bandwidth.  `fixed_share` is
+    the fixed part's share of the 32-sequence launch (ramp-up, the tail of
+    the longest sequences, launch)."""
+    import numpy as np
+    B, H, Hkv, d, W, C = gw.B, gw.H, gw.Hkv, gw.d, gw.W, gw.C
+    rows = []
+    for r in (1, 2, 4):
+        lens_r = lens * r
+        n_caches = 8 // r
+        cat = lambda t: torch.cat([t] * r, dim=0)
+        k_r, v_r, ks_r, vs_r = cat(kh), cat(vh), cat(Ks), cat(Vs)
+        lens_d = torch.tensor(lens_r, dtype=torch.int32, device=dev)
+        q_r = cat(qn)
+        caches = [eva.RaggedCache(B * r, H, Hkv, d, W, C, max_tokens=max(lens) + 1, dtype=gw.dtype, device=dev)
+                  for _ in range(n_caches)]
+        for c in caches:
+            eva.rcache_fill(c, k_r, v_r, ks_r, vs_r, lens_d)
+        del k_r, v_r, ks_r, vs_r
+        out = torch.empty_like(q_r)
+        # one graph per size (eager launches of ~15 us kernels would time the host)
+        g = torch.cuda.CUDAGraph()
+        stream = torch.cuda.Stream()
+        with torch.cuda.graph(g, stream=stream):
+            for c in caches:
+                eva.rdecode_step(c, q_r, out=out)
+        for _ in range(10):
+            g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        reps = 32
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (reps * n_caches)
+        rows.append((B * r, us, generation_counts(lens_r, B * r, H, Hkv, d, W, C, 2)[1]))
+        del caches, out, q_r, g
+    us = np.array([x[1] for x in rows])
+    nb = np.array([x[2] for x in rows], dtype=np.float64)
+    slope, fixed = np.polyfit(nb, us, 1)
+    return {"lengths": "the prompts (1024-3072 tokens)", "batch": [x[0] for x in rows],
+            "us": [float(x) for x in us], "alg_bytes": [int(x) for x in nb],
+            "fixed_us": float(fixed), "asymptotic_gbs": float(1e-3 / slope),
+            "fixed_share": float(fixed / us[0])}
 
 
 if __name__ == "__main__":
