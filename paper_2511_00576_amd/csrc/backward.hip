@@ -683,7 +683,10 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel(BwdParams a) {
         const float* src = (t < D / 4 ? a.dKs_w : a.dVs_w) + (bg * (size_t)a.n_chunks + chunk) * D + (t % (D / 4)) * 4;
         const size_t slot = (size_t)a.B * a.Hkv * a.n_chunks * D;
         floatx4 acc4 = *reinterpret_cast<const floatx4*>(src);
-        for (int sp = 1; sp < a.n_split; ++sp) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
+        // unrolled to the maximum split count so that the loads are in flight together
+#pragma unroll
+        for (int sp = 1; sp < kMaxBwdSplits; ++sp)
+            if (sp < a.n_split) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
         *reinterpret_cast<floatx4*>(gsh + t * 4) = acc4;
     }
     __syncthreads();
@@ -811,7 +814,9 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
         const float* src = (t < D / 4 ? a.dKs_w : a.dVs_w) + (bg * (size_t)a.n_chunks + chunk) * D + (t % (D / 4)) * 4;
         const size_t slot = (size_t)a.B * a.Hkv * a.n_chunks * D;
         floatx4 acc4 = *reinterpret_cast<const floatx4*>(src);
-        for (int sp = 1; sp < a.n_split; ++sp) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
+#pragma unroll
+        for (int sp = 1; sp < kMaxBwdSplits; ++sp)
+            if (sp < a.n_split) acc4 += *reinterpret_cast<const floatx4*>(src + sp * slot);
         *reinterpret_cast<floatx4*>(gsh + t * 4) = acc4;
     }
     // khat = mean key
@@ -903,6 +908,163 @@ __global__ __launch_bounds__(256) void bwd_summary_kernel_reg(BwdParams a) {
     }
 }
 
+// The same per-chunk pass with one wave per chunk: lane (r0, cc) holds
+// features cc*8 .. cc*8+7 of rows r0, r0 + RPS, ... (RPS = 64 / (D / 8)), and
+// every reduction is a cross-lane shuffle (no workgroup barrier), so many
+// chunks' loads are in flight per CU.  The summary gradients are summed over
+// the query-range splits by each lane for its own features.
+template <int D, int ROWS>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(ROWS >= 16 ? 2 : 1))) void bwd_summary_kernel_wave(BwdParams a) {
+    constexpr int TPR = D / 8;
+    constexpr int RPS = 64 / TPR;
+    constexpr int C = ROWS * RPS;
+    const int chunk = blockIdx.x;
+    const size_t bg = blockIdx.y;
+    const int L = a.L;
+    const int t = threadIdx.x, cc = t % TPR, r0 = t / TPR;
+    const int first = chunk * C;
+    const bf16* K = static_cast<const bf16*>(a.K) + (bg * (size_t)L + first + r0) * D + cc * 8;
+    const bf16* V = static_cast<const bf16*>(a.V) + (bg * (size_t)L + first + r0) * D + cc * 8;
+    u32x4 kw[ROWS], vw[ROWS];
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        kw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(K + (size_t)i * RPS * D));
+        vw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(V + (size_t)i * RPS * D));
+    }
+    // summary gradients of this lane's features: sums of the split partials
+    // (at most kMaxBwdSplits); row group r0 loads splits r0, r0 + RPS, ...,
+    // all in flight together, and the row groups' sums are added across lanes
+    float gkh[8], gvh[8];
+    {
+        static_assert(kMaxBwdSplits % RPS == 0, "splits spread evenly over the row groups");
+        const size_t off = (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+        const size_t slot = (size_t)a.B * a.Hkv * a.n_chunks * D;
+        floatx4 k0 = {0.f, 0.f, 0.f, 0.f}, k1 = k0, v0 = k0, v1 = k0;
+#pragma unroll
+        for (int q = 0; q < kMaxBwdSplits / RPS; ++q) {
+            const int sp = r0 + q * RPS;
+            if (sp < a.n_split) {
+                k0 += *reinterpret_cast<const floatx4*>(a.dKs_w + off + sp * slot);
+                k1 += *reinterpret_cast<const floatx4*>(a.dKs_w + off + sp * slot + 4);
+                v0 += *reinterpret_cast<const floatx4*>(a.dVs_w + off + sp * slot);
+                v1 += *reinterpret_cast<const floatx4*>(a.dVs_w + off + sp * slot + 4);
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            gkh[e] = k0[e];
+            gkh[4 + e] = k1[e];
+            gvh[e] = v0[e];
+            gvh[4 + e] = v1[e];
+        }
+    }
+    auto unpack = [](const u32x4& w, float out[8]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            out[2 * e] = bf16_lo(w[e]);
+            out[2 * e + 1] = bf16_hi(w[e]);
+        }
+    };
+    // over the lanes of one row (its TPR feature groups)
+    auto row_sum = [](float x) {
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1) x += __shfl_xor(x, off, 64);
+        return x;
+    };
+    // over the lanes holding the same features (the row groups)
+    auto rows_sum = [](float x) {
+#pragma unroll
+        for (int off = TPR; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
+        return x;
+    };
+    const float sc = a.scale_log2;  // log2(e) / sqrt(d): logits in log2 units
+    const float inv_sqrt_d = sc / kLog2e;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        gkh[e] = rows_sum(gkh[e]);
+        gvh[e] = rows_sum(gvh[e]);
+    }
+    // khat = mean key
+    float kh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] += k[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kh[e] = rows_sum(kh[e]) * (1.f / (float)C);
+    // logits (log2 units) and their max
+    float sl[ROWS];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x += kh[e] * k[e];
+        sl[i] = row_sum(x) * sc;
+        mx = fmaxf(mx, sl[i]);
+    }
+#pragma unroll
+    for (int off = TPR; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    // vhat = sum_j b_j v_j (unnormalized), the denominator, and dvhat . v_j
+    // (V is not needed after this loop)
+    float vh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float psum = 0.f;
+    float yv[ROWS];
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float v[8];
+        unpack(vw[i], v);
+        sl[i] = fast_exp2(sl[i] - mx);
+        psum += sl[i];
+        float y = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            vh[e] += sl[i] * v[e];
+            y += gvh[e] * v[e];
+        }
+        yv[i] = row_sum(y);
+    }
+    const float inv_den = 1.f / rows_sum(psum);
+    // dvhat . vhat
+    float x = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x += gvh[e] * rows_sum(vh[e]) * inv_den;
+    const float gvv = row_sum(x);
+    // b_j, da_j = b_j (dvhat . v_j - dvhat . vhat); dkhat = dK^_c + sum_j da_j k_j / sqrt(d)
+    const size_t kv = bg * (size_t)a.n_chunks * C + first + r0;
+    float dkh[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+        float k[8];
+        unpack(kw[i], k);
+        const float bj = sl[i] * inv_den;
+        const float da = bj * (yv[i] - gvv);
+        if (cc == 0) {
+            a.da_w[kv + (size_t)i * RPS] = da;
+            a.bw_w[kv + (size_t)i * RPS] = bj;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dkh[e] += da * k[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dkh[e] = rows_sum(dkh[e]);
+    if (r0 == 0) {
+        // every lane has read the split partials (slot 0 included) above
+        const size_t cv = (bg * (size_t)a.n_chunks + chunk) * D + cc * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            a.khat_w[cv + e] = kh[e];
+            a.dkhat_w[cv + e] = gkh[e] + dkh[e] * inv_sqrt_d;
+            a.dVs_w[cv + e] = gvh[e];  // the total dvhat, for the window tiles
+        }
+    }
+}
+
 }  // namespace
 
 template <int D, int VAR>
@@ -922,8 +1084,15 @@ hipError_t launch_backward_var(const BwdParams& p, hipStream_t stream) {
                            p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         constexpr int RPS = 256 / (D / 8);
+        constexpr int RPW = 64 / (D / 8);  // rows per sweep of one wave
         const dim3 grid(p.n_chunks, p.B * p.Hkv);
-        switch (p.C % RPS == 0 ? p.C / RPS : 0) {
+        // one wave per chunk when the chunk is 4, 8 or 16 rows per lane
+        const int wrows = p.C % RPW == 0 ? p.C / RPW : 0;
+        if (wrows == 4 || wrows == 8 || wrows == 16) {
+            if (wrows == 4) hipLaunchKernelGGL((bwd_summary_kernel_wave<D, 4>), grid, dim3(64), 0, stream, p);
+            if (wrows == 8) hipLaunchKernelGGL((bwd_summary_kernel_wave<D, 8>), grid, dim3(64), 0, stream, p);
+            if (wrows == 16) hipLaunchKernelGGL((bwd_summary_kernel_wave<D, 16>), grid, dim3(64), 0, stream, p);
+        } else switch (p.C % RPS == 0 ? p.C / RPS : 0) {
             case 1: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 1>), grid, dim3(256), 0, stream, p); break;
             case 2: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 2>), grid, dim3(256), 0, stream, p); break;
             case 4: hipLaunchKernelGGL((bwd_summary_kernel_reg<D, 4>), grid, dim3(256), 0, stream, p); break;

@@ -77,13 +77,14 @@ struct BwdParams {
 
 // Splits of the query range of each summary-key tile of the backward (a
 // function of the shapes only, so that the workspace size can use it).
+constexpr int kMaxBwdSplits = 16;  // query-range splits of a summary tile in the backward
 inline int bwd_summary_splits(long long B, long long Hkv, long long L, long long C, long long G) {
     const long long tiles = B * Hkv * ((L / C + 63) / 64);
     if (tiles <= 0) return 1;
     long long s = (2048 + tiles - 1) / tiles;              // about 2048 workgroups
     const long long by_len = ((L + 31) / 32) * G / 8;      // at least ~8 query blocks each
     if (s > by_len) s = by_len;
-    if (s > 16) s = 16;
+    if (s > kMaxBwdSplits) s = kMaxBwdSplits;
     return s < 1 ? 1 : (int)s;
 }
 

@@ -53,6 +53,10 @@ SHAPES = [
     (1, 4, 2, 400, 128, 96, 64),    # chunk of 4 rows per thread in the per-chunk pass
     (1, 2, 1, 333, 64, 50, 32),     # d = 64, one row per thread in the per-chunk pass
     (1, 2, 2, 260, 128, 32, 16),    # d = 128, one row per thread in the per-chunk pass
+    (1, 2, 1, 400, 64, 80, 64),     # d = 64, one wave per chunk, 8 rows per lane
+    (1, 2, 1, 520, 64, 100, 128),   # d = 64, one wave per chunk, 16 rows per lane
+    (1, 16, 1, 2048, 128, 128, 32), # G = 16: 16 query-range splits of each summary tile
+    (1, 8, 1, 4096, 128, 256, 64),  # 16 splits, one wave per chunk, 16 rows per lane
 ]
 
 
