@@ -233,27 +233,33 @@ def main():
 
     print(f"# prefill workload {w.name}: generating inputs", file=sys.stderr, flush=True)
     q, k, v = (t.to(dev) for t in inputs.workload_qkv(w))
-    Ks = torch.empty(B, Hkv, L // C, d, dtype=w.dtype, device=dev)
-    Vs = torch.empty_like(Ks)
-    O = torch.empty_like(q)
-    cache = eva.Cache(B, H, Hkv, d, W, C, max_tokens=L + 1, dtype=w.dtype, device=dev)
     kn = inputs.normal((B, Hkv, d), w.seed + 100, w.dtype).to(dev)
     vn = inputs.normal((B, Hkv, d), w.seed + 101, w.dtype).to(dev)
     qn = inputs.normal((B, H, d), w.seed + 102, w.dtype).to(dev)
-    od = torch.empty_like(qn)
+    # two buffer sets (inputs, summaries, output, cache), used by turns, so
+    # that no step starts on what the previous one left in the caches
+    sets = []
+    for r in range(2):
+        qq, kk, vv = (q, k, v) if r == 0 else (q.clone(), k.clone(), v.clone())
+        Ks_r = torch.empty(B, Hkv, L // C, d, dtype=w.dtype, device=dev)
+        sets.append({"q": qq, "k": kk, "v": vv, "Ks": Ks_r, "Vs": torch.empty_like(Ks_r), "O": torch.empty_like(qq),
+                     "cache": eva.Cache(B, H, Hkv, d, W, C, max_tokens=L + 1, dtype=w.dtype, device=dev),
+                     "od": torch.empty_like(qn)})
+    Ks, Vs, O = sets[0]["Ks"], sets[0]["Vs"], sets[0]["O"]
 
     # one step: summaries, cache fill (right after the summaries, while the
     # last rows of K and V are still in the caches), the fused attention,
     # then one appended token and a decode step with it (one fused launch)
-    def step(ev=None):
+    def step(i, ev=None):
+        st = sets[i % 2]
         if ev: ev[0].record()
-        eva.build_summaries(k, v, C, out=(Ks, Vs))
+        eva.build_summaries(st["k"], st["v"], C, out=(st["Ks"], st["Vs"]))
         if ev: ev[1].record()
-        eva.cache_fill(cache, k, v, Ks, Vs)
+        eva.cache_fill(st["cache"], st["k"], st["v"], st["Ks"], st["Vs"])
         if ev: ev[2].record()
-        eva.prefill_attention(q, k, v, Ks, Vs, W, C, out=O)
+        eva.prefill_attention(st["q"], st["k"], st["v"], st["Ks"], st["Vs"], W, C, out=st["O"])
         if ev: ev[3].record()
-        eva.append_decode(cache, qn, kn, vn, out=od)
+        eva.append_decode(st["cache"], qn, kn, vn, out=st["od"])
         if ev: ev[4].record()
 
     if args.copy_calibration:
@@ -271,8 +277,8 @@ def main():
     w0 = time.perf_counter()
     n_warm = 0
     while n_warm < args.warmup or time.perf_counter() - w0 < args.warmup_seconds:
-        for _ in range(10):
-            step()
+        for i in range(10):
+            step(i)
         n_warm += 10
         torch.cuda.synchronize()
     warm_s = time.perf_counter() - w0
@@ -283,13 +289,13 @@ def main():
     torch.cuda.synchronize()
     t0.record()
     for i in range(args.steps):
-        step()
+        step(i)
     t1.record()
     torch.cuda.synchronize()
     ms_step = t0.elapsed_time(t1) / args.steps
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     for i in range(args.steps):
-        step(evs[i])
+        step(i, evs[i])
     torch.cuda.synchronize()
 
     def avg(i, j):
@@ -389,7 +395,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic N(0,1), seeded",
         "config": {"workload": w.name, "B": B, "H": H, "H_kv": Hkv, "L": L, "d": d, "W": W, "C": C,
-                   "step": "summaries + cache fill + fused prefill + fused append/decode"},
+                   "step": "summaries + cache fill + fused prefill + fused append/decode",
+                   "buffer_sets": 2},
         "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": attn_gbs / PEAK_HBM_GBS,
                      "traffic": traffic,
@@ -404,7 +411,7 @@ def main():
                     "cache_fill_ms": ms_fill, "append_decode_ms": ms_app_dec,
                     "alg_flops": flops, "alg_bytes_attention": attn_bytes, "alg_bytes_summaries": summ_bytes},
     }
-    del q, k, v, O, Ks, Vs, cache
+    del q, k, v, O, Ks, Vs, sets
 
     if not args.no_other_prefill:
         out["prefill_workloads"] = bench_other_prefill(args, torch, eva, inputs, dev)
@@ -425,7 +432,7 @@ def prefill_only_workload(name, inputs):
     if name.startswith("long"):
         c = int(name[4:])
         return dataclasses.replace(lw, C=c, name=lw.name.replace("C256", f"C{c}"))
-    return {"llm": inputs.LLM_BF16, "gqa": inputs.GQA_BF16}[name]
+    return {"llm": inputs.LLM_BF16, "gqa": inputs.GQA_BF16, "kbench": inputs.KBENCH_BF16}[name]
 
 
 def bench_prefill_only(args, torch, eva, inputs, dev):
@@ -455,12 +462,13 @@ def bench_prefill_only(args, torch, eva, inputs, dev):
                       "prefill_source_sha": source_sha(PREFILL_SOURCES)}), flush=True)
 
 
-PREFILL_ONLY = ("llm", "gqa", "long64", "long128", "long256")
+PREFILL_ONLY = ("llm", "gqa", "long64", "long128", "long256", "kbench")
 
 
 def bench_other_prefill(args, torch, eva, inputs, dev):
-    """The GQA workload and the long-context workload at C = 64, 128, 256
-    (fixed W = 1024): fused attention time, algorithmic TFLOP/s against the
+    """The GQA workload, the long-context workload at C = 64, 128, 256
+    (fixed W = 1024) and a workload shaped like the paper's kernel benchmark
+    (B8 L16384 W256 C128): fused attention time, algorithmic TFLOP/s against the
     bf16 MFMA peak, and the summaries' time.  For the C sweep also the
     approximation side of the trade-off: on sampled rows, the relative
     distance of the EVA output from exact causal softmax attention over the
@@ -471,6 +479,7 @@ def bench_other_prefill(args, torch, eva, inputs, dev):
     lw = inputs.LONG_BF16
     cases = [(inputs.GQA_BF16, False)]
     cases += [(dataclasses.replace(lw, C=c, name=lw.name.replace("C256", f"C{c}")), True) for c in (64, 128, 256)]
+    cases += [(inputs.KBENCH_BF16, False)]
     cached = {}
     for wk, sample in cases:
         print(f"# prefill workload {wk.name}", file=sys.stderr, flush=True)

@@ -32,6 +32,10 @@ LLM_BF16 = Workload("llm-bf16 B8 H32 L4096 d128 W256 C64", 8, 32, 32, 4096, 128,
 GQA_BF16 = Workload("gqa-bf16 B4 H32/8 L8192 d128 W512 C128", 4, 32, 8, 8192, 128, 512, 128, torch.bfloat16, 3)
 LONG_BF16 = Workload("long-bf16 B1 H32/8 L32768 d128 W1024 C256", 1, 32, 8, 32768, 128, 1024, 256,
                      torch.bfloat16, 5)
+# shaped like the paper's kernel benchmark (section "FlashEVA Attention
+# speedup": window 256, 128-token chunks, 16k tokens at batch 8)
+KBENCH_BF16 = Workload("kbench-bf16 B8 H32 L16384 d128 W256 C128", 8, 32, 32, 16384, 128, 256, 128,
+                       torch.bfloat16, 7)
 
 
 @dataclass(frozen=True)
