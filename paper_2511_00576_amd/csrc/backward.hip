@@ -46,11 +46,12 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdBN = 32;     // rows per streamed block
-// dQ: 16 query columns per wave (126 VGPRs), a three-stage ring (50 KB):
-// three workgroups per CU.  Measured on MI355X (LLM workload): 537 us, vs 568
-// with 32 columns at two waves per SIMD and 634 with 32 columns and four
-// stages.
-constexpr int kDqColBlocks = 1, kDqNS = 3, kDqWpe = 3;
+// dQ: 16 query columns per wave (122 VGPRs), a two-stage ring (33 KB): four
+// workgroups per CU.  Measured on MI355X: the dQ kernel 588 us against 640
+// with three stages at three workgroups per CU (LLM and GQA workloads
+// averaged); earlier, 537 us (LLM) with three stages vs 568 with 32 columns
+// at two waves per SIMD and 634 with 32 columns and four stages.
+constexpr int kDqColBlocks = 1, kDqNS = 2, kDqWpe = 4;
 // dK/dV: LDS ring stages and blocks requested ahead of the one computed.
 // It fits 168 VGPRs, so three stages (50 KB) let three workgroups share a CU
 // (measured on MI355X: 631 vs 767 us for the window tiles of the LLM workload)
@@ -174,7 +175,7 @@ void bwd_dq_kernel(BwdParams a) {
     constexpr int NDC = Cfg::NDC, NDB = Cfg::NDB, BLK = Cfg::BLK;
     constexpr int CW = 16 * NCB;       // query columns per wave
     constexpr int AHEAD = NS - 1;      // blocks requested ahead of the one computed
-    static_assert(NS == 3, "the block loop below takes three steps per trip");
+    static_assert(NS == 2 || NS == 3, "the block loop below takes NS steps per trip");
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NS][2][BLK];  // [stage][K, V]
     __shared__ __attribute__((aligned(1024))) unsigned char dummy[1024];
 
@@ -361,13 +362,21 @@ void bwd_dq_kernel(BwdParams a) {
     typedef std::integral_constant<int, 1> P1;
     typedef std::integral_constant<int, 2> P2;
     int j = 0;
-    for (; j + 2 < nb; j += 3) {
-        block_step(P0{}, j);
-        block_step(P1{}, j + 1);
-        block_step(P2{}, j + 2);
+    if constexpr (NS == 3) {
+        for (; j + 2 < nb; j += 3) {
+            block_step(P0{}, j);
+            block_step(P1{}, j + 1);
+            block_step(P2{}, j + 2);
+        }
+        if (j < nb) block_step(P0{}, j);
+        if (j + 1 < nb) block_step(P1{}, j + 1);
+    } else {
+        for (; j + 1 < nb; j += 2) {
+            block_step(P0{}, j);
+            block_step(P1{}, j + 1);
+        }
+        if (j < nb) block_step(P0{}, j);
     }
-    if (j < nb) block_step(P0{}, j);
-    if (j + 1 < nb) block_step(P1{}, j + 1);
 
     bwait_vm<0>();  // no request may still be writing LDS when the workgroup ends
 
