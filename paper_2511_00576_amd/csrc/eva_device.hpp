@@ -74,15 +74,6 @@ __device__ __forceinline__ float xgroup_sum(float x) {
     return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
 }
 
-// Butterfly reductions inside 16-lane rows (DPP-friendly xor distances).
-__device__ __forceinline__ float row16_sum(float x) {
-    x += __shfl_xor(x, 1, 64);
-    x += __shfl_xor(x, 2, 64);
-    x += __shfl_xor(x, 4, 64);
-    x += __shfl_xor(x, 8, 64);
-    return x;
-}
-
 // LDS transposing read: each lane of a 16-lane group passes the address of 4
 // consecutive 16-bit elements; lanes 4j..4j+3 together name row j (16
 // elements).  Lane i of the group receives element i of rows 0..3.
@@ -145,11 +136,6 @@ __device__ __forceinline__ void rf_normals4(unsigned long long seed, uint32_t i,
         out[2 * h] = r * cs;
         out[2 * h + 1] = r * sn;
     }
-}
-
-__device__ __forceinline__ int visible_summaries(int n, int W, int C) {
-    int start = n - W + 1;
-    return start > 0 ? start / C : 0;
 }
 
 // Window variants (values of the ABI's eva_window).  Row n attends the exact

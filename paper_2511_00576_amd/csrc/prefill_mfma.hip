@@ -87,15 +87,6 @@ __device__ __forceinline__ void mwait_vm_lgkm0() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
 
-// One global_load_lds_dwordx4 (lane i: 16 B from base + voff to LDS M0 + 16 i),
-// as inline asm so the compiler does not drain every outstanding DMA before
-// each later LDS read; the kernel waits for exactly the block it needs.
-__device__ __forceinline__ void mlds_dma16(const void* base, unsigned voff, const void* lds_dst) {
-    const unsigned m0 =
-        __builtin_amdgcn_readfirstlane((unsigned)(size_t)(__attribute__((address_space(3))) const void*)lds_dst);
-    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(m0) : "memory");
-}
-
 // Lower-edge state of a 16 x 16 tile whose row offset (query - key at lane
 // offset zero) is c, a multiple of 16: 0 all valid, 1 none, 2 diagonal.
 __device__ __forceinline__ int lower_state(int c) { return c >= 16 ? 0 : (c < 0 ? 1 : 2); }
