@@ -208,7 +208,7 @@ def test_prefill_variant_full_size_sampled(variant, w):
         assert_parity(to64(O[b, h, torch.from_numpy(rows)]), ref, w.dtype, f"{w.name} variant {variant} b{b} h{h}")
 
 
-FULL = [inputs.LLM_BF16, inputs.GQA_BF16, inputs.LONG_BF16]
+FULL = [inputs.LLM_BF16, inputs.GQA_BF16, inputs.LONG_BF16, inputs.KBENCH_BF16]
 
 
 @pytest.mark.parametrize("w", FULL, ids=lambda w: w.name.split()[0])
