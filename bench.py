@@ -209,6 +209,9 @@ def main():
     ap.add_argument("--prefill-only", choices=sorted(PREFILL_ONLY),
                     help="profiling mode: only this prefill workload's summaries and fused attention "
                          "(--warmup launches, then --steps timed launches); prints its own JSON line")
+    ap.add_argument("--backward-only", choices=("llm", "gqa"),
+                    help="profiling mode: the training forward of this workload once, then --warmup and "
+                         "--steps backward calls (dQ, dK, dV); prints its own JSON line")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -226,6 +229,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.prefill_only:
         bench_prefill_only(args, torch, eva, inputs, dev)
+        return
+    if args.backward_only:
+        bench_backward_only(args, torch, eva, inputs, dev)
         return
     w = inputs.LLM_BF16
     B, H, Hkv, L, d, W, C = w.B, w.H, w.Hkv, w.L, w.d, w.W, w.C
@@ -463,6 +469,37 @@ def bench_prefill_only(args, torch, eva, inputs, dev):
 
 
 PREFILL_ONLY = ("llm", "gqa", "long64", "long128", "long256", "kbench")
+
+
+def bench_backward_only(args, torch, eva, inputs, dev):
+    """One workload's backward alone (for per-kernel profiles): the training
+    forward with the output residual once, then --warmup and --steps
+    backward calls into one workspace."""
+    wk = {"llm": inputs.LLM_BF16, "gqa": inputs.GQA_BF16}[args.backward_only]
+    print(f"# backward-only {wk.name}", file=sys.stderr, flush=True)
+    q, k, v = (t.to(dev) for t in inputs.workload_qkv(wk))
+    dO = inputs.normal((wk.B, wk.H, wk.L, wk.d), wk.seed + 7, wk.dtype).to(dev)
+    O, lse, Ks, Vs, O_lo = eva.prefill_forward(q, k, v, wk.W, wk.C, residual=True)
+    lib = eva._lib.load()
+    ws = torch.empty((lib.eva_prefill_backward_workspace_bytes(wk.B, wk.H, wk.Hkv, wk.L, wk.d, wk.C) + 3) // 4,
+                     dtype=torch.float32, device=dev)
+    run = lambda: eva.prefill_backward(q, k, v, Ks, Vs, O, lse, dO, wk.W, wk.C, workspace=ws, O_lo=O_lo)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    a0 = torch.cuda.Event(enable_timing=True)
+    a1 = torch.cuda.Event(enable_timing=True)
+    n = max(args.steps, 1)
+    a0.record()
+    for _ in range(n):
+        run()
+    a1.record()
+    torch.cuda.synchronize()
+    ms = a0.elapsed_time(a1) / n
+    flops = wk.B * wk.H * 10 * wk.d * attended(wk.L, wk.W, wk.C)
+    tf = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({"backward_only": wk.name, "calls": args.warmup + n, "backward_ms": ms, "alg_flops": flops,
+                      "tflops": tf, "mfma_frac": tf / PEAK_BF16_TFLOPS}), flush=True)
 
 
 def bench_other_prefill(args, torch, eva, inputs, dev):
