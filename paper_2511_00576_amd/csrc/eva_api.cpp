@@ -331,7 +331,7 @@ static int prefill_attention_impl(const void* Q, const void* K, const void* V, c
     if (any_summary(window, L, W, C) && (!Ksum || !Vsum || !aligned16(Ksum) || !aligned16(Vsum)))
         return EVA_ERR_INVALID;
 
-    eva::PrefillParams p;
+    eva::PrefillParams p{};
     p.Q = Q;
     p.K = K;
     p.V = V;
@@ -601,7 +601,7 @@ int eva_prefill_backward_ex(const void* Q, const void* K, const void* V, const v
     const BwdLayout lay = bwd_layout(B, H, H_kv, L, d, C);
     if (ws_bytes < lay.total) return EVA_ERR_CAPACITY;
     char* w = static_cast<char*>(ws);
-    eva::BwdParams p;
+    eva::BwdParams p{};
     p.Q = Q;
     p.K = K;
     p.V = V;
