@@ -644,8 +644,8 @@ void eva_ref_backward_terms_variant(const double* Q, const double* K, const doub
                 }
                 o[e] = acc;
             }
-            double D = 0.0;
-            for (int e = 0; e < d; ++e) D += g[e] * o[e];
+            double Dabs = 0.0;
+            for (int e = 0; e < d; ++e) Dabs += fabs(g[e] * o[e]);
             for (int e = 0; e < d; ++e) tq[e] = 0.0;
             for (long i = 0; i < count; ++i) {
                 const int win = i < n_win;
@@ -653,9 +653,11 @@ void eva_ref_backward_terms_variant(const double* Q, const double* K, const doub
                 const double* val = win ? V + (size_t)(lo + i) * d : Vs + (size_t)sidx[i - n_win] * d;
                 double* tkey = win ? Tk + (size_t)(lo + i) * d : Tks + (size_t)sidx[i - n_win] * d;
                 double* tval = win ? Tv + (size_t)(lo + i) * d : Tvs + (size_t)sidx[i - n_win] * d;
-                double gv = 0.0;
-                for (int e = 0; e < d; ++e) gv += g[e] * val[e];
-                const double dl = fabs(p[i] * (gv - D));
+                double gva = 0.0;
+                for (int e = 0; e < d; ++e) gva += fabs(g[e] * val[e]);
+                /* the logit gradient p_i (dO.v_i - D), D = dO.o, is a sum of
+                 * the terms of both dot products */
+                const double dl = p[i] * (gva + Dabs);
                 for (int e = 0; e < d; ++e) {
                     tq[e] += dl * fabs(key[e]) * inv_sqrt_d;
                     tkey[e] += dl * fabs(q[e]) * inv_sqrt_d;

@@ -543,16 +543,42 @@ def test_backward_terms_exact_without_cancellation():
     R = np.abs(rand((B, H, L, d), 97)) + 0.1
     np.testing.assert_allclose(oracle.backward_terms(q, k, v, R, W, C)[2], oracle.backward(q, k, v, R, W, C)[2],
                                rtol=1e-12, atol=0)
-    # dQ: with a two-token window and no chunk, row n's gradient is
-    # dl (k_{n-1} - k_n) / sqrt(d) (its two logit gradients cancel); keys of
-    # alternating sign make |k_{n-1} - k_n| = |k_{n-1}| + |k_n| entry by entry
+    # dQ: with a two-token window, no chunk, zero queries (both weights 1/2)
+    # and values +-a of alternating sign, every row n >= 1 has output 0, so
+    # D = 0 and its gradient is (dO.v_n / 2) (k_n - k_{n-1}) / sqrt(d); a
+    # positive dO makes |dO.v_n| = sum_e |dO_e v_e| and keys of alternating
+    # sign make |k_n - k_{n-1}| = |k_n| + |k_{n-1}| entry by entry, so no term
+    # cancels
     L = 12
-    q, v = rand((B, H, L, d), 98), rand((B, Hkv, L, d), 99)
+    q = np.zeros((B, H, L, d))
+    v = np.abs(rand((B, Hkv, L, d), 99)[:, :, :1]) + 0.1 + np.zeros((B, Hkv, L, d))
+    v[:, :, 1::2] *= -1
     k = np.abs(rand((B, Hkv, L, d), 100)) + 0.1
     k[:, :, 1::2] *= -1
-    R = rand((B, H, L, d), 101)
-    np.testing.assert_allclose(oracle.backward_terms(q, k, v, R, 2, L + 1)[0],
-                               np.abs(oracle.backward(q, k, v, R, 2, L + 1)[0]), rtol=1e-12, atol=1e-15)
+    R = np.abs(rand((B, H, L, d), 101)) + 0.1
+    tq = oracle.backward_terms(q, k, v, R, 2, L + 1)[0]
+    dq = oracle.backward(q, k, v, R, 2, L + 1)[0]
+    np.testing.assert_allclose(tq[:, :, 1:], np.abs(dq[:, :, 1:]), rtol=1e-12, atol=1e-15)
+
+
+def test_backward_terms_single_token_window():
+    # W = 1 and no chunk: every row attends only itself (weight 1), so
+    # D = dO.v_n, the logit gradient dO.v_n - D is exactly 0 and so are dQ and
+    # dK, while each of its two dot products has term magnitude
+    # m = sum_e |dO_e v_e|: T_q = 2 m |k_n| / sqrt(d), T_k = 2 m |q_n| / sqrt(d)
+    # (one query head per key here), and T_v = |dO_n| = dV
+    B, H, Hkv, L, d = 1, 1, 1, 9, 5
+    q, k, v = rand((B, H, L, d), 130), rand((B, Hkv, L, d), 131), rand((B, Hkv, L, d), 132)
+    R = rand((B, H, L, d), 133)
+    dq, dk, dv = oracle.backward(q, k, v, R, 1, L + 1)
+    tq, tk, tv = oracle.backward_terms(q, k, v, R, 1, L + 1)
+    gv = np.abs(R * v).sum(-1, keepdims=True)
+    np.testing.assert_allclose(dq, 0.0, atol=1e-14)
+    np.testing.assert_allclose(dk, 0.0, atol=1e-14)
+    np.testing.assert_allclose(tq, 2 * gv * np.abs(k) / np.sqrt(d), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(tk, 2 * gv * np.abs(q) / np.sqrt(d), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(tv, np.abs(R), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(dv, R, rtol=1e-12, atol=1e-15)
 
 
 def test_backward_terms_scale_with_the_output_gradient():
