@@ -158,8 +158,8 @@ def test_prefill_with_rf_summaries():
 VARIANTS = [oracle.CHUNK_ALIGNED, oracle.BLOCKED, oracle.NONCAUSAL]
 VARIANT_SHAPES = [
     # B, H, Hkv, L, d, W, C
-    (1, 2, 2, 300, 64, 40, 16),     # G = 1: 4-wave configuration
-    (2, 8, 2, 517, 128, 64, 24),    # G = 4: 8-wave configuration, ragged tail
+    (1, 2, 2, 300, 64, 40, 16),     # G = 1: one head per workgroup tile
+    (2, 8, 2, 517, 128, 64, 24),    # G = 4: four heads per tile, ragged tail
     (1, 4, 4, 700, 128, 100, 7),    # odd chunk, window not a multiple of 16
     (1, 2, 1, 250, 128, 1, 5),      # W = 1
     (1, 2, 2, 120, 64, 200, 16),    # W >= L
