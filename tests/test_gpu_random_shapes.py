@@ -2,7 +2,9 @@
 shapes of the other tests pin each boundary on purpose; these spread over
 the space of (B, G, H_kv, L, d, W, C, window variant, dtype) so that a
 combination nobody thought of is still compared element by element with the
-fp64 oracle.  Every case is deterministic (its seed is its index)."""
+fp64 oracle: the prefill, its backward, and decode after a prefill (prompt
+length, steps, fused or separate append, NaN-filled caches).  Every case is
+deterministic (its seed is its index)."""
 import numpy as np
 import pytest
 import torch
@@ -83,3 +85,36 @@ def test_backward_random_shape(i):
     tq, tk, tv = oracle.backward_terms(q, k, v, dO, W, C, variant=var)
     for g, rf, t, name in ((dQ, rq, tq, "dQ"), (dK, rk, tk, "dK"), (dV, rv, tv, "dV")):
         assert_grad_parity(to64(g), rf, t, f"case {i} {name}")
+
+
+CAUSAL = (oracle.SLIDING, oracle.CHUNK_ALIGNED, oracle.BLOCKED)
+
+
+def decode_case(i):
+    r = np.random.RandomState(6000 + i)
+    Hkv = int(r.choice([1, 2]))
+    G = int(r.choice([1, 2, 4, 8]))
+    B = int(r.choice([1, 2, 3]))
+    d = int(r.choice([64, 128]))
+    W = int(r.choice([1, 2, 7, 16, 33, 100, 256]))
+    C = int(r.choice([1, 3, 4, 16, 24, 64]))
+    L0 = int(r.randint(0, 401))
+    steps = int(r.randint(1, 41))
+    var = CAUSAL[int(r.randint(0, 3))]
+    fused = bool(r.randint(0, 2))
+    fill = float("nan") if r.randint(0, 2) else None
+    dtype = torch.float32 if i % 4 == 3 else torch.bfloat16
+    return B, G * Hkv, Hkv, d, W, C, L0, steps, var, fused, fill, dtype
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_decode_random_shape(i):
+    # prefill of L0 tokens into a cache (none when L0 = 0), then `steps`
+    # appended tokens, each decoded and compared with the oracle's row of
+    # the whole sequence; caches filled with NaN must not leak stale slots
+    from test_gpu_decode import run_sequence
+
+    B, H, Hkv, d, W, C, L0, steps, var, fused, fill, dtype = decode_case(i)
+    print(f"random decode {i}", flush=True)
+    run_sequence(B, H, Hkv, d, W, C, L0=L0, steps=steps, seed=7000 + i, fill=fill, fused=fused, window=var,
+                 dtype=dtype, check_every=max(1, steps // 8))
