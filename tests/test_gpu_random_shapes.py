@@ -2,9 +2,10 @@
 shapes of the other tests pin each boundary on purpose; these spread over
 the space of (B, G, H_kv, L, d, W, C, window variant, dtype) so that a
 combination nobody thought of is still compared element by element with the
-fp64 oracle: the prefill, its backward, and decode after a prefill (prompt
-length, steps, fused or separate append, NaN-filled caches).  Every case is
-deterministic (its seed is its index)."""
+fp64 oracle: the prefill, its backward, decode after a prefill (prompt
+length, steps, fused or separate append, NaN-filled caches), and ragged
+generation (per-sequence prompt lengths, active masks, caches that fill
+up).  Every case is deterministic (its seed is its index)."""
 import numpy as np
 import pytest
 import torch
@@ -118,3 +119,36 @@ def test_decode_random_shape(i):
     print(f"random decode {i}", flush=True)
     run_sequence(B, H, Hkv, d, W, C, L0=L0, steps=steps, seed=7000 + i, fill=fill, fused=fused, window=var,
                  dtype=dtype, check_every=max(1, steps // 8))
+
+
+def ragged_case(i):
+    r = np.random.RandomState(8000 + i)
+    Hkv = int(r.choice([1, 2]))
+    G = int(r.choice([1, 2, 4]))
+    B = int(r.randint(1, 6))
+    d = int(r.choice([64, 128]))
+    W = int(r.choice([1, 5, 16, 48, 100]))
+    C = int(r.choice([1, 4, 8, 16, 32]))
+    lens = [int(x) for x in r.randint(0, 301, size=B)]
+    steps = int(r.randint(1, 41))
+    var = CAUSAL[int(r.randint(0, 3))]
+    fused = bool(r.randint(0, 2))
+    use_ws = bool(r.randint(0, 2))
+    fill = float("nan") if r.randint(0, 2) else None
+    dtype = torch.float32 if i % 4 == 3 else torch.bfloat16
+    # some caches hold fewer tokens than the sequences reach: full
+    # sequences stop growing and keep decoding their last position
+    max_tokens = max(lens) + steps - (int(r.randint(0, 20)) if i % 3 == 0 else 0)
+    active = r.rand(steps, B) < 0.75  # seeded active masks
+    return B, G * Hkv, Hkv, d, W, C, lens, steps, var, fused, use_ws, fill, dtype, max(max_tokens, 1), active
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_ragged_random_shape(i):
+    from test_gpu_generate import run_steps
+
+    B, H, Hkv, d, W, C, lens, steps, var, fused, use_ws, fill, dtype, max_tokens, active = ragged_case(i)
+    print(f"random ragged {i} max_tokens={max_tokens}", flush=True)
+    run_steps(B, H, Hkv, d, W, C, lens=lens, steps=steps, seed=9000 + i, fill=fill,
+              active_fn=lambda t, b: active[t, b], use_ws=use_ws, max_tokens=max_tokens,
+              check_every=max(1, steps // 8), fused=fused, window=var, dtype=dtype)
