@@ -3,9 +3,10 @@ shapes of the other tests pin each boundary on purpose; these spread over
 the space of (B, G, H_kv, L, d, W, C, window variant, dtype) so that a
 combination nobody thought of is still compared element by element with the
 fp64 oracle: the prefill, its backward, decode after a prefill (prompt
-length, steps, fused or separate append, NaN-filled caches), and ragged
+length, steps, fused or separate append, NaN-filled caches), ragged
 generation (per-sequence prompt lengths, active masks, caches that fill
-up).  Every case is deterministic (its seed is its index)."""
+up), and stochastic summaries with the prefill over them.  Every case is
+deterministic (its seed is its index)."""
 import numpy as np
 import pytest
 import torch
@@ -152,3 +153,43 @@ def test_ragged_random_shape(i):
     run_steps(B, H, Hkv, d, W, C, lens=lens, steps=steps, seed=9000 + i, fill=fill,
               active_fn=lambda t, b: active[t, b], use_ws=use_ws, max_tokens=max_tokens,
               check_every=max(1, steps // 8), fused=fused, window=var, dtype=dtype)
+
+
+def rf_case(i):
+    r = np.random.RandomState(10000 + i)
+    Hkv = int(r.choice([1, 2]))
+    G = int(r.choice([1, 2, 4, 8]))
+    B = int(r.choice([1, 2]))
+    d = int(r.choice([64, 128]))
+    C = int(r.choice([1, 4, 16, 24, 64]))
+    L = int(r.randint(2 * C, 2 * C + 500))
+    W = int(r.choice([1, 7, 32, 100, 257]))
+    var = VARIANTS[int(r.randint(0, 4))]
+    lam = float(r.choice([0.0, 0.05, 0.1, 0.5]))
+    dtype = torch.float32 if i % 3 == 2 else torch.bfloat16
+    return B, G * Hkv, Hkv, L, d, W, C, var, lam, dtype
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_prefill_rf_random_shape(i):
+    # stochastic summaries (draws passed in) and the fused prefill over them,
+    # every output element against the oracle's rows over its own summaries
+    B, H, Hkv, L, d, W, C, var, lam, dtype = rf_case(i)
+    print(f"random rf prefill {i}: B{B} H{H}/{Hkv} L{L} d{d} W{W} C{C} window {var} lam {lam} {dtype}", flush=True)
+    q, k, v = inputs.qkv(B, H, Hkv, L, d, dtype, seed=11000 + i)
+    eps = inputs.normal((B, Hkv, L // C, d), 12000 + i)
+    qc, kc, vc = q.cuda(), k.cuda(), v.cuda()
+    Ks, Vs = eva.build_summaries_rf(kc, vc, eps.cuda(), C, lam=lam)
+    O = eva.prefill_attention(qc, kc, vc, Ks, Vs, W, C, window=var)
+    torch.cuda.synchronize()
+    rows = np.arange(L, dtype=np.int64)
+    G = H // Hkv
+    for b in range(B):
+        for g in range(Hkv):
+            rK, rV = oracle.summaries_rf(k[b, g], v[b, g], eps[b, g], C, lam=lam)
+            assert_parity(to64(Ks[b, g]), rK, dtype, f"case {i} Ksum b{b} g{g}")
+            assert_parity(to64(Vs[b, g]), rV, dtype, f"case {i} Vsum b{b} g{g}")
+            for h in range(g * G, (g + 1) * G):
+                ref = oracle.attend_rows_variant(to64(q[b, h]), rows, to64(k[b, g]), to64(v[b, g]), rK, rV, W, C,
+                                                 var)
+                assert_parity(to64(O[b, h]), ref, dtype, f"case {i} b{b} h{h}")
